@@ -1,0 +1,184 @@
+"""Oracle for the two-step-draft-then-verify loop (Section 2.1, Eq. 1-3).
+
+State of one sequence: a committed KV cache holding tokens t_0..t_{L-1} and
+a *pending* token t_L that is known but not yet cached.
+
+One loop (greedy, Section 2.1.1):
+
+* Draft step 1 (Eq. 1): run the block [t_L, a_1, ..., a_k] at positions
+  L..L+k.  Row 0 gives the exact next token t_{L+1}; row j (j >= 1, an
+  adaptive token) gives the draft d_j for position L+1+j.  Only row 0 is
+  committed (the adaptive rows' K/V are discarded).
+* Draft step 2 (Eq. 2): with L advanced by one, run [t_L, d_1, ..., d_k] at
+  positions L..L+k.  Row j gives o_j, the target's token after the first j
+  drafts.
+* Verification (Eq. 3): draft d_j is accepted while every earlier draft was
+  accepted and d_j equals o_{j-1} (the "stop cur loop" branch ends the
+  loop at the first mismatch, so acceptance is a prefix).  With m accepted
+  drafts the loop emits o_0..o_m and commits block rows 0..m; the pending
+  token becomes o_m.
+
+So a loop costs two block forwards and emits m + 2 tokens, 2 <= m + 2 <= k + 2
+(the bound stated after Eq. 3), and the emitted sequence equals plain greedy
+decoding (stated at the end of Section 2.1.1).
+
+Nucleus variant (Section 2.1.2), chain form: the exact tokens are sampled
+instead of arg-maxed, each with the uniform keyed by its own absolute
+position, and drafts are the arg-max of the adaptive rows (one branch of the
+paper's draft tree).  Verification keeps the longest prefix of drafts that
+the sampled outputs confirm, as in the greedy rule.  Because the token at
+position i is always Sample(p(. | t_<i), U(seed, b, i)), the output equals
+plain autoregressive nucleus sampling with the same uniforms.
+
+Start-up (the paper leaves it open): the prompt's first P-1 tokens are
+committed by a prefill and the last prompt token is the first pending token.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import model as M
+from . import sampling as S
+
+
+def verify_greedy(logits: np.ndarray, drafts=None):
+    """Eq. 3 on one block.  Returns (o [q] int, m).
+
+    o_j is the arg-max of row j (lowest id among ties).  With drafts
+    d_1..d_{q-1} (the block's rows 1..q-1), m is the number of leading j with
+    d_j == o_{j-1}.  Without drafts (draft step 1) m is 0.
+    """
+    o = np.array([S.argmax_lowest(r) for r in np.asarray(logits, np.float32)], np.int64)
+    if drafts is None:
+        return o, 0
+    m = 0
+    for j in range(1, o.shape[0]):
+        if int(drafts[j - 1]) != int(o[j - 1]):
+            break
+        m = j
+    return o, m
+
+
+def verify_nucleus(logits: np.ndarray, drafts, temperature, top_p, top_k, seed, b, pos0):
+    """Nucleus counterpart of ``verify_greedy``.  Returns (tokens [q], m, margin).
+
+    With drafts: s_j = Sample(row j, U(seed, b, pos0 + j)) for every row and m
+    counts leading matches d_j == s_{j-1}.  Without drafts (draft step 1):
+    row 0 is sampled with U(seed, b, pos0), rows 1.. are arg-maxed (the chain
+    of most probable drafts), and m is 0.  ``pos0`` is the absolute position
+    of the token sampled from row 0.  ``margin`` is the smallest rounding
+    margin of any sample taken.
+    """
+    lg = np.asarray(logits, np.float32)
+    q = lg.shape[0]
+    out = np.zeros(q, np.int64)
+    margin = np.inf
+    for j in range(q):
+        if drafts is None and j > 0:
+            out[j] = S.argmax_lowest(lg[j])
+            continue
+        tok, mg = S.sample(lg[j], temperature, top_p, top_k, S.uniform(seed, b, pos0 + j))
+        out[j] = tok
+        margin = min(margin, mg)
+    if drafts is None:
+        return out, 0, margin
+    m = 0
+    for j in range(1, q):
+        if int(drafts[j - 1]) != int(out[j - 1]):
+            break
+        m = j
+    return out, m, margin
+
+
+@dataclass
+class Trace:
+    """Every block the loop ran: tokens, positions, cache length, logits."""
+    blocks: list = field(default_factory=list)
+    loop_m: list = field(default_factory=list)
+    margins: list = field(default_factory=list)
+
+
+def _block(shape, weights, cache, tokens, bf16, per_row, trace):
+    L = cache.length
+    pos = np.arange(L, L + len(tokens))
+    logits, kv = M.forward_block(shape, weights, cache, tokens, pos, bf16=bf16, per_row=per_row)
+    if trace is not None:
+        trace.blocks.append({"tokens": np.asarray(tokens, np.int64), "cache_len": L,
+                             "logits": logits.astype(np.float32) if bf16 else logits})
+    return logits, kv
+
+
+def generate_sdsat(shape, weights, prompt, k, max_new, adaptive, mode="greedy",
+                   temperature=1.0, top_p=1.0, top_k=0, seed=0, b=0,
+                   bf16=False, per_row=False, force_drafts=None, trace=None):
+    """SDSAT generation of ``max_new`` tokens for one sequence.
+
+    ``force_drafts(n, k)``, if given, replaces the drafts of draft step 1 by
+    the tokens it returns for output positions n..n+k-1 (used to force the
+    all-accept and all-reject bounds).  Returns (tokens, per-loop m list).
+    """
+    prompt = np.asarray(prompt, np.int64)
+    adaptive = [int(a) for a in adaptive[:k]]
+    cache = M.prefill(shape, weights, prompt[:-1], bf16=bf16, per_row=per_row)
+    pending = int(prompt[-1])
+    out: list[int] = []
+    ms: list[int] = []
+    greedy = mode == "greedy" or temperature <= 0.0
+    while len(out) < max_new:
+        # draft step 1: [pending, a_1..a_k]
+        L = cache.length
+        logits, kv = _block(shape, weights, cache, [pending] + adaptive, bf16, per_row, trace)
+        if greedy:
+            d1, _ = verify_greedy(logits, None)
+        else:
+            d1, _, mg = verify_nucleus(logits, None, temperature, top_p, top_k, seed, b, L + 1)
+            if trace is not None:
+                trace.margins.append(mg)
+        t1 = int(d1[0])
+        drafts = [int(x) for x in d1[1:]]
+        cache.commit(kv, [0])
+        out.append(t1)
+        if force_drafts is not None:
+            drafts = [int(x) for x in force_drafts(len(out), k)]
+        # draft step 2: [t1, d_1..d_k]
+        L = cache.length
+        logits, kv = _block(shape, weights, cache, [t1] + drafts, bf16, per_row, trace)
+        if greedy:
+            o, m = verify_greedy(logits, drafts)
+        else:
+            o, m, mg = verify_nucleus(logits, drafts, temperature, top_p, top_k, seed, b, L + 1)
+            if trace is not None:
+                trace.margins.append(mg)
+        cache.commit(kv, range(m + 1))
+        out.extend(int(x) for x in o[: m + 1])
+        pending = int(o[m])
+        ms.append(m)
+    if trace is not None:
+        trace.loop_m = ms
+    return out[:max_new], ms
+
+
+def generate_ar(shape, weights, prompt, max_new, mode="greedy", temperature=1.0, top_p=1.0,
+                top_k=0, seed=0, b=0, bf16=False, per_row=False, trace=None):
+    """Plain autoregressive decoding, one token per block forward."""
+    prompt = np.asarray(prompt, np.int64)
+    cache = M.prefill(shape, weights, prompt[:-1], bf16=bf16, per_row=per_row)
+    pending = int(prompt[-1])
+    out: list[int] = []
+    greedy = mode == "greedy" or temperature <= 0.0
+    while len(out) < max_new:
+        L = cache.length
+        logits, kv = _block(shape, weights, cache, [pending], bf16, per_row, trace)
+        if greedy:
+            t = S.argmax_lowest(logits[0].astype(np.float32))
+        else:
+            t, mg = S.sample(logits[0].astype(np.float32), temperature, top_p, top_k,
+                             S.uniform(seed, b, L + 1))
+            if trace is not None:
+                trace.margins.append(mg)
+        cache.commit(kv, [0])
+        out.append(int(t))
+        pending = int(t)
+    return out

@@ -1,0 +1,263 @@
+"""Pins for the oracle's draft / verify / commit loop and sampler (CPU only).
+
+What the paper fixes (Section 2.1): greedy two-step-draft-then-verify emits
+exactly the greedy tokens; a loop runs two block forwards and emits between
+2 and k+2 tokens; Eq. 3 accepts a prefix of the drafts.  What mathematics
+fixes: the sampler's output distribution is the renormalised top-p set,
+which is checked here against the classic sorted-cumulative definition, and
+the keyed uniforms are SplitMix64's published outputs.
+"""
+import json
+import math
+import os
+from types import SimpleNamespace
+
+import numpy as np
+import pytest
+
+from oracle import decode as D
+from oracle import model as M
+from oracle import sampling as S
+from paper_2403_18647_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _model(name="tiny", **kw):
+    wl = synth.workload(name, **kw)
+    W = {n: synth.tensor(wl, n) for n in synth.tensor_names(wl.shape)}
+    return wl, M.Weights(wl.shape, W)
+
+
+# ---------------------------------------------------------------- Eq. 3 worked cases
+def _one_hot_logits(targets, V=16):
+    lg = np.full((len(targets), V), -1.0, np.float32)
+    for r, t in enumerate(targets):
+        lg[r, t] = 1.0
+    return lg
+
+
+def test_eq3_worked_cases_golden():
+    cases = json.load(open(os.path.join(GOLDEN, "eq3_cases.json")))["cases"]
+    for c in cases:
+        lg = _one_hot_logits(c["targets"])
+        o, m = D.verify_greedy(lg, c["drafts"])
+        assert m == c["m"], c["note"]
+        assert list(o[: m + 1]) == c["emit"], c["note"]
+        assert m + 2 <= c["k"] + 2
+
+
+def test_argmax_ties_take_lowest_id():
+    lg = np.zeros((1, 10), np.float32)
+    lg[0, [3, 7]] = 5.0
+    o, _ = D.verify_greedy(lg, None)
+    assert o[0] == 3
+
+
+# ---------------------------------------------------------------- greedy equivalence and bounds
+@pytest.mark.parametrize("k,identical,gain_std", [(5, False, 0.0), (3, False, 0.1), (1, True, 0.1),
+                                                   (5, True, 0.0)])
+def test_sdsat_greedy_equals_ar_greedy_bitwise(k, identical, gain_std):
+    """Section 2.1.1: greedy SDSAT output is exactly the plain greedy output."""
+    wl, w = _model(gain_std=gain_std)
+    sh = wl.shape
+    pr = synth.prompts(wl)[0]
+    ad = synth.adaptive_ids(sh, k, identical=identical)
+    tr = D.Trace()
+    out, ms = D.generate_sdsat(sh, w, pr, k, wl.max_new, ad, per_row=True, trace=tr)
+    ref = D.generate_ar(sh, w, pr, wl.max_new, per_row=True)
+    assert out == ref
+    # loop accounting (the bound after Eq. 3): two blocks per loop, 2..k+2 tokens per loop
+    assert len(tr.blocks) == 2 * len(ms)
+    assert all(0 <= m <= k for m in ms)
+    assert sum(m + 2 for m in ms) >= wl.max_new > sum(m + 2 for m in ms[:-1])
+
+
+def test_k0_is_plain_decoding_two_blocks_per_loop():
+    wl, w = _model()
+    sh = wl.shape
+    pr = synth.prompts(wl)[0]
+    tr = D.Trace()
+    out, ms = D.generate_sdsat(sh, w, pr, 0, 20, [], per_row=True, trace=tr)
+    assert out == D.generate_ar(sh, w, pr, 20, per_row=True)
+    assert ms == [0] * 10 and len(tr.blocks) == 20
+    assert all(len(b["tokens"]) == 1 for b in tr.blocks)
+
+
+def test_forced_perfect_drafts_accept_all_and_forced_wrong_drafts_reject_all():
+    wl, w = _model()
+    sh = wl.shape
+    pr = synth.prompts(wl)[0]
+    k, n = 5, 60
+    ref = D.generate_ar(sh, w, pr, n + k + 2, per_row=True)
+
+    def perfect(pos, kk):
+        return ref[pos:pos + kk]
+
+    def wrong(pos, kk):
+        return [(t + 1) % sh.vocab for t in ref[pos:pos + kk]]
+
+    out, ms = D.generate_sdsat(sh, w, pr, k, n, synth.adaptive_ids(sh, k), per_row=True,
+                               force_drafts=perfect)
+    assert out == ref[:n] and all(m == k for m in ms)
+    assert len(ms) == math.ceil(n / (k + 2))
+    out, ms = D.generate_sdsat(sh, w, pr, k, n, synth.adaptive_ids(sh, k), per_row=True,
+                               force_drafts=wrong)
+    assert out == ref[:n] and all(m == 0 for m in ms)
+
+
+def test_bf16_mode_greedy_equivalence_holds_too():
+    """The equivalence is a property of the loop, not of the arithmetic: per-row
+    bf16-rounded forwards give the same identity."""
+    wl, w = _model(gain_std=0.1)
+    sh = wl.shape
+    pr = synth.prompts(wl)[0]
+    out, _ = D.generate_sdsat(sh, w, pr, 4, 24, synth.adaptive_ids(sh, 4), bf16=True, per_row=True)
+    assert out == D.generate_ar(sh, w, pr, 24, bf16=True, per_row=True)
+
+
+def test_batch_sequences_are_independent():
+    wl, w = _model()
+    sh = wl.shape
+    prs = synth.prompts(wl, batch=2)
+    a, _ = D.generate_sdsat(sh, w, prs[1], 3, 12, synth.adaptive_ids(sh, 3), per_row=True)
+    assert a == D.generate_ar(sh, w, prs[1], 12, per_row=True)
+
+
+# ---------------------------------------------------------------- RNG
+def test_splitmix64_published_vectors():
+    vec = json.load(open(os.path.join(GOLDEN, "splitmix64_vectors.json")))["vectors"]
+    for seed, outs in vec.items():
+        for n, h in enumerate(outs, start=1):
+            assert S.splitmix64(int(seed), n) == int(h, 16)
+
+
+def test_uniform_keyed_stream_is_uniform():
+    u = np.array([S.uniform(3, b, p) for b in range(4) for p in range(25000)])
+    assert u.min() >= 0.0 and u.max() < 1.0
+    counts, _ = np.histogram(u, bins=50, range=(0, 1))
+    chi2 = ((counts - len(u) / 50) ** 2 / (len(u) / 50)).sum()
+    assert chi2 < 95.0          # df=49, p ~ 1e-4
+    assert S.uniform(3, 0, 7) != S.uniform(3, 1, 7) != S.uniform(4, 0, 7)
+
+
+# ---------------------------------------------------------------- sampler
+def _classic_top_p(logits, T, p, top_k=0):
+    """Sort descending and keep the shortest prefix whose mass reaches p (tie-free logits)."""
+    z = np.asarray(logits, np.float32).astype(np.float64) / float(np.float32(T))
+    order = np.argsort(-z, kind="stable")
+    if top_k:
+        order = order[:top_k]
+    pr = np.exp(z[order] - z[order].max())
+    pr /= pr.sum()
+    n = int(np.searchsorted(np.cumsum(pr), float(np.float32(p)) - 1e-15) + 1)
+    keep = order[:n]
+    q = np.zeros(len(z))
+    q[keep] = pr[:n] / pr[:n].sum()
+    return q
+
+
+def _interval_freqs(logits, T, p, top_k, n=40001):
+    us = (np.arange(n) + 0.5) / n
+    toks = [S.sample(logits, T, p, top_k, u)[0] for u in us]
+    return np.bincount(toks, minlength=len(logits)) / n
+
+
+@pytest.mark.parametrize("T,p,top_k", [(1.0, 0.9, 0), (0.8, 0.95, 0), (0.5, 0.5, 0), (1.0, 1.0, 0),
+                                       (1.0, 0.95, 3), (2.0, 0.99, 5)])
+def test_sampler_matches_classic_top_p(T, p, top_k):
+    rng = np.random.default_rng(11)
+    logits = (rng.standard_normal(12) * 2.0).astype(np.float32)
+    want = _classic_top_p(logits, T, p, top_k)
+    got = _interval_freqs(logits, T, p, top_k)
+    np.testing.assert_allclose(got, want, atol=5e-5)
+
+
+def test_sampler_reductions():
+    rng = np.random.default_rng(12)
+    lg = rng.standard_normal(20).astype(np.float32)
+    am = int(np.argmax(lg))
+    for u in (0.0, 0.3, 0.999):
+        assert S.sample(lg, 1e-3, 0.95, 0, u)[0] == am      # T -> 0
+        assert S.sample(lg, 1.0, 1e-6, 0, u)[0] == am      # p -> 0
+        assert S.sample(lg, 0.0, 0.95, 0, u)[0] == am      # T = 0: greedy
+        assert S.sample(lg, 1.0, 0.95, 1, u)[0] == am      # top_k = 1
+    # p = 1, no top-k: the full softmax
+    sm = np.exp(lg.astype(np.float64) - lg.max())
+    np.testing.assert_allclose(_interval_freqs(lg, 1.0, 1.0, 0), sm / sm.sum(), atol=5e-5)
+
+
+def test_sampler_ties_at_threshold_are_all_kept():
+    lg = np.array([3.0, 1.0, 1.0, 1.0, -5.0], np.float32)
+    ids, _, _ = S.nucleus_set(lg, 1.0, 0.5)       # mass of the top id alone < 0.5
+    e3 = math.exp(3.0)
+    assert e3 / (e3 + 3 * math.e + math.exp(-5)) < 0.9
+    ids, _, _ = S.nucleus_set(lg, 1.0, 0.9)
+    assert list(ids) == [0, 1, 2, 3]
+
+
+# ---------------------------------------------------------------- nucleus SDSAT
+def _peaked_tiny():
+    sh = synth.small_shape(n_layers=2, d_model=64, n_heads=2, head_dim=32, d_ffn=128,
+                           vocab=8, n_adaptive=5)
+    wl = synth.Workload("chi", sh, seed=21, batch=1, k=2, prompt_len=6, max_new=3,
+                        mode="nucleus", temperature=1.0, top_p=0.9, weight_std=0.3)
+    W = {n: synth.tensor(wl, n) for n in synth.tensor_names(sh)}
+    return wl, M.Weights(sh, W)
+
+
+@pytest.mark.parametrize("T,p,top_k", [(0.8, 0.95, 0), (1.0, 0.9, 10), (0.2, 0.95, 10)])
+def test_sdsat_nucleus_equals_ar_nucleus_tokenwise(T, p, top_k):
+    """Position-keyed uniforms make the chain-form SDSAT nucleus loop emit the AR nucleus sequence."""
+    wl, w = _model(weight_std=0.08)
+    sh = wl.shape
+    pr = synth.prompts(wl)[0]
+    for b in range(3):
+        tr = D.Trace()
+        out, ms = D.generate_sdsat(sh, w, pr, 4, 30, synth.adaptive_ids(sh, 4), mode="nucleus",
+                                   temperature=T, top_p=p, top_k=top_k, seed=99, b=b,
+                                   per_row=True, trace=tr)
+        ref = D.generate_ar(sh, w, pr, 30, mode="nucleus", temperature=T, top_p=p, top_k=top_k,
+                            seed=99, b=b, per_row=True)
+        assert out == ref
+        assert min(tr.margins) > 1e-12
+
+
+def test_nucleus_sdsat_preserves_top_p_joint_distribution():
+    """Chi-square of the first two tokens over many keyed streams against exact
+    enumeration of the AR nucleus distribution (classic top-p definition)."""
+    wl, w = _peaked_tiny()
+    sh = wl.shape
+    pr = synth.prompts(wl)[0]
+    T, p = wl.temperature, wl.top_p
+    # exact joint of the first two tokens
+    cache = M.prefill(sh, w, pr[:-1])
+    lg0, kv = M.forward_block(sh, w, cache, [pr[-1]], [len(pr) - 1])
+    p1 = _classic_top_p(lg0[0].astype(np.float32), T, p)
+    c1 = cache.copy()
+    c1.commit(kv, [0])
+    joint = np.zeros((sh.vocab, sh.vocab))
+    for t1 in range(sh.vocab):
+        if p1[t1] == 0:
+            continue
+        lg1, _ = M.forward_block(sh, w, c1, [t1], [len(pr)])
+        joint[t1] = p1[t1] * _classic_top_p(lg1[0].astype(np.float32), T, p)
+    assert 3 <= np.count_nonzero(joint) < sh.vocab ** 2   # top-p truncates, and is not degenerate
+    n = 3000
+    counts = np.zeros_like(joint)
+    for b in range(n):
+        out, _ = D.generate_sdsat(sh, w, pr, wl.k, 2, synth.adaptive_ids(sh, wl.k), mode="nucleus",
+                                  temperature=T, top_p=p, seed=wl.seed, b=b)
+        counts[out[0], out[1]] += 1
+    assert counts[joint == 0].sum() == 0                   # nothing outside the nucleus
+    exp = joint.reshape(-1) * n
+    obs = counts.reshape(-1)
+    big = exp >= 5
+    chi2 = ((obs[big] - exp[big]) ** 2 / exp[big]).sum()
+    rest_e, rest_o = exp[~big & (exp > 0)].sum(), obs[~big & (exp > 0)].sum()
+    dof = int(big.sum()) - 1
+    if rest_e > 0:
+        chi2 += (rest_o - rest_e) ** 2 / rest_e
+        dof += 1
+    # generous bound: chi2 < dof + 5 sqrt(2 dof)
+    assert chi2 < dof + 5 * math.sqrt(2 * dof), (chi2, dof)
