@@ -158,7 +158,7 @@ def _linear(x: np.ndarray, w: np.ndarray, per_row: bool) -> np.ndarray:
     return x @ w.T
 
 
-def _attention(qh, kh, vh, ck, cv, vis, scale, per_row):
+def attention(qh, kh, vh, ck, cv, vis, scale, per_row=False):
     """softmax(q k^T * scale) v over the committed cache plus the visible block rows.
 
     qh, kh, vh: [q, H, Dh] block rows; ck, cv: [L, H, Dh] committed rows.
@@ -228,7 +228,7 @@ def forward_block(shape, weights: Weights, cache: KVCache, tokens, positions,
         kh = rnd(apply_rope(kh, cos, sin))
         vh = rnd(vh)
         block_kv.append((kh, vh))
-        o = _attention(qh, kh, vh, cache.k[layer], cache.v[layer], vis, scale, per_row)
+        o = attention(qh, kh, vh, cache.k[layer], cache.v[layer], vis, scale, per_row)
         o = rnd(o.reshape(q, d))
         x = x + _linear(o, weights[p + "wo"], per_row)
         h2 = rnd(rms_norm(x, weights[p + "ffn_norm"], eps))

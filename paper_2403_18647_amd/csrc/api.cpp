@@ -1,0 +1,759 @@
+// Host runtime of the SDSAT block-decode library: context, workspace layout,
+// weight packing, block forward, verification, KV commit and the draft/verify
+// generation loop (Section 2.1).  Declared in include/sdsat.h.
+#include <hip/hip_runtime.h>
+
+#include <chrono>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/sdsat.h"
+#include "kernels.h"
+
+using namespace sdsat;
+
+namespace {
+
+thread_local std::string g_init_error = "no error";
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Bump allocator over the caller's workspace; with base == 0 it only measures.
+struct Carver {
+    char* base;
+    size_t off = 0;
+    explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+    void* take(size_t bytes) {
+        off = align_up(off, 256);
+        void* p = base ? base + off : nullptr;
+        off += bytes;
+        return p;
+    }
+};
+
+struct Dims {
+    int L, d, H, Dh, F, V, A, esz, dtype;
+    int S;           // KV slots per sequence (max_ctx rounded up to 32)
+    int maxB, maxQ, maxM;
+    int ks_d, ks_f;  // k-steps for K = d and K = F
+    int nt_qkv, nt_o, nt_gu, nt_down, nt_lm;
+    int n_ssq;       // d / 16
+};
+
+int make_dims(const sdsat_config* c, Dims* D, std::string* why) {
+    if (!c) { *why = "config is NULL"; return SDSAT_EINVAL; }
+    if (c->n_layers < 1 || c->d_model < 16 || c->n_heads < 1 || c->d_ffn < 8 || c->vocab < 2 ||
+        c->n_adaptive < 0 || c->max_batch < 1 || c->max_ctx < 1 || c->max_block < 1) {
+        *why = "config has a non-positive dimension";
+        return SDSAT_EINVAL;
+    }
+    if (c->head_dim != 64 && c->head_dim != 128) { *why = "head_dim must be 64 or 128"; return SDSAT_EUNSUPPORTED; }
+    if (c->n_heads * c->head_dim != c->d_model) { *why = "d_model must equal n_heads * head_dim"; return SDSAT_EINVAL; }
+    if (c->d_model % 16) { *why = "d_model must be a multiple of 16"; return SDSAT_EUNSUPPORTED; }
+    if (c->dtype != SDSAT_DTYPE_FP32 && c->dtype != SDSAT_DTYPE_BF16) { *why = "dtype must be 0 or 1"; return SDSAT_EINVAL; }
+    if (c->max_block > 64) { *why = "max_block must be <= 64"; return SDSAT_EUNSUPPORTED; }
+    if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) { *why = "rms_eps must be >= 0 and rope_base > 0"; return SDSAT_EINVAL; }
+    D->L = c->n_layers; D->d = c->d_model; D->H = c->n_heads; D->Dh = c->head_dim; D->F = c->d_ffn;
+    D->V = c->vocab; D->A = c->n_adaptive; D->dtype = c->dtype; D->esz = c->dtype == SDSAT_DTYPE_BF16 ? 2 : 4;
+    D->S = (int)align_up((size_t)c->max_ctx, 32);
+    D->maxB = c->max_batch; D->maxQ = c->max_block;
+    D->maxM = c->max_batch * c->max_block < 64 ? c->max_batch * c->max_block : 64;
+    D->ks_d = (D->d + 31) / 32; D->ks_f = (D->F + 31) / 32;
+    D->nt_qkv = 3 * D->d / 16; D->nt_o = D->d / 16; D->nt_gu = (D->F + 7) / 8; D->nt_down = D->d / 16;
+    D->nt_lm = (D->V + 15) / 16;
+    D->n_ssq = D->d / 16;
+    return SDSAT_OK;
+}
+
+enum ProfKind { PK_OFF = 0, PK_GATEUP = 1, PK_QKV = 2, PK_ATTN = 3, PK_DOWN = 4, PK_O = 5, PK_LM = 6, PK_BLOCK = 7 };
+
+}  // namespace
+
+struct sdsat_ctx {
+    sdsat_config cfg;
+    Dims D;
+    hipStream_t stream = nullptr;
+    std::string err = "no error";
+    int device = 0;
+    // caller weights
+    const void* embed = nullptr;
+    std::vector<const float*> attn_norm, ffn_norm;
+    const float* final_norm = nullptr;
+    // packed weights
+    std::vector<void*> w_qkv, w_o, w_gu, w_down;
+    void* w_lm = nullptr;
+    // cache
+    void* kc = nullptr; void* vc = nullptr;
+    size_t layer_elems = 0;   // elements per layer of K (and of V)
+    float* rope_cos = nullptr; float* rope_sin = nullptr;
+    // activations
+    float* x = nullptr; float* ssq = nullptr;
+    void* qbuf = nullptr; void* obuf = nullptr; void* ubuf = nullptr;
+    // scratch
+    float* gemm_part = nullptr; int* gemm_cnt = nullptr;
+    float* attn_part = nullptr; int* attn_cnt = nullptr;
+    int* cache_len = nullptr; int* err_flag = nullptr; int* verify_cnt = nullptr;
+    // generation buffers
+    int *tok1 = nullptr, *out1 = nullptr, *out2 = nullptr, *n_accept = nullptr, *pending = nullptr;
+    int *active = nullptr, *n_commit = nullptr, *pos0 = nullptr, *adaptive = nullptr, *ptok = nullptr;
+    float* logits = nullptr;
+    int* h_pin = nullptr;   // pinned host staging
+    size_t h_pin_ints = 0;
+    // upper bounds of cache_len, tracked on the host for launch planning
+    std::vector<int> len_hint;
+    // profiling
+    int prof_kind = PK_OFF;
+    std::vector<hipEvent_t> events;
+    size_t ev_used = 0;
+};
+
+namespace {
+
+int fail(sdsat_ctx* c, int code, const std::string& msg) {
+    if (c) c->err = msg; else g_init_error = msg;
+    return code;
+}
+
+#define HIPCHK(ctx, expr)                                                                   \
+    do {                                                                                    \
+        hipError_t e_ = (expr);                                                             \
+        if (e_ != hipSuccess)                                                               \
+            return fail((ctx), SDSAT_EDEVICE, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+// Carve every device buffer of a context (ctx may be a measuring dummy).
+void carve(sdsat_ctx* c, Carver& cv) {
+    const Dims& D = c->D;
+    const size_t e = D.esz;
+    c->w_qkv.resize(D.L); c->w_o.resize(D.L); c->w_gu.resize(D.L); c->w_down.resize(D.L);
+    for (int l = 0; l < D.L; ++l) {
+        c->w_qkv[l] = cv.take(packed_elems(D.nt_qkv, D.ks_d) * e);
+        c->w_o[l] = cv.take(packed_elems(D.nt_o, D.ks_d) * e);
+        c->w_gu[l] = cv.take(packed_elems(D.nt_gu, D.ks_d) * e);
+        c->w_down[l] = cv.take(packed_elems(D.nt_down, D.ks_f) * e);
+    }
+    c->w_lm = cv.take(packed_elems(D.nt_lm, D.ks_d) * e);
+    c->layer_elems = (size_t)D.maxB * D.H * D.S * D.Dh;
+    c->kc = cv.take(c->layer_elems * D.L * e);
+    c->vc = cv.take(c->layer_elems * D.L * e);
+    c->rope_cos = (float*)cv.take((size_t)D.S * (D.Dh / 2) * 4);
+    c->rope_sin = (float*)cv.take((size_t)D.S * (D.Dh / 2) * 4);
+    c->x = (float*)cv.take((size_t)D.maxM * D.d * 4);
+    c->ssq = (float*)cv.take((size_t)D.maxM * D.n_ssq * 4);
+    c->qbuf = cv.take((size_t)D.maxB * D.maxQ * D.d * e);
+    c->obuf = cv.take((size_t)D.maxM * D.d * e);
+    c->ubuf = cv.take((size_t)D.maxM * D.F * e);
+    // split-K scratch: the largest need over the five GEMMs at any M <= maxM
+    size_t part = 0;
+    int groups = 0;
+    for (int M = 1; M <= D.maxM; ++M) {
+        const int nts[5] = {D.nt_qkv, D.nt_o, D.nt_gu, D.nt_down, D.nt_lm};
+        const int kss[5] = {D.ks_d, D.ks_d, D.ks_d, D.ks_f, D.ks_d};
+        for (int i = 0; i < 5; ++i) {
+            const GemmPlan p = plan_gemm(D.dtype, M, nts[i], kss[i]);
+            const size_t f = gemm_partial_floats(p, nts[i]);
+            if (f > part) part = f;
+            if (gemm_groups(nts[i]) > groups) groups = gemm_groups(nts[i]);
+        }
+    }
+    c->gemm_part = (float*)cv.take(part * 4);
+    c->gemm_cnt = (int*)cv.take((size_t)groups * 4);
+    c->attn_part = (float*)cv.take(attention_partial_floats(D.maxB, D.H, D.maxQ, D.Dh) * 4);
+    c->attn_cnt = (int*)cv.take((size_t)D.maxB * D.H * 4);
+    c->cache_len = (int*)cv.take((size_t)D.maxB * 4);
+    c->err_flag = (int*)cv.take(4);
+    c->verify_cnt = (int*)cv.take((size_t)D.maxB * 4);
+    const size_t bq = (size_t)D.maxB * D.maxQ;
+    c->tok1 = (int*)cv.take(bq * 4);
+    c->out1 = (int*)cv.take(bq * 4);
+    c->out2 = (int*)cv.take(bq * 4);
+    c->ptok = (int*)cv.take(bq * 4);
+    c->n_accept = (int*)cv.take((size_t)D.maxB * 4);
+    c->pending = (int*)cv.take((size_t)D.maxB * 4);
+    c->active = (int*)cv.take((size_t)D.maxB * 4);
+    c->n_commit = (int*)cv.take((size_t)D.maxB * 4);
+    c->pos0 = (int*)cv.take((size_t)D.maxB * 4);
+    c->adaptive = (int*)cv.take(64 * 4);
+    c->logits = (float*)cv.take(bq * D.V * 4);
+}
+
+void* layer_k(sdsat_ctx* c, int l) { return (char*)c->kc + (size_t)l * c->layer_elems * c->D.esz; }
+void* layer_v(sdsat_ctx* c, int l) { return (char*)c->vc + (size_t)l * c->layer_elems * c->D.esz; }
+
+// ---------------------------------------------------------------- profiling
+void prof_begin(sdsat_ctx* c, int kind, hipEvent_t* out) {
+    *out = nullptr;
+    if (c->prof_kind != kind) return;
+    if (c->ev_used + 2 > c->events.size()) {
+        for (int i = 0; i < 64; ++i) {
+            hipEvent_t ev;
+            if (hipEventCreate(&ev) != hipSuccess) return;
+            c->events.push_back(ev);
+        }
+    }
+    *out = c->events[c->ev_used];
+    c->ev_used += 2;
+    (void)hipEventRecord(*out, c->stream);
+}
+
+void prof_end(sdsat_ctx* c, hipEvent_t start) {
+    if (!start) return;
+    // the stop event follows its start in the pool
+    for (size_t i = 0; i + 1 < c->ev_used; i += 2)
+        if (c->events[i] == start) { (void)hipEventRecord(c->events[i + 1], c->stream); return; }
+}
+
+// ---------------------------------------------------------------- GEMM helpers
+int run_gemm(sdsat_ctx* c, int kind, int xs, int ep, int M, int n_tiles, int k_steps, int N, int K,
+             const void* W, GemmArgs a) {
+    const GemmPlan p = plan_gemm(c->D.dtype, M, n_tiles, k_steps);
+    a.M = M; a.N = N; a.K = K; a.n_tiles = n_tiles; a.k_steps = k_steps;
+    a.splits = p.splits; a.chunk_steps = p.chunk_steps; a.W = W;
+    a.partial = c->gemm_part; a.counter = c->gemm_cnt; a.err = c->err_flag;
+    hipEvent_t ev;
+    prof_begin(c, kind, &ev);
+    HIPCHK(c, launch_gemm(c->D.dtype, xs, ep, p, a, c->stream));
+    prof_end(c, ev);
+    return SDSAT_OK;
+}
+
+int check_block_args(sdsat_ctx* c, int B, int q) {
+    if (B < 1 || q < 1) return fail(c, SDSAT_EINVAL, "batch and q must be >= 1");
+    if (B > c->D.maxB) return fail(c, SDSAT_ECAPACITY, "batch exceeds max_batch");
+    if (q > c->D.maxQ) return fail(c, SDSAT_ECAPACITY, "q exceeds max_block");
+    return SDSAT_OK;
+}
+
+int max_hint(sdsat_ctx* c, int B) {
+    int m = 0;
+    for (int b = 0; b < B; ++b) m = c->len_hint[b] > m ? c->len_hint[b] : m;
+    return m;
+}
+
+// The host keeps upper bounds of cache_len (commit amounts live on the device).
+// When a bound says a block would not fit, read the true lengths once.
+int fits(sdsat_ctx* c, int B, int q, bool* ok) {
+    *ok = max_hint(c, B) + q <= c->D.S;
+    if (*ok) return SDSAT_OK;
+    std::vector<int> len(B);
+    HIPCHK(c, hipMemcpyAsync(len.data(), c->cache_len, (size_t)B * 4, hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    for (int b = 0; b < B; ++b) c->len_hint[b] = len[b];
+    *ok = max_hint(c, B) + q <= c->D.S;
+    return SDSAT_OK;
+}
+
+int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask, const void* qbuf, void* out,
+                    int out_f32) {
+    const Dims& D = c->D;
+    const AttnPlan p = plan_attention(B, D.H, q, max_hint(c, B));
+    AttnArgs a{};
+    a.qbuf = qbuf; a.kc = layer_k(c, layer); a.vc = layer_v(c, layer);
+    a.cache_len = c->cache_len; a.mask = mask;
+    a.B = B; a.q = q; a.H = D.H; a.S_max = D.S; a.chunk_keys = p.chunk_keys; a.n_chunks = p.n_chunks;
+    a.scale = (float)(1.0 / std::sqrt((double)D.Dh));
+    a.part = c->attn_part; a.counter = c->attn_cnt; a.out = out; a.out_f32 = out_f32; a.err = c->err_flag;
+    hipEvent_t ev;
+    prof_begin(c, PK_ATTN, &ev);
+    HIPCHK(c, launch_attention(D.dtype, D.Dh, a, c->stream));
+    prof_end(c, ev);
+    return SDSAT_OK;
+}
+
+int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const uint64_t* mask, float* logits) {
+    const Dims& D = c->D;
+    const int M = B * q;
+    hipEvent_t evb;
+    prof_begin(c, PK_BLOCK, &evb);
+    HIPCHK(c, launch_embed(D.dtype, c->embed, D.V + D.A, D.d, tokens, M, c->x, c->ssq, D.n_ssq, c->err_flag,
+                           c->stream));
+    for (int l = 0; l < D.L; ++l) {
+        GemmArgs a{};
+        // attention sub-block: RMSNorm -> QKV (+RoPE, KV write) -> attention -> O (+residual)
+        a.x = c->x; a.ldx = D.d; a.ssq = c->ssq; a.n_ssq = D.n_ssq; a.eps = c->cfg.rms_eps;
+        a.gain = c->attn_norm[l];
+        a.qbuf = c->qbuf; a.kc = layer_k(c, l); a.vc = layer_v(c, l);
+        a.cache_len = c->cache_len; a.q = q; a.H = D.H; a.Dh = D.Dh; a.S_max = D.S; a.mask = mask;
+        a.rope_cos = c->rope_cos; a.rope_sin = c->rope_sin;
+        int rc = run_gemm(c, PK_QKV, XS_NORM, EP_QKV, M, D.nt_qkv, D.ks_d, 3 * D.d, D.d, c->w_qkv[l], a);
+        if (rc) return rc;
+        rc = attention_layer(c, l, B, q, mask, c->qbuf, c->obuf, 0);
+        if (rc) return rc;
+        GemmArgs o{};
+        o.xa = c->obuf; o.ldx = D.d; o.resid = c->x; o.ldy = D.d; o.ssq_out = c->ssq;
+        rc = run_gemm(c, PK_O, XS_ACT, EP_RESID, M, D.nt_o, D.ks_d, D.d, D.d, c->w_o[l], o);
+        if (rc) return rc;
+        // feed-forward sub-block: RMSNorm -> gate/up (+SwiGLU) -> down (+residual)
+        GemmArgs f{};
+        f.x = c->x; f.ldx = D.d; f.ssq = c->ssq; f.n_ssq = D.n_ssq; f.eps = c->cfg.rms_eps;
+        f.gain = c->ffn_norm[l]; f.uout = c->ubuf; f.F = D.F;
+        rc = run_gemm(c, PK_GATEUP, XS_NORM, EP_SWIGLU, M, D.nt_gu, D.ks_d, 2 * D.F, D.d, c->w_gu[l], f);
+        if (rc) return rc;
+        GemmArgs dn{};
+        dn.xa = c->ubuf; dn.ldx = D.F; dn.resid = c->x; dn.ldy = D.d; dn.ssq_out = c->ssq;
+        rc = run_gemm(c, PK_DOWN, XS_ACT, EP_RESID, M, D.nt_down, D.ks_f, D.d, D.F, c->w_down[l], dn);
+        if (rc) return rc;
+    }
+    if (logits) {
+        GemmArgs h{};
+        h.x = c->x; h.ldx = D.d; h.ssq = c->ssq; h.n_ssq = D.n_ssq; h.eps = c->cfg.rms_eps;
+        h.gain = c->final_norm; h.y = logits; h.ldy = D.V;
+        int rc = run_gemm(c, PK_LM, XS_NORM, EP_STORE, M, D.nt_lm, D.ks_d, D.V, D.d, c->w_lm, h);
+        if (rc) return rc;
+    }
+    prof_end(c, evb);
+    return SDSAT_OK;
+}
+
+int read_err_flag(sdsat_ctx* c) {
+    int h = 0;
+    HIPCHK(c, hipMemcpyAsync(&h, c->err_flag, 4, hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    if (h) {
+        HIPCHK(c, launch_fill_i32(c->err_flag, 1, 0, c->stream));
+        return fail(c, SDSAT_EDATA, (h & 1)   ? "token id out of range in a block"
+                                    : (h & 2) ? "invalid commit rows"
+                                    : (h & 4) ? "cache capacity exceeded"
+                                              : "attention launched for a shorter cache than committed");
+    }
+    return SDSAT_OK;
+}
+
+}  // namespace
+
+// ================================================================= C-ABI
+extern "C" {
+
+int sdsat_query_sizes(const sdsat_config* cfg, size_t* workspace_bytes) {
+    if (!workspace_bytes) return fail(nullptr, SDSAT_EINVAL, "workspace_bytes is NULL");
+    sdsat_ctx tmp;
+    std::string why;
+    int rc = make_dims(cfg, &tmp.D, &why);
+    if (rc) return fail(nullptr, rc, why);
+    tmp.cfg = *cfg;
+    Carver cv(nullptr);
+    carve(&tmp, cv);
+    *workspace_bytes = align_up(cv.off, 256);
+    return SDSAT_OK;
+}
+
+int sdsat_init(const sdsat_config* cfg, const void* const* weights, int32_t n_weights, void* workspace,
+               size_t workspace_bytes, void* hip_stream, sdsat_ctx** out) {
+    if (!out) return fail(nullptr, SDSAT_EINVAL, "out is NULL");
+    *out = nullptr;
+    sdsat_ctx* c = new (std::nothrow) sdsat_ctx();
+    if (!c) return fail(nullptr, SDSAT_ENOMEM, "host allocation failed");
+    std::string why;
+    int rc = make_dims(cfg, &c->D, &why);
+    if (rc) { delete c; return fail(nullptr, rc, why); }
+    c->cfg = *cfg;
+    const Dims& D = c->D;
+    if (!weights || n_weights != 1 + 9 * D.L + 2) {
+        delete c;
+        return fail(nullptr, SDSAT_EINVAL, "weights must hold 1 + 9*n_layers + 2 pointers");
+    }
+    for (int i = 0; i < n_weights; ++i)
+        if (!weights[i]) { delete c; return fail(nullptr, SDSAT_EINVAL, "a weight pointer is NULL"); }
+    if (!workspace || ((uintptr_t)workspace & 255)) {
+        delete c;
+        return fail(nullptr, SDSAT_EINVAL, "workspace must be non-NULL and 256-byte aligned");
+    }
+    size_t need = 0;
+    sdsat_query_sizes(cfg, &need);
+    if (workspace_bytes < need) {
+        delete c;
+        return fail(nullptr, SDSAT_ENOMEM, "workspace smaller than sdsat_query_sizes()");
+    }
+    c->stream = (hipStream_t)hip_stream;
+    Carver cv(workspace);
+    carve(c, cv);
+    c->len_hint.assign(D.maxB, 0);
+    (void)hipGetDevice(&c->device);
+
+    c->embed = weights[0];
+    c->attn_norm.resize(D.L); c->ffn_norm.resize(D.L);
+    for (int l = 0; l < D.L; ++l) {
+        const void* const* w = weights + 1 + 9 * l;
+        c->attn_norm[l] = (const float*)w[0];
+        c->ffn_norm[l] = (const float*)w[5];
+        PackArgs p{};
+        p.dtype = D.dtype; p.K = D.d; p.k_steps = D.ks_d; p.head_dim = D.Dh; p.F = D.F;
+        // Wq, Wk, Wv stacked, rows grouped for RoPE pairs
+        p.perm = PACK_ROPE; p.N = 3 * D.d; p.n_tiles = D.nt_qkv; p.src0 = w[1]; p.src1 = w[2]; p.src2 = w[3];
+        p.N0 = D.d; p.N1 = D.d; p.dst = c->w_qkv[l];
+        launch_pack(p, c->stream);
+        p.perm = PACK_PLAIN; p.N = D.d; p.n_tiles = D.nt_o; p.src0 = w[4]; p.src1 = p.src2 = nullptr;
+        p.N0 = D.d; p.N1 = 0; p.dst = c->w_o[l];
+        launch_pack(p, c->stream);
+        p.perm = PACK_GATEUP; p.N = 2 * D.F; p.n_tiles = D.nt_gu; p.src0 = w[6]; p.src1 = w[7];
+        p.N0 = D.F; p.N1 = D.F; p.dst = c->w_gu[l];
+        launch_pack(p, c->stream);
+        p.perm = PACK_PLAIN; p.N = D.d; p.K = D.F; p.k_steps = D.ks_f; p.n_tiles = D.nt_down; p.src0 = w[8];
+        p.src1 = nullptr; p.N0 = D.d; p.N1 = 0; p.dst = c->w_down[l];
+        launch_pack(p, c->stream);
+    }
+    c->final_norm = (const float*)weights[1 + 9 * D.L];
+    {
+        PackArgs p{};
+        p.dtype = D.dtype; p.K = D.d; p.k_steps = D.ks_d; p.perm = PACK_PLAIN; p.N = D.V; p.n_tiles = D.nt_lm;
+        p.src0 = weights[2 + 9 * D.L]; p.N0 = D.V; p.dst = c->w_lm;
+        launch_pack(p, c->stream);
+    }
+    auto init_fail = [&](int code) { std::string m = c->err; delete c; return fail(nullptr, code, m); };
+    if (hipGetLastError() != hipSuccess) { c->err = "weight packing launch failed"; return init_fail(SDSAT_EDEVICE); }
+    // rotary tables: angle = pos * base^(-2i/Dh) in double, cos/sin rounded to float
+    {
+        const int half = D.Dh / 2;
+        std::vector<float> cs((size_t)D.S * half), sn((size_t)D.S * half);
+        for (int pos = 0; pos < D.S; ++pos)
+            for (int i = 0; i < half; ++i) {
+                const double inv = std::pow((double)cfg->rope_base, -2.0 * i / D.Dh);
+                const double ang = (double)pos * inv;
+                cs[(size_t)pos * half + i] = (float)std::cos(ang);
+                sn[(size_t)pos * half + i] = (float)std::sin(ang);
+            }
+        if (hipMemcpyAsync(c->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, c->stream) != hipSuccess ||
+            hipMemcpyAsync(c->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, c->stream) != hipSuccess) {
+            c->err = "rotary table upload failed";
+            return init_fail(SDSAT_EDEVICE);
+        }
+        // KV cache starts zero-filled: slots past a sequence's keys are read (and masked) inside
+        // 32-key blocks, so they must hold finite values
+        const size_t kv_words = c->layer_elems * D.L * D.esz / 4;
+        if (launch_fill_i32((int*)c->kc, kv_words, 0, c->stream) != hipSuccess ||
+            launch_fill_i32((int*)c->vc, kv_words, 0, c->stream) != hipSuccess) {
+            c->err = "cache fill failed";
+            return init_fail(SDSAT_EDEVICE);
+        }
+        const int ngroups = gemm_groups(D.nt_lm > D.nt_gu ? (D.nt_lm > D.nt_qkv ? D.nt_lm : D.nt_qkv)
+                                                          : (D.nt_gu > D.nt_qkv ? D.nt_gu : D.nt_qkv));
+        (void)launch_fill_i32(c->gemm_cnt, ngroups, 0, c->stream);
+        (void)launch_fill_i32(c->attn_cnt, (size_t)D.maxB * D.H, 0, c->stream);
+        (void)launch_fill_i32(c->verify_cnt, D.maxB, 0, c->stream);
+        (void)launch_fill_i32(c->cache_len, D.maxB, 0, c->stream);
+        (void)launch_fill_i32(c->err_flag, 1, 0, c->stream);
+        if (hipStreamSynchronize(c->stream) != hipSuccess) {
+            c->err = std::string("init failed: ") + hipGetErrorString(hipGetLastError());
+            return init_fail(SDSAT_EDEVICE);
+        }
+    }
+    c->h_pin_ints = (size_t)D.maxB * D.maxQ * 4 + 64;
+    if (hipHostMalloc((void**)&c->h_pin, c->h_pin_ints * 4, hipHostMallocDefault) != hipSuccess) {
+        c->err = "pinned host allocation failed";
+        return init_fail(SDSAT_ENOMEM);
+    }
+    *out = c;
+    return SDSAT_OK;
+}
+
+int sdsat_reset(sdsat_ctx* c, int32_t batch) {
+    if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
+    if (batch < 1 || batch > c->D.maxB) return fail(c, SDSAT_EINVAL, "batch out of range");
+    HIPCHK(c, launch_set_len(c->cache_len, batch, nullptr, 0, c->stream));
+    for (int b = 0; b < batch; ++b) c->len_hint[b] = 0;
+    return SDSAT_OK;
+}
+
+int sdsat_set_cache_len(sdsat_ctx* c, int32_t batch, const int32_t* h_len) {
+    if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
+    if (batch < 1 || batch > c->D.maxB || !h_len) return fail(c, SDSAT_EINVAL, "bad batch or h_len");
+    for (int b = 0; b < batch; ++b)
+        if (h_len[b] < 0 || h_len[b] > c->D.S) return fail(c, SDSAT_ECAPACITY, "length exceeds max_ctx");
+    // stage through the pinned buffer; wait so the staging can be reused
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    std::memcpy(c->h_pin, h_len, (size_t)batch * 4);
+    HIPCHK(c, hipMemcpyAsync(c->n_commit, c->h_pin, (size_t)batch * 4, hipMemcpyHostToDevice, c->stream));
+    HIPCHK(c, launch_set_len(c->cache_len, batch, c->n_commit, 0, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    for (int b = 0; b < batch; ++b) c->len_hint[b] = h_len[b];
+    return SDSAT_OK;
+}
+
+const int32_t* sdsat_cache_len_ptr(const sdsat_ctx* c) { return c ? c->cache_len : nullptr; }
+
+int sdsat_forward_block(sdsat_ctx* c, int32_t batch, int32_t q, const int32_t* d_tokens,
+                        const uint64_t* d_ancestor_mask, float* d_logits) {
+    if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
+    int rc = check_block_args(c, batch, q);
+    if (rc) return rc;
+    if (!d_tokens) return fail(c, SDSAT_EINVAL, "d_tokens is NULL");
+    if (batch * q > 64) return fail(c, SDSAT_ECAPACITY, "batch * q must be <= 64");
+    bool ok = false;
+    rc = fits(c, batch, q, &ok);
+    if (rc) return rc;
+    if (!ok) return fail(c, SDSAT_ECAPACITY, "cache_len + q exceeds max_ctx");
+    return forward_block_impl(c, batch, q, d_tokens, d_ancestor_mask, d_logits);
+}
+
+int sdsat_verify_greedy(sdsat_ctx* c, int32_t batch, int32_t q, const float* d_logits, const int32_t* d_drafts,
+                        int32_t* d_tokens_out, int32_t* d_n_accept) {
+    if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
+    int rc = check_block_args(c, batch, q);
+    if (rc) return rc;
+    if (!d_logits || !d_tokens_out || (d_drafts && !d_n_accept))
+        return fail(c, SDSAT_EINVAL, "NULL logits, tokens_out, or n_accept with drafts");
+    HIPCHK(c, launch_verify_greedy(d_logits, batch, q, c->D.V, d_drafts, q - 1, d_tokens_out, d_n_accept,
+                                   c->verify_cnt, c->stream));
+    return SDSAT_OK;
+}
+
+int sdsat_verify_nucleus(sdsat_ctx* c, int32_t batch, int32_t q, const float* d_logits, const int32_t* d_drafts,
+                         float temperature, float top_p, int32_t top_k, uint64_t seed, const int32_t* d_pos0,
+                         int32_t* d_tokens_out, int32_t* d_n_accept) {
+    if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
+    int rc = check_block_args(c, batch, q);
+    if (rc) return rc;
+    if (!d_logits || !d_tokens_out || !d_pos0 || (d_drafts && !d_n_accept))
+        return fail(c, SDSAT_EINVAL, "NULL logits, tokens_out, pos0, or n_accept with drafts");
+    if (c->D.V > 32768) return fail(c, SDSAT_EUNSUPPORTED, "nucleus verification needs vocab <= 32768");
+    if (!(top_p > 0.f) || std::isnan(temperature)) return fail(c, SDSAT_EINVAL, "top_p must be > 0");
+    HIPCHK(c, launch_verify_nucleus(d_logits, batch, q, c->D.V, d_drafts, q - 1, temperature, top_p, top_k, seed,
+                                    d_pos0, d_tokens_out, d_n_accept, c->verify_cnt, c->stream));
+    return SDSAT_OK;
+}
+
+int sdsat_commit_kv(sdsat_ctx* c, int32_t batch, int32_t q, const int32_t* d_n_commit, const int32_t* d_rows) {
+    if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
+    int rc = check_block_args(c, batch, q);
+    if (rc) return rc;
+    if (!d_n_commit) return fail(c, SDSAT_EINVAL, "d_n_commit is NULL");
+    const Dims& D = c->D;
+    if (d_rows)
+        HIPCHK(c, launch_commit_gather(D.dtype, c->kc, c->vc, c->layer_elems, D.L, batch, D.H, D.Dh, D.S,
+                                       c->cache_len, d_n_commit, d_rows, q, c->err_flag, c->stream));
+    HIPCHK(c, launch_commit(c->cache_len, batch, d_n_commit, D.S, c->err_flag, c->stream));
+    for (int b = 0; b < batch; ++b) c->len_hint[b] = std::min(c->len_hint[b] + q, D.S);
+    return SDSAT_OK;
+}
+
+int sdsat_generate(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t P, int32_t max_new, int32_t k,
+                   const int32_t* h_adaptive_ids, int32_t mode, float temperature, float top_p, int32_t top_k,
+                   uint64_t seed, int32_t* h_out, sdsat_stats* h_stats) {
+    if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
+    const Dims& D = c->D;
+    if (batch < 1 || batch > D.maxB) return fail(c, SDSAT_ECAPACITY, "batch exceeds max_batch");
+    if (!h_prompts || !h_out || P < 1 || max_new < 0 || k < 0) return fail(c, SDSAT_EINVAL, "bad prompts/out/P/k");
+    if (k > 0 && !h_adaptive_ids) return fail(c, SDSAT_EINVAL, "h_adaptive_ids is NULL");
+    const int q = k + 1;
+    if (q > D.maxQ) return fail(c, SDSAT_ECAPACITY, "k + 1 exceeds max_block");
+    if (batch * q > 64) return fail(c, SDSAT_ECAPACITY, "batch * (k + 1) must be <= 64");
+    if (mode != SDSAT_MODE_GREEDY && mode != SDSAT_MODE_NUCLEUS) return fail(c, SDSAT_EINVAL, "bad mode");
+    const bool nucleus = mode == SDSAT_MODE_NUCLEUS && temperature > 0.f;
+    if (nucleus && D.V > 32768) return fail(c, SDSAT_EUNSUPPORTED, "nucleus verification needs vocab <= 32768");
+    for (int j = 0; j < k; ++j)
+        if (h_adaptive_ids[j] < 0 || h_adaptive_ids[j] >= D.V + D.A)
+            return fail(c, SDSAT_EINVAL, "adaptive id out of range");
+    if ((long)P - 1 + (long)max_new + q + 1 > D.S) return fail(c, SDSAT_ECAPACITY, "prompt + max_new exceeds max_ctx");
+    for (long i = 0; i < (long)batch * P; ++i)
+        if (h_prompts[i] < 0 || h_prompts[i] >= D.V + D.A) return fail(c, SDSAT_EINVAL, "prompt id out of range");
+
+    sdsat_stats st;
+    std::memset(&st, 0, sizeof(st));
+    using clk = std::chrono::steady_clock;
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    const auto t0 = clk::now();
+    int rc = sdsat_reset(c, batch);
+    if (rc) return rc;
+    // prefill: prompt tokens 0..P-2 in blocks of up to qc rows per sequence
+    const int qc = std::max(1, std::min(D.maxQ, 64 / batch));
+    for (int lo = 0; lo < P - 1; lo += qc) {
+        const int n = std::min(qc, P - 1 - lo);
+        for (int b = 0; b < batch; ++b)
+            for (int r = 0; r < n; ++r) c->h_pin[b * n + r] = h_prompts[(size_t)b * P + lo + r];
+        HIPCHK(c, hipMemcpyAsync(c->ptok, c->h_pin, (size_t)batch * n * 4, hipMemcpyHostToDevice, c->stream));
+        rc = forward_block_impl(c, batch, n, c->ptok, nullptr, nullptr);
+        if (rc) return rc;
+        HIPCHK(c, launch_fill_i32(c->n_commit, batch, n, c->stream));
+        HIPCHK(c, launch_commit(c->cache_len, batch, c->n_commit, D.S, c->err_flag, c->stream));
+        for (int b = 0; b < batch; ++b) c->len_hint[b] += n;
+        HIPCHK(c, hipStreamSynchronize(c->stream));   // the pinned staging buffer is reused
+        st.prefill_blocks++;
+    }
+    for (int b = 0; b < batch; ++b) c->h_pin[b] = h_prompts[(size_t)b * P + P - 1];
+    for (int j = 0; j < k; ++j) c->h_pin[batch + j] = h_adaptive_ids[j];
+    HIPCHK(c, hipMemcpyAsync(c->pending, c->h_pin, (size_t)batch * 4, hipMemcpyHostToDevice, c->stream));
+    if (k) HIPCHK(c, hipMemcpyAsync(c->adaptive, c->h_pin + batch, (size_t)k * 4, hipMemcpyHostToDevice, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    rc = read_err_flag(c);
+    if (rc) return rc;
+    const auto t1 = clk::now();
+
+    std::vector<int> produced(batch, 0);
+    int* h_act = c->h_pin;                       // [batch]
+    int* h_o1 = c->h_pin + 64;                   // [batch*q]
+    int* h_o2 = h_o1 + (size_t)batch * q;        // [batch*q]
+    int* h_m = h_o2 + (size_t)batch * q;         // [batch]
+    int* h_err = h_m + batch;
+    for (;;) {
+        bool any = false;
+        for (int b = 0; b < batch; ++b) { h_act[b] = produced[b] < max_new; any |= h_act[b] != 0; }
+        if (!any) break;
+        HIPCHK(c, hipMemcpyAsync(c->active, h_act, (size_t)batch * 4, hipMemcpyHostToDevice, c->stream));
+        // draft step 1 (Eq. 1): [pending, a_1..a_k]
+        HIPCHK(c, launch_build_draft1(c->pending, c->adaptive, batch, k, c->tok1, c->stream));
+        rc = forward_block_impl(c, batch, q, c->tok1, nullptr, c->logits);
+        if (rc) return rc;
+        if (nucleus) {
+            HIPCHK(c, launch_pos0(c->cache_len, batch, 1, c->pos0, c->stream));
+            HIPCHK(c, launch_verify_nucleus(c->logits, batch, q, D.V, nullptr, q - 1, temperature, top_p, top_k, seed,
+                                            c->pos0, c->out1, nullptr, c->verify_cnt, c->stream));
+        } else {
+            HIPCHK(c, launch_verify_greedy(c->logits, batch, q, D.V, nullptr, q - 1, c->out1, nullptr, c->verify_cnt,
+                                           c->stream));
+        }
+        HIPCHK(c, launch_commit(c->cache_len, batch, c->active, D.S, c->err_flag, c->stream));   // keep row 0 (active: 1)
+        for (int b = 0; b < batch; ++b) c->len_hint[b] += h_act[b];
+        // draft step 2 (Eq. 2): [t1, d_1..d_k] = out1
+        rc = forward_block_impl(c, batch, q, c->out1, nullptr, c->logits);
+        if (rc) return rc;
+        if (nucleus) {
+            HIPCHK(c, launch_pos0(c->cache_len, batch, 1, c->pos0, c->stream));
+            HIPCHK(c, launch_verify_nucleus(c->logits, batch, q, D.V, c->out1 + 1, q, temperature, top_p, top_k,
+                                            seed, c->pos0, c->out2, c->n_accept, c->verify_cnt, c->stream));
+        } else {
+            HIPCHK(c, launch_verify_greedy(c->logits, batch, q, D.V, c->out1 + 1, q, c->out2, c->n_accept,
+                                           c->verify_cnt, c->stream));
+        }
+        // verification (Eq. 3): commit rows 0..m, pending = o_m
+        HIPCHK(c, launch_loop_commit(c->cache_len, batch, q, c->active, c->n_accept, c->out2, c->pending,
+                                     c->n_commit, c->stream));
+        HIPCHK(c, hipMemcpyAsync(h_o1, c->out1, (size_t)batch * q * 4, hipMemcpyDeviceToHost, c->stream));
+        HIPCHK(c, hipMemcpyAsync(h_o2, c->out2, (size_t)batch * q * 4, hipMemcpyDeviceToHost, c->stream));
+        HIPCHK(c, hipMemcpyAsync(h_m, c->n_accept, (size_t)batch * 4, hipMemcpyDeviceToHost, c->stream));
+        HIPCHK(c, hipMemcpyAsync(h_err, c->err_flag, 4, hipMemcpyDeviceToHost, c->stream));
+        HIPCHK(c, hipStreamSynchronize(c->stream));
+        if (*h_err) {
+            rc = read_err_flag(c);
+            return rc ? rc : fail(c, SDSAT_EDATA, "device error flag set");
+        }
+        st.loops++;
+        st.blocks += 2;
+        for (int b = 0; b < batch; ++b) {
+            if (!h_act[b]) continue;
+            const int m = h_m[b];
+            if (m < 0 || m > k) return fail(c, SDSAT_EDEVICE, "verification returned an invalid prefix length");
+            st.accepted += m;
+            st.accept_hist[m]++;
+            st.tokens += m + 2;
+            int* row = h_out + (size_t)b * max_new;
+            if (produced[b] < max_new) row[produced[b]++] = h_o1[b * q];
+            for (int j = 0; j <= m && produced[b] < max_new; ++j) row[produced[b]++] = h_o2[b * q + j];
+            c->len_hint[b] += m + 1;
+        }
+    }
+    const auto t2 = clk::now();
+    st.prefill_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
+    st.decode_ms = std::chrono::duration<double, std::milli>(t2 - t1).count();
+    if (h_stats) *h_stats = st;
+    return SDSAT_OK;
+}
+
+int sdsat_kv_write(sdsat_ctx* c, int32_t layer, int32_t batch, int32_t n, const float* d_k, const float* d_v,
+                   const int32_t* d_pos) {
+    if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
+    const Dims& D = c->D;
+    if (layer < 0 || layer >= D.L || batch < 1 || batch > D.maxB || n < 0 || !d_k || !d_v || !d_pos)
+        return fail(c, SDSAT_EINVAL, "bad kv_write arguments");
+    HIPCHK(c, launch_kv_write(D.dtype, layer_k(c, layer), layer_v(c, layer), batch, n, D.H, D.Dh, D.S, d_k, d_v,
+                              d_pos, c->stream));
+    return SDSAT_OK;
+}
+
+int sdsat_attention(sdsat_ctx* c, int32_t layer, int32_t batch, int32_t q, const float* d_q,
+                    const uint64_t* d_ancestor_mask, float* d_out) {
+    if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
+    int rc = check_block_args(c, batch, q);
+    if (rc) return rc;
+    const Dims& D = c->D;
+    if (layer < 0 || layer >= D.L || !d_q || !d_out) return fail(c, SDSAT_EINVAL, "bad attention arguments");
+    bool ok = false;
+    rc = fits(c, batch, q, &ok);
+    if (rc) return rc;
+    if (!ok) return fail(c, SDSAT_ECAPACITY, "cache_len + q exceeds max_ctx");
+    HIPCHK(c, launch_to_elem(D.dtype, d_q, c->qbuf, (size_t)batch * q * D.d, c->stream));
+    return attention_layer(c, layer, batch, q, d_ancestor_mask, c->qbuf, d_out, 1);
+}
+
+size_t sdsat_linear_packed_bytes(int32_t dtype, int32_t N, int32_t K) {
+    if (N < 1 || K < 1) return 0;
+    return packed_elems((N + 15) / 16, (K + 31) / 32) * (dtype == SDSAT_DTYPE_BF16 ? 2 : 4);
+}
+
+int sdsat_linear_pack(int32_t dtype, int32_t N, int32_t K, const void* d_w, void* d_packed, void* hip_stream) {
+    if ((dtype != 0 && dtype != 1) || N < 1 || K < 1 || !d_w || !d_packed)
+        return fail(nullptr, SDSAT_EINVAL, "bad linear_pack arguments");
+    PackArgs p{};
+    p.dtype = dtype; p.N = N; p.K = K; p.n_tiles = (N + 15) / 16; p.k_steps = (K + 31) / 32; p.perm = PACK_PLAIN;
+    p.src0 = d_w; p.N0 = N; p.dst = d_packed;
+    launch_pack(p, (hipStream_t)hip_stream);
+    if (hipGetLastError() != hipSuccess) return fail(nullptr, SDSAT_EDEVICE, "pack launch failed");
+    return SDSAT_OK;
+}
+
+size_t sdsat_linear_scratch_bytes(int32_t M, int32_t N, int32_t K) {
+    if (M < 1 || M > 64 || N < 1 || K < 1) return 0;
+    const int nt = (N + 15) / 16, ks = (K + 31) / 32;
+    size_t f = 0;
+    for (int dt = 0; dt < 2; ++dt) {
+        const GemmPlan p = plan_gemm(dt, M, nt, ks);
+        f = std::max(f, gemm_partial_floats(p, nt));
+    }
+    return align_up((size_t)gemm_groups(nt) * 4, 256) + f * 4;
+}
+
+int sdsat_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const float* d_x, const void* d_packed, float* d_y,
+                 void* d_scratch, void* hip_stream) {
+    if ((dtype != 0 && dtype != 1) || M < 1 || M > 64 || N < 1 || K < 1 || !d_x || !d_packed || !d_y || !d_scratch)
+        return fail(nullptr, SDSAT_EINVAL, "bad linear arguments");
+    const int nt = (N + 15) / 16, ks = (K + 31) / 32;
+    const GemmPlan p = plan_gemm(dtype, M, nt, ks);
+    GemmArgs a{};
+    a.M = M; a.N = N; a.K = K; a.n_tiles = nt; a.k_steps = ks; a.splits = p.splits; a.chunk_steps = p.chunk_steps;
+    a.W = d_packed; a.x = d_x; a.ldx = K; a.y = d_y; a.ldy = N;
+    a.counter = (int*)d_scratch;
+    a.partial = (float*)((char*)d_scratch + align_up((size_t)gemm_groups(nt) * 4, 256));
+    hipError_t e = launch_gemm(dtype, XS_F32, EP_STORE, p, a, (hipStream_t)hip_stream);
+    if (e != hipSuccess) return fail(nullptr, SDSAT_EDEVICE, std::string("linear launch: ") + hipGetErrorString(e));
+    return SDSAT_OK;
+}
+
+int sdsat_profile_kernel(sdsat_ctx* c, int32_t kind) {
+    if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
+    if (kind < 0 || kind > 7) return fail(c, SDSAT_EINVAL, "bad kernel kind");
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    c->prof_kind = kind;
+    c->ev_used = 0;
+    return SDSAT_OK;
+}
+
+int sdsat_kernel_time(sdsat_ctx* c, double* total_ms, int64_t* launches) {
+    if (!c || !total_ms || !launches) return fail(c, SDSAT_EINVAL, "NULL argument");
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    double tot = 0.0;
+    for (size_t i = 0; i + 1 < c->ev_used; i += 2) {
+        float ms = 0.f;
+        HIPCHK(c, hipEventElapsedTime(&ms, c->events[i], c->events[i + 1]));
+        tot += ms;
+    }
+    *total_ms = tot;
+    *launches = (int64_t)(c->ev_used / 2);
+    c->ev_used = 0;
+    return SDSAT_OK;
+}
+
+int sdsat_destroy(sdsat_ctx* c) {
+    if (!c) return SDSAT_OK;
+    (void)hipStreamSynchronize(c->stream);
+    for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
+    if (c->h_pin) (void)hipHostFree(c->h_pin);
+    delete c;
+    return SDSAT_OK;
+}
+
+const char* sdsat_last_error(const sdsat_ctx* c) { return c ? c->err.c_str() : g_init_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,122 @@
+// Internal launcher interface between the host runtime (api.cpp) and the HIP
+// kernels.  Not part of the public C-ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sdsat {
+
+// ---------------------------------------------------------------- packed weights
+// A matrix W [N, K] is stored as 16-column tiles x 32-wide contraction steps:
+// packed[tile][kstep][lane][8] with lane l holding row perm(tile, l % 16) and
+// k = 32*kstep + 8*(l/16) + 0..7 (zero past K or past N).  The row permutation
+// groups rows so that an epilogue finds partner rows in the same tile:
+enum PackPerm {
+    PACK_PLAIN = 0,   // tile t, column c -> row 16t + c
+    PACK_ROPE = 1,    // rows in heads of Dh: tile j of a head holds pair indices 8j..8j+7,
+                      // column c<8 -> row 8j+c, c>=8 -> row Dh/2 + 8j + c-8
+    PACK_GATEUP = 2,  // two stacked [F, K] matrices (gate then up): tile t, c<8 -> gate row 8t+c,
+                      // c>=8 -> up row 8t+c-8
+};
+
+struct PackArgs {
+    int dtype;          // 0 fp32, 1 bf16
+    int N, K;           // rows / columns of the (stacked) source
+    int n_tiles, k_steps;
+    int perm, head_dim, F;
+    const void* src0;   // rows [0, N0)
+    const void* src1;   // rows [N0, N0+N1) (stacked second matrix) or null
+    const void* src2;
+    int N0, N1;         // row counts of src0, src1 (src2 takes the rest)
+    void* dst;
+};
+void launch_pack(const PackArgs& a, hipStream_t s);
+size_t packed_elems(int n_tiles, int k_steps);
+
+// ---------------------------------------------------------------- skinny GEMM
+enum XSource { XS_NORM = 0, XS_ACT = 1, XS_F32 = 2 };
+enum Epilogue { EP_STORE = 0, EP_QKV = 1, EP_RESID = 2, EP_SWIGLU = 3 };
+
+struct GemmArgs {
+    int M, N, K;             // rows of X; real output columns; real contraction length
+    int n_tiles, k_steps;    // packed tile counts
+    int splits, chunk_steps; // split-K: WG (group, split) covers k-steps [split*chunk, ...)
+    const void* W;           // packed weights
+    // X source
+    const float* x;          // XS_NORM / XS_F32: float [M][ldx]
+    const void* xa;          // XS_ACT: T [M][ldx]
+    int ldx;
+    const float* ssq;        // XS_NORM: partial sums of squares [M][n_ssq]
+    int n_ssq;
+    float eps;
+    const float* gain;       // XS_NORM: float [K]
+    // epilogues
+    float* y; int ldy;                   // EP_STORE: float [M][ldy]
+    float* resid; float* ssq_out;        // EP_RESID: resid [M][ldy] (+=), ssq_out [M][n_tiles]
+    void* qbuf; void* kc; void* vc;      // EP_QKV: Q [M][H][Dh]; layer base of K and V caches
+    const int* cache_len; int q, H, Dh, S_max;
+    const uint64_t* mask;                // [M] ancestor masks or null (chain)
+    const float* rope_cos; const float* rope_sin;   // [S_max][Dh/2]
+    void* uout; int F;                   // EP_SWIGLU: T [M][F]
+    // split-K scratch
+    float* partial; int* counter;
+    int* err;                            // device error flags (bit 4: write past the cache)
+};
+
+struct GemmPlan {
+    int splits, chunk_steps, mt, grid, lds_bytes;
+};
+GemmPlan plan_gemm(int dtype, int M, int n_tiles, int k_steps);
+size_t gemm_partial_floats(const GemmPlan& p, int n_tiles);
+int gemm_groups(int n_tiles);
+hipError_t launch_gemm(int dtype, int xs, int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+    const void* qbuf;        // T [B*q][H][Dh]
+    const void* kc;          // T K cache of one layer: [B][H][S_max][Dh]
+    const void* vc;          // T V cache of one layer: [B][H][S_max/32][Dh][32] (keys permuted, vperm)
+    const int* cache_len;
+    const uint64_t* mask;    // [B*q] or null
+    int B, q, H, S_max, chunk_keys, n_chunks;
+    float scale;
+    float* part;             // scratch
+    int* counter;            // [B*H]
+    void* out;               // T (or float if out_f32) [B*q][H*Dh]
+    int out_f32;
+    int* err;                // device error flags (bit 4: read past the cache)
+};
+struct AttnPlan { int chunk_keys, n_chunks, grid; };
+AttnPlan plan_attention(int B, int H, int q, int max_len);
+size_t attention_partial_floats(int B, int H, int q_max, int head_dim);
+hipError_t launch_attention(int dtype, int head_dim, const AttnArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- misc kernels
+hipError_t launch_embed(int dtype, const void* embed, int n_rows_emb, int d, const int* tokens, int M,
+                        float* x, float* ssq, int n_ssq, int* err, hipStream_t s);
+hipError_t launch_kv_write(int dtype, void* kc, void* vc, int B, int n, int H, int Dh, int S_max,
+                           const float* k, const float* v, const int* pos, hipStream_t s);
+hipError_t launch_to_elem(int dtype, const float* src, void* dst, size_t n, hipStream_t s);
+hipError_t launch_commit(int* cache_len, int B, const int* n_commit, int S_max, int* err, hipStream_t s);
+hipError_t launch_commit_gather(int dtype, void* kc, void* vc, size_t layer_stride_elems, int n_layers,
+                                int B, int H, int Dh, int S_max, const int* cache_len, const int* n_commit,
+                                const int* rows, int q, int* err, hipStream_t s);
+hipError_t launch_set_len(int* cache_len, int B, const int* vals_or_null, int value, hipStream_t s);
+hipError_t launch_fill_i32(int* p, size_t n, int value, hipStream_t s);
+
+// ---------------------------------------------------------------- verify
+hipError_t launch_verify_greedy(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,
+                                int* tokens_out, int* n_accept, int* counter, hipStream_t s);
+hipError_t launch_verify_nucleus(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,
+                                 float temperature, float top_p, int top_k, uint64_t seed, const int* pos0,
+                                 int* tokens_out, int* n_accept, int* counter, hipStream_t s);
+
+// ---------------------------------------------------------------- decode-loop helpers
+hipError_t launch_build_draft1(const int* pending, const int* adaptive, int B, int k, int* tokens, hipStream_t s);
+hipError_t launch_loop_commit(int* cache_len, int B, int q, const int* active, const int* n_accept,
+                              const int* tokens2, int* pending, int* n_commit_out, hipStream_t s);
+hipError_t launch_pos0(const int* cache_len, int B, int offset, int* pos0, hipStream_t s);
+
+}  // namespace sdsat

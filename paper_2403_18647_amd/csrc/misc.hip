@@ -1,0 +1,226 @@
+// Small kernels of the block forward and the decode loop: embedding gather,
+// KV-cache commit (length bump, or in-place gather for tree-shaped blocks),
+// cache writes for tests, and the device-side bookkeeping of a draft/verify
+// loop (Section 2.1: draft step 1 keeps one row, verification keeps m+1).
+#include "device.h"
+#include "kernels.h"
+
+namespace sdsat {
+
+// x[m] = E[token[m]] as float, plus per-16-column sums of squares (the
+// partials the first RMSNorm prologue reduces).  Out-of-range ids set *err
+// and read row 0.
+template <typename T>
+__global__ void embed_kernel(const T* emb, int n_rows, int d, const int* tokens, float* x, float* ssq,
+                             int n_ssq, int* err) {
+    const int m = blockIdx.x;
+    int tok = tokens[m];
+    if (tok < 0 || tok >= n_rows) {
+        if (threadIdx.x == 0) atomicOr(err, 1);
+        tok = 0;
+    }
+    const T* src = emb + (size_t)tok * d;
+    for (int t = threadIdx.x; t < n_ssq; t += blockDim.x) {
+        float ss = 0.f;
+        for (int j = 0; j < 16; ++j) {
+            const int k = 16 * t + j;
+            if (k < d) {
+                const float v = to_f32<T>(src[k]);
+                x[(size_t)m * d + k] = v;
+                ss += v * v;
+            }
+        }
+        ssq[(size_t)m * n_ssq + t] = ss;
+    }
+}
+
+hipError_t launch_embed(int dtype, const void* embed, int n_rows_emb, int d, const int* tokens, int M,
+                        float* x, float* ssq, int n_ssq, int* err, hipStream_t s) {
+    if (dtype == 1)
+        hipLaunchKernelGGL(embed_kernel<uint16_t>, dim3(M), dim3(256), 0, s, (const uint16_t*)embed, n_rows_emb,
+                           d, tokens, x, ssq, n_ssq, err);
+    else
+        hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, (const float*)embed, n_rows_emb, d,
+                           tokens, x, ssq, n_ssq, err);
+    return hipGetLastError();
+}
+
+// K/V rows [B][n][H][Dh] float -> cache slots pos[b*n + i]
+template <typename T>
+__global__ void kv_write_kernel(T* kc, T* vc, int B, int n, int H, int Dh, int S_max, const float* k,
+                                const float* v, const int* pos) {
+    const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t total = (size_t)B * n * H * Dh;
+    if (idx >= total) return;
+    const int d = (int)(idx % Dh);
+    const int h = (int)((idx / Dh) % H);
+    const int i = (int)((idx / ((size_t)Dh * H)) % n);
+    const int b = (int)(idx / ((size_t)Dh * H * n));
+    const int p = pos[(size_t)b * n + i];
+    if (p < 0 || p >= S_max) return;
+    kc[(((size_t)b * H + h) * S_max + p) * Dh + d] = to_elem<T>(k[idx]);
+    const size_t blk = ((size_t)b * H + h) * (S_max / 32) + p / 32;
+    vc[(blk * Dh + d) * 32 + vperm(p & 31)] = to_elem<T>(v[idx]);
+}
+
+hipError_t launch_kv_write(int dtype, void* kc, void* vc, int B, int n, int H, int Dh, int S_max,
+                           const float* k, const float* v, const int* pos, hipStream_t s) {
+    const size_t total = (size_t)B * n * H * Dh;
+    const int blocks = (int)((total + 255) / 256);
+    if (blocks == 0) return hipSuccess;
+    if (dtype == 1)
+        hipLaunchKernelGGL(kv_write_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s, (uint16_t*)kc, (uint16_t*)vc,
+                           B, n, H, Dh, S_max, k, v, pos);
+    else
+        hipLaunchKernelGGL(kv_write_kernel<float>, dim3(blocks), dim3(256), 0, s, (float*)kc, (float*)vc, B, n, H,
+                           Dh, S_max, k, v, pos);
+    return hipGetLastError();
+}
+
+template <typename T>
+__global__ void to_elem_kernel(const float* src, T* dst, size_t n) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) dst[i] = to_elem<T>(src[i]);
+}
+
+hipError_t launch_to_elem(int dtype, const float* src, void* dst, size_t n, hipStream_t s) {
+    const int blocks = (int)((n + 255) / 256);
+    if (blocks == 0) return hipSuccess;
+    if (dtype == 1) hipLaunchKernelGGL(to_elem_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s, src, (uint16_t*)dst, n);
+    else hipLaunchKernelGGL(to_elem_kernel<float>, dim3(blocks), dim3(256), 0, s, src, (float*)dst, n);
+    return hipGetLastError();
+}
+
+// cache_len[b] += n[b], kept within [0, S_max] (an out-of-range n sets err bit 4)
+__global__ void commit_kernel(int* cache_len, int B, const int* n_commit, int S_max, int* err) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    const int v = cache_len[b] + n_commit[b];
+    if (v < 0 || v > S_max) {
+        atomicOr(err, 4);
+        cache_len[b] = v < 0 ? 0 : S_max;
+    } else {
+        cache_len[b] = v;
+    }
+}
+
+hipError_t launch_commit(int* cache_len, int B, const int* n_commit, int S_max, int* err, hipStream_t s) {
+    hipLaunchKernelGGL(commit_kernel, dim3((B + 63) / 64), dim3(64), 0, s, cache_len, B, n_commit, S_max, err);
+    return hipGetLastError();
+}
+
+// Tree case: move block rows rows[b][j] (strictly ascending, rows[b][j] >= j)
+// to slot L + j.  Walking j upwards never overwrites a row still to be read.
+// One thread per (layer, b, h, d); the length bump is a separate launch.
+template <typename T>
+__global__ void gather_kernel(T* kc, T* vc, size_t layer_stride, int n_layers, int B, int H, int Dh, int S_max,
+                              const int* cache_len, const int* n_commit, const int* rows, int q, int* err) {
+    const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t total = (size_t)n_layers * B * H * Dh;
+    if (idx >= total) return;
+    const int d = (int)(idx % Dh);
+    const int h = (int)((idx / Dh) % H);
+    const int b = (int)((idx / ((size_t)Dh * H)) % B);
+    const int layer = (int)(idx / ((size_t)Dh * H * B));
+    const int L = cache_len[b];
+    const int n = n_commit[b];
+    T* K = kc + layer * layer_stride + ((size_t)b * H + h) * S_max * Dh;
+    T* V = vc + layer * layer_stride + ((size_t)b * H + h) * S_max * Dh;
+    int prev = -1;
+    for (int j = 0; j < n; ++j) {
+        const int r = rows[(size_t)b * q + j];
+        if (r <= prev || r < j || r >= q || L + r >= S_max) {
+            if (d == 0 && h == 0 && layer == 0) atomicOr(err, 2);
+            return;
+        }
+        prev = r;
+        if (r == j) continue;
+        const int src = L + r, dst = L + j;
+        K[(size_t)dst * Dh + d] = K[(size_t)src * Dh + d];
+        V[((size_t)(dst / 32) * Dh + d) * 32 + vperm(dst & 31)] = V[((size_t)(src / 32) * Dh + d) * 32 + vperm(src & 31)];
+    }
+}
+
+hipError_t launch_commit_gather(int dtype, void* kc, void* vc, size_t layer_stride_elems, int n_layers, int B,
+                                int H, int Dh, int S_max, const int* cache_len, const int* n_commit,
+                                const int* rows, int q, int* err, hipStream_t s) {
+    const size_t total = (size_t)n_layers * B * H * Dh;
+    const int blocks = (int)((total + 255) / 256);
+    if (dtype == 1)
+        hipLaunchKernelGGL(gather_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s, (uint16_t*)kc, (uint16_t*)vc,
+                           layer_stride_elems, n_layers, B, H, Dh, S_max, cache_len, n_commit, rows, q, err);
+    else
+        hipLaunchKernelGGL(gather_kernel<float>, dim3(blocks), dim3(256), 0, s, (float*)kc, (float*)vc,
+                           layer_stride_elems, n_layers, B, H, Dh, S_max, cache_len, n_commit, rows, q, err);
+    return hipGetLastError();
+}
+
+__global__ void set_len_kernel(int* cache_len, int B, const int* vals, int value) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b < B) cache_len[b] = vals ? vals[b] : value;
+}
+
+hipError_t launch_set_len(int* cache_len, int B, const int* vals_or_null, int value, hipStream_t s) {
+    hipLaunchKernelGGL(set_len_kernel, dim3((B + 63) / 64), dim3(64), 0, s, cache_len, B, vals_or_null, value);
+    return hipGetLastError();
+}
+
+__global__ void fill_i32_kernel(int* p, size_t n, int value) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = value;
+}
+
+hipError_t launch_fill_i32(int* p, size_t n, int value, hipStream_t s) {
+    const int blocks = (int)((n + 255) / 256);
+    if (blocks == 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(blocks), dim3(256), 0, s, p, n, value);
+    return hipGetLastError();
+}
+
+// draft step 1 block: [pending_b, a_1..a_k]
+__global__ void build_draft1_kernel(const int* pending, const int* adaptive, int B, int k, int* tokens) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= B * (k + 1)) return;
+    const int b = i / (k + 1), j = i % (k + 1);
+    tokens[i] = j == 0 ? pending[b] : adaptive[j - 1];
+}
+
+hipError_t launch_build_draft1(const int* pending, const int* adaptive, int B, int k, int* tokens, hipStream_t s) {
+    const int n = B * (k + 1);
+    hipLaunchKernelGGL(build_draft1_kernel, dim3((n + 63) / 64), dim3(64), 0, s, pending, adaptive, B, k, tokens);
+    return hipGetLastError();
+}
+
+// after verification: active sequences commit m+1 rows and take o_m as the
+// next pending token; finished ones commit nothing.
+__global__ void loop_commit_kernel(int* cache_len, int B, int q, const int* active, const int* n_accept,
+                                   const int* tokens2, int* pending, int* n_commit_out) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    const int m = n_accept[b];
+    const int n = active[b] ? m + 1 : 0;
+    n_commit_out[b] = n;
+    if (n) {
+        cache_len[b] += n;
+        pending[b] = tokens2[(size_t)b * q + m];
+    }
+}
+
+hipError_t launch_loop_commit(int* cache_len, int B, int q, const int* active, const int* n_accept,
+                              const int* tokens2, int* pending, int* n_commit_out, hipStream_t s) {
+    hipLaunchKernelGGL(loop_commit_kernel, dim3((B + 63) / 64), dim3(64), 0, s, cache_len, B, q, active, n_accept,
+                       tokens2, pending, n_commit_out);
+    return hipGetLastError();
+}
+
+__global__ void pos0_kernel(const int* cache_len, int B, int offset, int* pos0) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b < B) pos0[b] = cache_len[b] + offset;
+}
+
+hipError_t launch_pos0(const int* cache_len, int B, int offset, int* pos0, hipStream_t s) {
+    hipLaunchKernelGGL(pos0_kernel, dim3((B + 63) / 64), dim3(64), 0, s, cache_len, B, offset, pos0);
+    return hipGetLastError();
+}
+
+}  // namespace sdsat

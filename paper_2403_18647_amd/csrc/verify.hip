@@ -1,0 +1,401 @@
+// Verification kernels (Section 2.1.1 Eq. 3 and Section 2.1.2).
+//
+// One workgroup per logits row (b, j) reduces over the vocabulary; the last
+// workgroup of sequence b to finish (device-scope counter) then scans the rows
+// for the accepted prefix: m = number of leading j >= 1 with
+// drafts[b][j-1] == token[b][j-1].
+//
+// Greedy: arg-max with ties to the lowest id.
+// Nucleus: float64 arithmetic on z = logit / T.  Optional top-k (ties keep
+// lower ids) and the top-p threshold are found by radix descent over the
+// order-preserving 32-bit keys of the float logits (4 bits per pass, 8
+// passes): the threshold is the largest key K with S(K) = sum of e^(z - zmax)
+// over kept ids with key >= K at least p * E.  The token is the smallest id of
+// the nucleus whose ascending-id cumulative mass exceeds u * S(K*), with the
+// cumulative sums formed by a block-wide prefix scan in id order.  All sums
+// use a fixed reduction order, so results are reproducible run to run.
+#include "device.h"
+#include "kernels.h"
+
+namespace sdsat {
+
+// ---------------------------------------------------------------- helpers
+__device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
+    return v > bv || (v == bv && i < bi);
+}
+
+template <int NT>
+__device__ int block_argmax(const float* row, int V, float* s_val, int* s_idx) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+    if ((V & 3) == 0) {
+        const float4* r4 = reinterpret_cast<const float4*>(row);
+        for (int i = threadIdx.x; i < V / 4; i += NT) {
+            const float4 v = r4[i];
+            if (better(v.x, 4 * i, bv, bi)) { bv = v.x; bi = 4 * i; }
+            if (better(v.y, 4 * i + 1, bv, bi)) { bv = v.y; bi = 4 * i + 1; }
+            if (better(v.z, 4 * i + 2, bv, bi)) { bv = v.z; bi = 4 * i + 2; }
+            if (better(v.w, 4 * i + 3, bv, bi)) { bv = v.w; bi = 4 * i + 3; }
+        }
+    } else {
+        for (int i = threadIdx.x; i < V; i += NT) {
+            const float v = row[i];
+            if (better(v, i, bv, bi)) { bv = v; bi = i; }
+        }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float ov = __shfl_xor(bv, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (lane == 0) { s_val[wave] = bv; s_idx[wave] = bi; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < NT / 64; ++w)
+            if (better(s_val[w], s_idx[w], bv, bi)) { bv = s_val[w]; bi = s_idx[w]; }
+        s_idx[0] = bi == 0x7fffffff ? 0 : bi;
+    }
+    __syncthreads();
+    const int r = s_idx[0];
+    __syncthreads();
+    return r;
+}
+
+// last workgroup of sequence b computes the accepted prefix length
+__device__ void finish_sequence(int b, int q, const int* drafts, int drafts_ld, const int* tokens_out,
+                                int* n_accept, int* counter) {
+    __shared__ int s_last;
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) s_last = atomicAdd(&counter[b], 1) == q - 1;
+    __syncthreads();
+    if (!s_last || threadIdx.x != 0) return;
+    __threadfence();
+    int m = 0;
+    if (drafts) {
+        for (int j = 1; j < q; ++j) {
+            if (drafts[(size_t)b * drafts_ld + j - 1] != tokens_out[(size_t)b * q + j - 1]) break;
+            m = j;
+        }
+    }
+    if (n_accept) n_accept[b] = m;
+    counter[b] = 0;
+}
+
+__global__ void __launch_bounds__(256) verify_greedy_kernel(const float* logits, int q, int V, const int* drafts,
+                                                            int drafts_ld, int* tokens_out, int* n_accept,
+                                                            int* counter) {
+    __shared__ float s_val[4];
+    __shared__ int s_idx[4];
+    const int row = blockIdx.x, b = row / q;
+    const int t = block_argmax<256>(logits + (size_t)row * V, V, s_val, s_idx);
+    if (threadIdx.x == 0) tokens_out[row] = t;
+    finish_sequence(b, q, drafts, drafts_ld, tokens_out, n_accept, counter);
+}
+
+hipError_t launch_verify_greedy(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,
+                                int* tokens_out, int* n_accept, int* counter, hipStream_t s) {
+    hipLaunchKernelGGL(verify_greedy_kernel, dim3(B * q), dim3(256), 0, s, logits, q, V, drafts, drafts_ld,
+                       tokens_out, n_accept, counter);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- nucleus
+static constexpr int kNT = 1024;    // threads per row
+static constexpr int kCPT = 32;     // ids per thread (contiguous): V <= 32768
+static constexpr int kWaves = kNT / 64;
+
+__device__ __forceinline__ uint32_t order_key(float f) {
+    uint32_t u = __float_as_uint(f);
+    if (u == 0x80000000u) u = 0u;   // -0 and +0 compare equal
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// SplitMix64 (Steele, Lea, Flood 2014): output number n of the generator started at `state`
+__device__ __forceinline__ uint64_t splitmix64(uint64_t state, uint64_t n) {
+    uint64_t z = state + n * 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ double keyed_uniform(uint64_t seed, int b, int pos) {
+    const uint64_t c = ((uint64_t)(uint32_t)b << 32) | (uint32_t)pos;
+    return (double)(splitmix64(seed, c + 1) >> 11) * (1.0 / 9007199254740992.0);
+}
+
+__device__ __forceinline__ double dshfl_xor(double v, int o) {
+    int2 p = __builtin_bit_cast(int2, v);
+    p.x = __shfl_xor(p.x, o, 64);
+    p.y = __shfl_xor(p.y, o, 64);
+    return __builtin_bit_cast(double, p);
+}
+
+__device__ __forceinline__ double dshfl_up(double v, int o) {
+    int2 p = __builtin_bit_cast(int2, v);
+    p.x = __shfl_up(p.x, o, 64);
+    p.y = __shfl_up(p.y, o, 64);
+    return __builtin_bit_cast(double, p);
+}
+
+// Sum of NV doubles per thread over the block, fixed order; result in every thread.
+template <int NV>
+__device__ void block_sum_d(double (&v)[NV], double* s_buf /* [kWaves][NV] */) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) v[i] += dshfl_xor(v[i], o);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (lane == 0)
+#pragma unroll
+        for (int i = 0; i < NV; ++i) s_buf[wave * NV + i] = v[i];
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        double s = 0.0;
+        for (int w = 0; w < kWaves; ++w) s += s_buf[w * NV + i];
+        v[i] = s;
+    }
+    __syncthreads();
+}
+
+__device__ int block_sum_i(int v, int* s_buf) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (lane == 0) s_buf[wave] = v;
+    __syncthreads();
+    int s = 0;
+    for (int w = 0; w < kWaves; ++w) s += s_buf[w];
+    __syncthreads();
+    return s;
+}
+
+// exclusive prefix sum of one int per thread, thread order
+__device__ int block_exscan_i(int v, int* s_buf) {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    int inc = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += t;
+    }
+    if (lane == 63) s_buf[wave] = inc;
+    __syncthreads();
+    int base = 0;
+    for (int w = 0; w < wave; ++w) base += s_buf[w];
+    __syncthreads();
+    return base + inc - v;
+}
+
+// exclusive prefix sum of one double per thread, thread order
+__device__ double block_exscan_d(double v, double* s_buf) {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    double inc = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const double t = dshfl_up(inc, o);
+        if (lane >= o) inc += t;
+    }
+    if (lane == 63) s_buf[wave] = inc;
+    __syncthreads();
+    double base = 0.0;
+    for (int w = 0; w < wave; ++w) base += s_buf[w];
+    __syncthreads();
+    return base + (inc - v);
+}
+
+__device__ int block_min_i(int v, int* s_buf) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (lane == 0) s_buf[wave] = v;
+    __syncthreads();
+    int s = s_buf[0];
+    for (int w = 1; w < kWaves; ++w) s = min(s, s_buf[w]);
+    __syncthreads();
+    return s;
+}
+
+__device__ int block_max_i(int v, int* s_buf) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (lane == 0) s_buf[wave] = v;
+    __syncthreads();
+    int s = s_buf[0];
+    for (int w = 1; w < kWaves; ++w) s = max(s, s_buf[w]);
+    __syncthreads();
+    return s;
+}
+
+__device__ float block_max_f(float v, float* s_buf) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (lane == 0) s_buf[wave] = v;
+    __syncthreads();
+    float s = s_buf[0];
+    for (int w = 1; w < kWaves; ++w) s = fmaxf(s, s_buf[w]);
+    __syncthreads();
+    return s;
+}
+
+__device__ int sample_row(const float* row, int V, double T, double p, int top_k, double u) {
+    __shared__ double s_d[kWaves * 16];
+    __shared__ int s_i[kWaves];
+    __shared__ float s_f[kWaves];
+    const int id0 = threadIdx.x * kCPT;
+    float lv[kCPT];
+#pragma unroll
+    for (int i = 0; i < kCPT; i += 4) {
+        if (id0 + i + 3 < V && (V & 3) == 0) {
+            const float4 v = *reinterpret_cast<const float4*>(row + id0 + i);
+            lv[i] = v.x; lv[i + 1] = v.y; lv[i + 2] = v.z; lv[i + 3] = v.w;
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) lv[i + j] = id0 + i + j < V ? row[id0 + i + j] : -INFINITY;
+        }
+    }
+    uint32_t kept = 0;   // bit i: id0+i is kept by top-k
+#pragma unroll
+    for (int i = 0; i < kCPT; ++i) if (id0 + i < V) kept |= 1u << i;
+
+    if (top_k > 0 && top_k < V) {
+        // largest key Kk with count(key >= Kk) >= top_k
+        uint32_t prefix = 0;
+        for (int shift = 28; shift >= 0; shift -= 4) {
+            int cnt[16];
+#pragma unroll
+            for (int v = 0; v < 16; ++v) cnt[v] = 0;
+#pragma unroll
+            for (int i = 0; i < kCPT; ++i) {
+                if (!((kept >> i) & 1u)) continue;
+                const uint32_t key = order_key(lv[i]);
+#pragma unroll
+                for (int v = 0; v < 16; ++v) cnt[v] += key >= (prefix | ((uint32_t)v << shift)) ? 1 : 0;
+            }
+            int best = 0;
+            for (int v = 0; v < 16; ++v) {
+                const int tot = block_sum_i(cnt[v], s_i);
+                if (tot >= top_k) best = v;
+            }
+            prefix |= (uint32_t)best << shift;
+        }
+        const uint32_t Kk = prefix;
+        int gt = 0, eq = 0;
+#pragma unroll
+        for (int i = 0; i < kCPT; ++i) {
+            if (!((kept >> i) & 1u)) continue;
+            const uint32_t key = order_key(lv[i]);
+            gt += key > Kk;
+            eq += key == Kk;
+        }
+        const int need = top_k - block_sum_i(gt, s_i);
+        int rank = block_exscan_i(eq, s_i);
+        uint32_t nk = 0;
+#pragma unroll
+        for (int i = 0; i < kCPT; ++i) {
+            if (!((kept >> i) & 1u)) continue;
+            const uint32_t key = order_key(lv[i]);
+            if (key > Kk) nk |= 1u << i;
+            else if (key == Kk) { if (rank < need) nk |= 1u << i; ++rank; }
+        }
+        kept = nk;
+    }
+
+    float lmax = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kCPT; ++i) if ((kept >> i) & 1u) lmax = fmaxf(lmax, lv[i]);
+    lmax = block_max_f(lmax, s_f);
+    const double zmax = (double)lmax / T;
+    double e[kCPT];
+    double tot[1] = {0.0};
+#pragma unroll
+    for (int i = 0; i < kCPT; ++i) {
+        e[i] = ((kept >> i) & 1u) ? exp((double)lv[i] / T - zmax) : 0.0;
+        tot[0] += e[i];
+    }
+    block_sum_d<1>(tot, s_d);
+    const double pE = (p < 1.0 ? p : 1.0) * tot[0];
+
+    // top-p threshold key
+    uint32_t prefix = 0;
+    double mass = tot[0];
+    for (int shift = 28; shift >= 0; shift -= 4) {
+        double S[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) S[v] = 0.0;
+#pragma unroll
+        for (int i = 0; i < kCPT; ++i) {
+            if (!((kept >> i) & 1u)) continue;
+            const uint32_t key = order_key(lv[i]);
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                if (key >= (prefix | ((uint32_t)v << shift))) S[v] += e[i];
+        }
+        block_sum_d<16>(S, s_d);
+        int best = 0;
+        double bm = S[0];
+#pragma unroll
+        for (int v = 1; v < 16; ++v) if (S[v] >= pE) { best = v; bm = S[v]; }
+        prefix |= (uint32_t)best << shift;
+        mass = bm;
+    }
+    const uint32_t Kstar = prefix;
+
+    // inverse CDF over the nucleus in ascending id order
+    double loc = 0.0;
+    uint32_t inN = 0;
+#pragma unroll
+    for (int i = 0; i < kCPT; ++i)
+        if (((kept >> i) & 1u) && order_key(lv[i]) >= Kstar) { inN |= 1u << i; loc += e[i]; }
+    const double pre = block_exscan_d(loc, s_d);
+    const double target = u * mass;
+    int cand = 0x7fffffff;
+    int last = -1;
+    double cum = pre;
+#pragma unroll
+    for (int i = 0; i < kCPT; ++i) {
+        if (!((inN >> i) & 1u)) continue;
+        cum += e[i];
+        last = id0 + i;
+        if (cand == 0x7fffffff && cum > target) cand = id0 + i;
+    }
+    cand = block_min_i(cand, s_i);
+    if (cand == 0x7fffffff) cand = block_max_i(last, s_i);
+    return cand;
+}
+
+__global__ void __launch_bounds__(kNT) verify_nucleus_kernel(const float* logits, int q, int V, const int* drafts,
+                                                             int drafts_ld, float temperature, float top_p,
+                                                             int top_k, uint64_t seed, const int* pos0,
+                                                             int* tokens_out, int* n_accept, int* counter) {
+    __shared__ float s_val[kWaves];
+    __shared__ int s_idx[kWaves];
+    const int row = blockIdx.x, b = row / q, j = row % q;
+    const float* lg = logits + (size_t)row * V;
+    const bool sample = temperature > 0.f && (drafts != nullptr || j == 0);
+    int t;
+    if (sample) {
+        const double u = keyed_uniform(seed, b, pos0[b] + j);
+        t = sample_row(lg, V, (double)temperature, (double)top_p, top_k, u);
+    } else {
+        t = block_argmax<kNT>(lg, V, s_val, s_idx);
+    }
+    if (threadIdx.x == 0) tokens_out[row] = t;
+    finish_sequence(b, q, drafts, drafts_ld, tokens_out, n_accept, counter);
+}
+
+hipError_t launch_verify_nucleus(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,
+                                 float temperature, float top_p, int top_k, uint64_t seed, const int* pos0,
+                                 int* tokens_out, int* n_accept, int* counter, hipStream_t s) {
+    if (V > kNT * kCPT) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(verify_nucleus_kernel, dim3(B * q), dim3(kNT), 0, s, logits, q, V, drafts, drafts_ld,
+                       temperature, top_p, top_k, seed, pos0, tokens_out, n_accept, counter);
+    return hipGetLastError();
+}
+
+}  // namespace sdsat

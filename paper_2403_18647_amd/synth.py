@@ -198,3 +198,32 @@ def small_shape(**kw) -> ModelShape:
 
 def workload(name: str, **kw) -> Workload:
     return replace(WORKLOADS[name], **kw)
+
+
+def device_weights(wl: Workload, device="cuda"):
+    """Generate every tensor and upload it, in the fixed order, as torch tensors
+    (bfloat16 or float32 matrices, float32 gains).  One pinned staging buffer is
+    reused for all tensors."""
+    import torch
+    shape = wl.shape
+    names = tensor_names(shape)
+    bf16 = shape.dtype == "bf16"
+    biggest = max(int(np.prod(tensor_shape(shape, n))) for n in names)
+    host_dt = torch.int16 if bf16 else torch.float32
+    stage = torch.empty(biggest, dtype=host_dt, pin_memory=torch.cuda.is_available())
+    stage_np = stage.numpy().view(np.uint16 if bf16 else np.float32)
+    out = []
+    for n in names:
+        shp = tensor_shape(shape, n)
+        cnt = int(np.prod(shp))
+        if is_gain(n):
+            w = tensor(wl, n)
+            host = torch.from_numpy(bf16_bits_to_f32(w) if bf16 else w)
+            out.append(host.to(device))
+            continue
+        fill_tensor(wl, n, stage_np[:cnt])
+        dev = torch.empty(shp, dtype=torch.bfloat16 if bf16 else torch.float32, device=device)
+        src = stage[:cnt].view(torch.bfloat16) if bf16 else stage[:cnt]
+        dev.view(-1).copy_(src, non_blocking=False)
+        out.append(dev)
+    return out
