@@ -203,8 +203,9 @@ int sdsat_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const float* d_
 
 /* Per-kernel timing with HIP events on the context's stream.  kind: 0 off,
  * 1 gate/up GEMM, 2 QKV GEMM, 3 attention, 4 down GEMM, 5 O GEMM, 6 LM head,
- * 7 whole forward block.  sdsat_kernel_time synchronizes the stream and
- * returns the summed milliseconds and launch count since the last call. */
+ * 7 whole block forward with logits (draft / verify blocks), 8 whole block
+ * forward without logits (prefill).  sdsat_kernel_time synchronizes the stream
+ * and returns the summed milliseconds and launch count since the last call. */
 int sdsat_profile_kernel(sdsat_ctx* ctx, int32_t kind);
 int sdsat_kernel_time(sdsat_ctx* ctx, double* total_ms, int64_t* launches);
 

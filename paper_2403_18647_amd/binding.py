@@ -19,7 +19,8 @@ SDSAT_OK = 0
 ERRORS = {-1: "EINVAL", -2: "ENOMEM", -3: "EDEVICE", -4: "ECAPACITY", -5: "EUNSUPPORTED", -6: "EDATA"}
 DTYPE_FP32, DTYPE_BF16 = 0, 1
 MODE_GREEDY, MODE_NUCLEUS = 0, 1
-PROFILE_KINDS = {"off": 0, "gateup": 1, "qkv": 2, "attention": 3, "down": 4, "o": 5, "lm_head": 6, "block": 7}
+PROFILE_KINDS = {"off": 0, "gateup": 1, "qkv": 2, "attention": 3, "down": 4, "o": 5, "lm_head": 6, "block": 7,
+                 "prefill": 8}
 
 
 class sdsat_config(ctypes.Structure):

@@ -42,6 +42,7 @@ struct Dims {
     int ks_d, ks_f;  // k-steps for K = d and K = F
     int nt_qkv, nt_o, nt_gu, nt_down, nt_lm;
     int n_ssq;       // d / 16
+    int d_pad, F_pad;  // activation row strides (contraction lengths padded to 32)
 };
 
 int make_dims(const sdsat_config* c, Dims* D, std::string* why) {
@@ -66,10 +67,15 @@ int make_dims(const sdsat_config* c, Dims* D, std::string* why) {
     D->nt_qkv = 3 * D->d / 16; D->nt_o = D->d / 16; D->nt_gu = (D->F + 7) / 8; D->nt_down = D->d / 16;
     D->nt_lm = (D->V + 15) / 16;
     D->n_ssq = D->d / 16;
+    D->d_pad = D->ks_d * 32; D->F_pad = D->ks_f * 32;
     return SDSAT_OK;
 }
 
-enum ProfKind { PK_OFF = 0, PK_GATEUP = 1, PK_QKV = 2, PK_ATTN = 3, PK_DOWN = 4, PK_O = 5, PK_LM = 6, PK_BLOCK = 7 };
+enum ProfKind {
+    PK_OFF = 0, PK_GATEUP = 1, PK_QKV = 2, PK_ATTN = 3, PK_DOWN = 4, PK_O = 5, PK_LM = 6,
+    PK_BLOCK = 7,     // block forwards that produce logits (draft and verify blocks)
+    PK_PREFILL = 8,   // block forwards without logits (prefill)
+};
 
 }  // namespace
 
@@ -89,13 +95,13 @@ struct sdsat_ctx {
     // cache
     void* kc = nullptr; void* vc = nullptr;
     size_t layer_elems = 0;   // elements per layer of K (and of V)
-    float* rope_cos = nullptr; float* rope_sin = nullptr;
+    double* inv_freq = nullptr;   // rotary inverse frequencies [Dh/2]
     // activations
     float* x = nullptr; float* ssq = nullptr;
+    void* xb = nullptr;   // x in the matrix element type, row stride d_pad (zero pad)
     void* qbuf = nullptr; void* obuf = nullptr; void* ubuf = nullptr;
     // scratch
-    float* gemm_part = nullptr; int* gemm_cnt = nullptr;
-    float* attn_part = nullptr; int* attn_cnt = nullptr;
+    float* attn_part = nullptr;
     int* cache_len = nullptr; int* err_flag = nullptr; int* verify_cnt = nullptr;
     // generation buffers
     int *tok1 = nullptr, *out1 = nullptr, *out2 = nullptr, *n_accept = nullptr, *pending = nullptr;
@@ -140,30 +146,14 @@ void carve(sdsat_ctx* c, Carver& cv) {
     c->layer_elems = (size_t)D.maxB * D.H * D.S * D.Dh;
     c->kc = cv.take(c->layer_elems * D.L * e);
     c->vc = cv.take(c->layer_elems * D.L * e);
-    c->rope_cos = (float*)cv.take((size_t)D.S * (D.Dh / 2) * 4);
-    c->rope_sin = (float*)cv.take((size_t)D.S * (D.Dh / 2) * 4);
+    c->inv_freq = (double*)cv.take((size_t)(D.Dh / 2) * 8);
     c->x = (float*)cv.take((size_t)D.maxM * D.d * 4);
     c->ssq = (float*)cv.take((size_t)D.maxM * D.n_ssq * 4);
+    c->xb = cv.take((size_t)D.maxM * D.d_pad * e);
     c->qbuf = cv.take((size_t)D.maxB * D.maxQ * D.d * e);
-    c->obuf = cv.take((size_t)D.maxM * D.d * e);
-    c->ubuf = cv.take((size_t)D.maxM * D.F * e);
-    // split-K scratch: the largest need over the five GEMMs at any M <= maxM
-    size_t part = 0;
-    int groups = 0;
-    for (int M = 1; M <= D.maxM; ++M) {
-        const int nts[5] = {D.nt_qkv, D.nt_o, D.nt_gu, D.nt_down, D.nt_lm};
-        const int kss[5] = {D.ks_d, D.ks_d, D.ks_d, D.ks_f, D.ks_d};
-        for (int i = 0; i < 5; ++i) {
-            const GemmPlan p = plan_gemm(D.dtype, M, nts[i], kss[i]);
-            const size_t f = gemm_partial_floats(p, nts[i]);
-            if (f > part) part = f;
-            if (gemm_groups(nts[i]) > groups) groups = gemm_groups(nts[i]);
-        }
-    }
-    c->gemm_part = (float*)cv.take(part * 4);
-    c->gemm_cnt = (int*)cv.take((size_t)groups * 4);
+    c->obuf = cv.take((size_t)D.maxM * D.d_pad * e);
+    c->ubuf = cv.take((size_t)D.maxM * D.F_pad * e);
     c->attn_part = (float*)cv.take(attention_partial_floats(D.maxB, D.H, D.maxQ, D.Dh) * 4);
-    c->attn_cnt = (int*)cv.take((size_t)D.maxB * D.H * 4);
     c->cache_len = (int*)cv.take((size_t)D.maxB * 4);
     c->err_flag = (int*)cv.take(4);
     c->verify_cnt = (int*)cv.take((size_t)D.maxB * 4);
@@ -208,15 +198,13 @@ void prof_end(sdsat_ctx* c, hipEvent_t start) {
 }
 
 // ---------------------------------------------------------------- GEMM helpers
-int run_gemm(sdsat_ctx* c, int kind, int xs, int ep, int M, int n_tiles, int k_steps, int N, int K,
-             const void* W, GemmArgs a) {
-    const GemmPlan p = plan_gemm(c->D.dtype, M, n_tiles, k_steps);
-    a.M = M; a.N = N; a.K = K; a.n_tiles = n_tiles; a.k_steps = k_steps;
-    a.splits = p.splits; a.chunk_steps = p.chunk_steps; a.W = W;
-    a.partial = c->gemm_part; a.counter = c->gemm_cnt; a.err = c->err_flag;
+int run_gemm(sdsat_ctx* c, int kind, int ep, int M, int n_tiles, int k_steps, int N, int K, const void* W,
+             GemmArgs a) {
+    const GemmPlan p = plan_gemm(M, n_tiles, k_steps);
+    a.M = M; a.N = N; a.K = K; a.n_tiles = n_tiles; a.k_steps = k_steps; a.W = W; a.err = c->err_flag;
     hipEvent_t ev;
     prof_begin(c, kind, &ev);
-    HIPCHK(c, launch_gemm(c->D.dtype, xs, ep, p, a, c->stream));
+    HIPCHK(c, launch_gemm(c->D.dtype, ep, p, a, c->stream));
     prof_end(c, ev);
     return SDSAT_OK;
 }
@@ -248,18 +236,19 @@ int fits(sdsat_ctx* c, int B, int q, bool* ok) {
 }
 
 int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask, const void* qbuf, void* out,
-                    int out_f32) {
+                    int out_f32, int ldo) {
     const Dims& D = c->D;
-    const AttnPlan p = plan_attention(B, D.H, q, max_hint(c, B));
+    const AttnPlan p = plan_attention(B, D.H, q, D.Dh, max_hint(c, B));
     AttnArgs a{};
     a.qbuf = qbuf; a.kc = layer_k(c, layer); a.vc = layer_v(c, layer);
     a.cache_len = c->cache_len; a.mask = mask;
-    a.B = B; a.q = q; a.H = D.H; a.S_max = D.S; a.chunk_keys = p.chunk_keys; a.n_chunks = p.n_chunks;
+    a.B = B; a.q = q; a.H = D.H; a.S_max = D.S;
     a.scale = (float)(1.0 / std::sqrt((double)D.Dh));
-    a.part = c->attn_part; a.counter = c->attn_cnt; a.out = out; a.out_f32 = out_f32; a.err = c->err_flag;
+    a.splits = p.splits; a.part = c->attn_part;
+    a.out = out; a.out_f32 = out_f32; a.ldo = ldo; a.err = c->err_flag;
     hipEvent_t ev;
     prof_begin(c, PK_ATTN, &ev);
-    HIPCHK(c, launch_attention(D.dtype, D.Dh, a, c->stream));
+    HIPCHK(c, launch_attention(D.dtype, D.Dh, p, a, c->stream));
     prof_end(c, ev);
     return SDSAT_OK;
 }
@@ -268,41 +257,42 @@ int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const 
     const Dims& D = c->D;
     const int M = B * q;
     hipEvent_t evb;
-    prof_begin(c, PK_BLOCK, &evb);
-    HIPCHK(c, launch_embed(D.dtype, c->embed, D.V + D.A, D.d, tokens, M, c->x, c->ssq, D.n_ssq, c->err_flag,
-                           c->stream));
+    prof_begin(c, logits ? PK_BLOCK : PK_PREFILL, &evb);
+    HIPCHK(c, launch_embed(D.dtype, c->embed, D.V + D.A, D.d, tokens, M, c->x, c->xb, D.d_pad, c->ssq, D.n_ssq,
+                           c->err_flag, c->stream));
     for (int l = 0; l < D.L; ++l) {
-        GemmArgs a{};
         // attention sub-block: RMSNorm -> QKV (+RoPE, KV write) -> attention -> O (+residual)
-        a.x = c->x; a.ldx = D.d; a.ssq = c->ssq; a.n_ssq = D.n_ssq; a.eps = c->cfg.rms_eps;
-        a.gain = c->attn_norm[l];
+        GemmArgs a{};
+        a.xa = c->xb; a.ldx = D.d_pad; a.ssq = c->ssq; a.n_ssq = D.n_ssq; a.eps = c->cfg.rms_eps;
         a.qbuf = c->qbuf; a.kc = layer_k(c, l); a.vc = layer_v(c, l);
         a.cache_len = c->cache_len; a.q = q; a.H = D.H; a.Dh = D.Dh; a.S_max = D.S; a.mask = mask;
-        a.rope_cos = c->rope_cos; a.rope_sin = c->rope_sin;
-        int rc = run_gemm(c, PK_QKV, XS_NORM, EP_QKV, M, D.nt_qkv, D.ks_d, 3 * D.d, D.d, c->w_qkv[l], a);
+        a.inv_freq = c->inv_freq;
+        int rc = run_gemm(c, PK_QKV, EP_QKV, M, D.nt_qkv, D.ks_d, 3 * D.d, D.d, c->w_qkv[l], a);
         if (rc) return rc;
-        rc = attention_layer(c, l, B, q, mask, c->qbuf, c->obuf, 0);
+        rc = attention_layer(c, l, B, q, mask, c->qbuf, c->obuf, 0, D.d_pad);
         if (rc) return rc;
         GemmArgs o{};
-        o.xa = c->obuf; o.ldx = D.d; o.resid = c->x; o.ldy = D.d; o.ssq_out = c->ssq;
-        rc = run_gemm(c, PK_O, XS_ACT, EP_RESID, M, D.nt_o, D.ks_d, D.d, D.d, c->w_o[l], o);
+        o.xa = c->obuf; o.ldx = D.d_pad; o.resid = c->x; o.ldy = D.d; o.xb = c->xb; o.ldxb = D.d_pad;
+        o.ssq_out = c->ssq;
+        rc = run_gemm(c, PK_O, EP_RESID, M, D.nt_o, D.ks_d, D.d, D.d, c->w_o[l], o);
         if (rc) return rc;
         // feed-forward sub-block: RMSNorm -> gate/up (+SwiGLU) -> down (+residual)
         GemmArgs f{};
-        f.x = c->x; f.ldx = D.d; f.ssq = c->ssq; f.n_ssq = D.n_ssq; f.eps = c->cfg.rms_eps;
-        f.gain = c->ffn_norm[l]; f.uout = c->ubuf; f.F = D.F;
-        rc = run_gemm(c, PK_GATEUP, XS_NORM, EP_SWIGLU, M, D.nt_gu, D.ks_d, 2 * D.F, D.d, c->w_gu[l], f);
+        f.xa = c->xb; f.ldx = D.d_pad; f.ssq = c->ssq; f.n_ssq = D.n_ssq; f.eps = c->cfg.rms_eps;
+        f.uout = c->ubuf; f.F = D.F; f.ldu = D.F_pad;
+        rc = run_gemm(c, PK_GATEUP, EP_SWIGLU, M, D.nt_gu, D.ks_d, 2 * D.F, D.d, c->w_gu[l], f);
         if (rc) return rc;
         GemmArgs dn{};
-        dn.xa = c->ubuf; dn.ldx = D.F; dn.resid = c->x; dn.ldy = D.d; dn.ssq_out = c->ssq;
-        rc = run_gemm(c, PK_DOWN, XS_ACT, EP_RESID, M, D.nt_down, D.ks_f, D.d, D.F, c->w_down[l], dn);
+        dn.xa = c->ubuf; dn.ldx = D.F_pad; dn.resid = c->x; dn.ldy = D.d; dn.xb = c->xb; dn.ldxb = D.d_pad;
+        dn.ssq_out = c->ssq;
+        rc = run_gemm(c, PK_DOWN, EP_RESID, M, D.nt_down, D.ks_f, D.d, D.F, c->w_down[l], dn);
         if (rc) return rc;
     }
     if (logits) {
         GemmArgs h{};
-        h.x = c->x; h.ldx = D.d; h.ssq = c->ssq; h.n_ssq = D.n_ssq; h.eps = c->cfg.rms_eps;
-        h.gain = c->final_norm; h.y = logits; h.ldy = D.V;
-        int rc = run_gemm(c, PK_LM, XS_NORM, EP_STORE, M, D.nt_lm, D.ks_d, D.V, D.d, c->w_lm, h);
+        h.xa = c->xb; h.ldx = D.d_pad; h.ssq = c->ssq; h.n_ssq = D.n_ssq; h.eps = c->cfg.rms_eps;
+        h.y = logits; h.ldy = D.V;
+        int rc = run_gemm(c, PK_LM, EP_STORE, M, D.nt_lm, D.ks_d, D.V, D.d, c->w_lm, h);
         if (rc) return rc;
     }
     prof_end(c, evb);
@@ -383,41 +373,41 @@ int sdsat_init(const sdsat_config* cfg, const void* const* weights, int32_t n_we
         PackArgs p{};
         p.dtype = D.dtype; p.K = D.d; p.k_steps = D.ks_d; p.head_dim = D.Dh; p.F = D.F;
         // Wq, Wk, Wv stacked, rows grouped for RoPE pairs
+        // Wq, Wk, Wv stacked, rows grouped for RoPE pairs, attn_norm gain folded in
         p.perm = PACK_ROPE; p.N = 3 * D.d; p.n_tiles = D.nt_qkv; p.src0 = w[1]; p.src1 = w[2]; p.src2 = w[3];
-        p.N0 = D.d; p.N1 = D.d; p.dst = c->w_qkv[l];
+        p.N0 = D.d; p.N1 = D.d; p.gain = (const float*)w[0]; p.dst = c->w_qkv[l];
         launch_pack(p, c->stream);
         p.perm = PACK_PLAIN; p.N = D.d; p.n_tiles = D.nt_o; p.src0 = w[4]; p.src1 = p.src2 = nullptr;
-        p.N0 = D.d; p.N1 = 0; p.dst = c->w_o[l];
+        p.N0 = D.d; p.N1 = 0; p.gain = nullptr; p.dst = c->w_o[l];
         launch_pack(p, c->stream);
+        // gate and up interleaved per tile, ffn_norm gain folded in
         p.perm = PACK_GATEUP; p.N = 2 * D.F; p.n_tiles = D.nt_gu; p.src0 = w[6]; p.src1 = w[7];
-        p.N0 = D.F; p.N1 = D.F; p.dst = c->w_gu[l];
+        p.N0 = D.F; p.N1 = D.F; p.gain = (const float*)w[5]; p.dst = c->w_gu[l];
         launch_pack(p, c->stream);
         p.perm = PACK_PLAIN; p.N = D.d; p.K = D.F; p.k_steps = D.ks_f; p.n_tiles = D.nt_down; p.src0 = w[8];
-        p.src1 = nullptr; p.N0 = D.d; p.N1 = 0; p.dst = c->w_down[l];
+        p.src1 = nullptr; p.N0 = D.d; p.N1 = 0; p.gain = nullptr; p.dst = c->w_down[l];
         launch_pack(p, c->stream);
     }
     c->final_norm = (const float*)weights[1 + 9 * D.L];
     {
         PackArgs p{};
         p.dtype = D.dtype; p.K = D.d; p.k_steps = D.ks_d; p.perm = PACK_PLAIN; p.N = D.V; p.n_tiles = D.nt_lm;
-        p.src0 = weights[2 + 9 * D.L]; p.N0 = D.V; p.dst = c->w_lm;
+        p.src0 = weights[2 + 9 * D.L]; p.N0 = D.V; p.gain = (const float*)weights[1 + 9 * D.L]; p.dst = c->w_lm;
         launch_pack(p, c->stream);
     }
     auto init_fail = [&](int code) { std::string m = c->err; delete c; return fail(nullptr, code, m); };
     if (hipGetLastError() != hipSuccess) { c->err = "weight packing launch failed"; return init_fail(SDSAT_EDEVICE); }
-    // rotary tables: angle = pos * base^(-2i/Dh) in double, cos/sin rounded to float
+    // rotary inverse frequencies base^(-2i/Dh), in double (the QKV epilogue forms
+    // the angle pos * inv_freq in double and rounds cos / sin to float)
     {
         const int half = D.Dh / 2;
-        std::vector<float> cs((size_t)D.S * half), sn((size_t)D.S * half);
-        for (int pos = 0; pos < D.S; ++pos)
-            for (int i = 0; i < half; ++i) {
-                const double inv = std::pow((double)cfg->rope_base, -2.0 * i / D.Dh);
-                const double ang = (double)pos * inv;
-                cs[(size_t)pos * half + i] = (float)std::cos(ang);
-                sn[(size_t)pos * half + i] = (float)std::sin(ang);
-            }
-        if (hipMemcpyAsync(c->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, c->stream) != hipSuccess ||
-            hipMemcpyAsync(c->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, c->stream) != hipSuccess) {
+        std::vector<double> inv(half);
+        for (int i = 0; i < half; ++i) inv[i] = std::pow((double)cfg->rope_base, -2.0 * i / D.Dh);
+        if (hipMemcpyAsync(c->inv_freq, inv.data(), inv.size() * 8, hipMemcpyHostToDevice, c->stream) != hipSuccess) {
+            c->err = "rotary table upload failed";
+            return init_fail(SDSAT_EDEVICE);
+        }
+        if (hipStreamSynchronize(c->stream) != hipSuccess) {   // the host vector goes out of scope
             c->err = "rotary table upload failed";
             return init_fail(SDSAT_EDEVICE);
         }
@@ -429,10 +419,10 @@ int sdsat_init(const sdsat_config* cfg, const void* const* weights, int32_t n_we
             c->err = "cache fill failed";
             return init_fail(SDSAT_EDEVICE);
         }
-        const int ngroups = gemm_groups(D.nt_lm > D.nt_gu ? (D.nt_lm > D.nt_qkv ? D.nt_lm : D.nt_qkv)
-                                                          : (D.nt_gu > D.nt_qkv ? D.nt_gu : D.nt_qkv));
-        (void)launch_fill_i32(c->gemm_cnt, ngroups, 0, c->stream);
-        (void)launch_fill_i32(c->attn_cnt, (size_t)D.maxB * D.H, 0, c->stream);
+        // activation pads must read as zero
+        (void)launch_fill_i32((int*)c->xb, (size_t)D.maxM * D.d_pad * D.esz / 4, 0, c->stream);
+        (void)launch_fill_i32((int*)c->obuf, (size_t)D.maxM * D.d_pad * D.esz / 4, 0, c->stream);
+        (void)launch_fill_i32((int*)c->ubuf, (size_t)D.maxM * D.F_pad * D.esz / 4, 0, c->stream);
         (void)launch_fill_i32(c->verify_cnt, D.maxB, 0, c->stream);
         (void)launch_fill_i32(c->cache_len, D.maxB, 0, c->stream);
         (void)launch_fill_i32(c->err_flag, 1, 0, c->stream);
@@ -675,7 +665,7 @@ int sdsat_attention(sdsat_ctx* c, int32_t layer, int32_t batch, int32_t q, const
     if (rc) return rc;
     if (!ok) return fail(c, SDSAT_ECAPACITY, "cache_len + q exceeds max_ctx");
     HIPCHK(c, launch_to_elem(D.dtype, d_q, c->qbuf, (size_t)batch * q * D.d, c->stream));
-    return attention_layer(c, layer, batch, q, d_ancestor_mask, c->qbuf, d_out, 1);
+    return attention_layer(c, layer, batch, q, d_ancestor_mask, c->qbuf, d_out, 1, D.d);
 }
 
 size_t sdsat_linear_packed_bytes(int32_t dtype, int32_t N, int32_t K) {
@@ -696,13 +686,7 @@ int sdsat_linear_pack(int32_t dtype, int32_t N, int32_t K, const void* d_w, void
 
 size_t sdsat_linear_scratch_bytes(int32_t M, int32_t N, int32_t K) {
     if (M < 1 || M > 64 || N < 1 || K < 1) return 0;
-    const int nt = (N + 15) / 16, ks = (K + 31) / 32;
-    size_t f = 0;
-    for (int dt = 0; dt < 2; ++dt) {
-        const GemmPlan p = plan_gemm(dt, M, nt, ks);
-        f = std::max(f, gemm_partial_floats(p, nt));
-    }
-    return align_up((size_t)gemm_groups(nt) * 4, 256) + f * 4;
+    return align_up((size_t)M * align_up((size_t)K, 32) * 4, 256);   // x converted to the matrix type
 }
 
 int sdsat_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const float* d_x, const void* d_packed, float* d_y,
@@ -710,20 +694,21 @@ int sdsat_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const float* d_
     if ((dtype != 0 && dtype != 1) || M < 1 || M > 64 || N < 1 || K < 1 || !d_x || !d_packed || !d_y || !d_scratch)
         return fail(nullptr, SDSAT_EINVAL, "bad linear arguments");
     const int nt = (N + 15) / 16, ks = (K + 31) / 32;
-    const GemmPlan p = plan_gemm(dtype, M, nt, ks);
+    hipStream_t st = (hipStream_t)hip_stream;
+    hipError_t e = launch_to_elem_rows(dtype, d_x, M, K, d_scratch, ks * 32, st);
+    if (e != hipSuccess) return fail(nullptr, SDSAT_EDEVICE, std::string("linear input: ") + hipGetErrorString(e));
+    const GemmPlan p = plan_gemm(M, nt, ks);
     GemmArgs a{};
-    a.M = M; a.N = N; a.K = K; a.n_tiles = nt; a.k_steps = ks; a.splits = p.splits; a.chunk_steps = p.chunk_steps;
-    a.W = d_packed; a.x = d_x; a.ldx = K; a.y = d_y; a.ldy = N;
-    a.counter = (int*)d_scratch;
-    a.partial = (float*)((char*)d_scratch + align_up((size_t)gemm_groups(nt) * 4, 256));
-    hipError_t e = launch_gemm(dtype, XS_F32, EP_STORE, p, a, (hipStream_t)hip_stream);
+    a.M = M; a.N = N; a.K = K; a.n_tiles = nt; a.k_steps = ks; a.W = d_packed;
+    a.xa = d_scratch; a.ldx = ks * 32; a.y = d_y; a.ldy = N;
+    e = launch_gemm(dtype, EP_STORE, p, a, st);
     if (e != hipSuccess) return fail(nullptr, SDSAT_EDEVICE, std::string("linear launch: ") + hipGetErrorString(e));
     return SDSAT_OK;
 }
 
 int sdsat_profile_kernel(sdsat_ctx* c, int32_t kind) {
     if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
-    if (kind < 0 || kind > 7) return fail(c, SDSAT_EINVAL, "bad kernel kind");
+    if (kind < 0 || kind > 8) return fail(c, SDSAT_EINVAL, "bad kernel kind");
     HIPCHK(c, hipStreamSynchronize(c->stream));
     c->prof_kind = kind;
     c->ev_used = 0;

@@ -6,70 +6,142 @@
 //   the block rows r may see (0..r, or the rows set in its ancestor mask).
 // The block's own K/V rows were written into slots L_b.. by the QKV epilogue.
 //
-// Work split (flash-decoding): one wave per (b, h, key chunk).  Per 32 keys a
-// wave computes the 32 x q score tile S^T = K Q^T on the matrix cores (A = K
-// rows straight from the cache, B = Q^T from registers), runs an online
-// softmax per query row (query rows live in lanes, keys in registers and lane
-// groups), and accumulates O^T = V^T P^T with A = V^T read from the cache's
-// key-permuted 32-key blocks (vperm) and B = P^T taken from the score
-// registers as they are.  Chunks are merged by the last-arriving wave of each
-// (b, h) with a log-sum-exp combine, in chunk order.
+// One workgroup per (b, h).  Its waves take contiguous runs of 32-key blocks.
+// Per block a wave computes the 32 x q score tile S^T = K Q^T on the matrix
+// cores (A = K rows straight from the cache, B = Q^T from registers), runs an
+// online softmax per query row (query rows live in lanes, keys in registers
+// and lane groups), and accumulates O^T = V^T P^T with A = V^T read from the
+// cache's key-permuted 32-key blocks (vperm) and B = P^T taken from the score
+// registers as they are.  The next block's K and V are in flight while the
+// current one is computed.  The waves' partial results are merged in LDS with
+// a log-sum-exp combine in wave order (deterministic; no global scratch).
 #include "device.h"
 #include "kernels.h"
 
 namespace sdsat {
 
-static constexpr int kMaxChunks = 32;
-static constexpr int kMinChunkKeys = 64;
-static constexpr int kTargetWaves = 4096;
+static constexpr int kMaxWaves = 8;
+static constexpr int kMaxSplits = 8;
 
-AttnPlan plan_attention(int B, int H, int q, int max_len) {
+// When the (b, h) pairs alone cannot fill the GPU, each pair's key blocks are
+// split over up to 8 workgroups.  Waves per workgroup: about two 32-key blocks
+// each, at most 8 / MT (LDS holds waves x Dh/16 x MT tiles of 1 KiB).
+AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len) {
     AttnPlan p;
-    const int T = max_len + q;
-    int want = kTargetWaves / (B * H);
-    want = want < 1 ? 1 : (want > kMaxChunks ? kMaxChunks : want);
-    int ck = (T + want - 1) / want;
-    ck = (ck + 31) / 32 * 32;
-    if (ck < kMinChunkKeys) ck = kMinChunkKeys;
-    int n = (T + ck - 1) / ck;
-    if (n > kMaxChunks) {   // cannot happen with want <= kMaxChunks, kept as a guard
-        ck = ((T + kMaxChunks - 1) / kMaxChunks + 31) / 32 * 32;
-        n = (T + ck - 1) / ck;
-    }
-    p.chunk_keys = ck;
-    p.n_chunks = n;
-    p.grid = B * H * n;
+    const int mt = (q + 15) / 16;
+    const int nblk = (max_len + q + 31) / 32;
+    const int pairs = B * H;
+    int splits = pairs >= 256 ? 1 : (256 + pairs - 1) / pairs;
+    if (splits > kMaxSplits) splits = kMaxSplits;
+    if (splits > nblk) splits = nblk;
+    if (splits < 1) splits = 1;
+    const int per_split = (nblk + splits - 1) / splits;
+    int w = (per_split + 1) / 2;
+    if (w > kMaxWaves / mt) w = kMaxWaves / mt;
+    if (w < 1) w = 1;
+    p.waves = w;
+    p.splits = splits;
+    p.grid = pairs * splits;
+    p.lds_bytes = w * (head_dim / 16) * mt * 64 * 16;
     return p;
 }
 
-// per (b, h, chunk): MT*16 rows x (Dh + 4) floats (unnormalised O, max, sum, 2 pad for 16-byte rows)
 size_t attention_partial_floats(int B, int H, int q_max, int head_dim) {
-    const int rows = (q_max + 15) / 16 * 16;
-    return (size_t)B * H * kMaxChunks * rows * (head_dim + 4);
+    return (size_t)B * H * kMaxSplits * ((q_max + 15) / 16 * 16) * (head_dim + 4);
+}
+
+template <typename T, int NDS, int NDT>
+__device__ __forceinline__ void load_kv(Frag<T> (&kf)[2][NDS], Frag<T> (&vf)[NDT], const T* kbase, const T* vbase,
+                                        int blk, int c, int g) {
+    constexpr int DH = NDS * 32;
+    const int kb0 = blk * 32;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int ds = 0; ds < NDS; ++ds)
+            kf[kt][ds] = Frag<T>::load(kbase + (size_t)(kb0 + 16 * kt + c) * DH + ds * 32 + 8 * g);
+    const T* vblk = vbase + (size_t)blk * DH * 32;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) vf[dt] = Frag<T>::load(vblk + (size_t)(dt * 16 + c) * 32 + 8 * g);
+}
+
+template <typename T, int NDS, int NDT, int MT>
+__device__ __forceinline__ void attend_block(const Frag<T> (&kf)[2][NDS], const Frag<T> (&vf)[NDT],
+                                             const Frag<T> (&qf)[NDS][MT], const uint64_t (&mrow)[MT], int blk,
+                                             int L, int Tb, int q, bool tree, float scale, int c, int g,
+                                             float (&rmax)[MT], float (&rsum)[MT], f32x4_t (&o)[NDT][MT]) {
+    const int kb0 = blk * 32;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        f32x4_t s0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+#pragma unroll
+        for (int ds = 0; ds < NDS; ++ds) {
+            mma(s0, kf[0][ds], qf[ds][mt]);
+            mma(s1, kf[1][ds], qf[ds][mt]);
+        }
+        // s0[r], s1[r] = S^T[key = kb0 + 16kt + 4g + r][m = 16mt + c]
+        const int m = 16 * mt + c;
+        float sv[8];
+        bool vis[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int key = kb0 + (i < 4 ? 4 * g + i : 16 + 4 * g + (i - 4));
+            bool v = key < Tb && m < q;
+            if (tree) v = v && (key < L || ((mrow[mt] >> (key - L)) & 1ull));
+            else v = v && key <= L + m;
+            vis[i] = v;
+            sv[i] = (i < 4 ? s0[i] : s1[i - 4]) * scale;
+        }
+        float bm = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) if (vis[i]) bm = fmaxf(bm, sv[i]);
+        bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
+        bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+        const float nmax = fmaxf(rmax[mt], bm);
+        const float alpha = rmax[mt] == -INFINITY ? 0.f : expf(rmax[mt] - nmax);
+        float p[8];
+        float ps = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            p[i] = vis[i] ? expf(sv[i] - nmax) : 0.f;
+            ps += p[i];
+        }
+        rsum[mt] = rsum[mt] * alpha + ps;
+        rmax[mt] = nmax;
+        const Frag<T> pf = Frag<T>::from_f32(p);
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+            o[dt][mt] *= alpha;
+            mma(o[dt][mt], vf[dt], pf);
+        }
+    }
 }
 
 template <typename T, int DH, int MT>
-__global__ void __launch_bounds__(64) attn_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     constexpr int NDS = DH / 32;   // 32-wide steps over the head dimension
     constexpr int NDT = DH / 16;   // 16-row output tiles over the head dimension
-    const int lane = threadIdx.x, c = lane & 15, g = lane >> 4;
-    const int bh = blockIdx.x / a.n_chunks, chunk = blockIdx.x % a.n_chunks;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    f32x4_t* opart = reinterpret_cast<f32x4_t*>(smem_raw);   // [waves][NDT][MT][64]
+    __shared__ float s_max[kMaxWaves][64], s_sum[kMaxWaves][64];
+
+    const int nw = blockDim.x >> 6;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, c = lane & 15, g = lane >> 4;
+    const int bh = blockIdx.x / a.splits, sp = blockIdx.x % a.splits;
     const int b = bh / a.H, h = bh % a.H;
     const int q = a.q;
     const int L = a.cache_len[b];
     const int Tb = L + q;
     if (Tb > a.S_max) {   // the host checks capacity; never read past this sequence's cache
-        if (lane == 0 && chunk == 0) atomicOr(a.err, 4);
+        if (threadIdx.x == 0) atomicOr(a.err, 4);
         return;
     }
-    const int n_chunks = (Tb + a.chunk_keys - 1) / a.chunk_keys;
-    if (n_chunks > a.n_chunks) {   // launch planned for a shorter cache: flag it, touch nothing
-        if (lane == 0 && chunk == 0) atomicOr(a.err, 8);
-        return;
-    }
-    if (chunk >= n_chunks) return;
-    const int k_lo = chunk * a.chunk_keys;
-    const int k_hi = min(Tb, k_lo + a.chunk_keys);
+    const int nblk = (Tb + 31) / 32;
+    const int per_wg = (nblk + a.splits - 1) / a.splits;   // this workgroup: blocks [wlo, whi)
+    const int wlo = sp * per_wg, whi = min(nblk, wlo + per_wg);
+    const int per = (max(0, whi - wlo) + nw - 1) / nw;
+    const int blo = wlo + wave * per;
+    const int bhi = min(whi, blo + per);
 
     const T* qb = reinterpret_cast<const T*>(a.qbuf);
     Frag<T> qf[NDS][MT];
@@ -83,9 +155,9 @@ __global__ void __launch_bounds__(64) attn_kernel(AttnArgs a) {
             qf[ds][mt] = m < q ? Frag<T>::load(qb + (((size_t)b * q + m) * a.H + h) * DH + ds * 32 + 8 * g)
                                : Frag<T>::zero();
     }
-
     const T* kbase = reinterpret_cast<const T*>(a.kc) + ((size_t)b * a.H + h) * a.S_max * DH;
     const T* vbase = reinterpret_cast<const T*>(a.vc) + ((size_t)b * a.H + h) * a.S_max * DH;
+    const bool tree = a.mask != nullptr;
 
     float rmax[MT], rsum[MT];
     f32x4_t o[NDT][MT];
@@ -97,157 +169,155 @@ __global__ void __launch_bounds__(64) attn_kernel(AttnArgs a) {
         for (int dt = 0; dt < NDT; ++dt) o[dt][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
 
-    for (int kb0 = k_lo; kb0 < k_hi; kb0 += 32) {
-        // scores: s[kt][mt][r] = S^T[key = kb0 + 16kt + 4g + r][m = 16mt + c]
-        Frag<T> kf[2][NDS];
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-            for (int ds = 0; ds < NDS; ++ds)
-                kf[kt][ds] = Frag<T>::load(kbase + (size_t)(kb0 + 16 * kt + c) * DH + ds * 32 + 8 * g);
-        Frag<T> vf[NDT];
-        const T* vblk = vbase + (size_t)(kb0 / 32) * DH * 32;
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) vf[dt] = Frag<T>::load(vblk + (size_t)(dt * 16 + c) * 32 + 8 * g);
-
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            f32x4_t s0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, s1 = s0;
-#pragma unroll
-            for (int ds = 0; ds < NDS; ++ds) {
-                mma(s0, kf[0][ds], qf[ds][mt]);
-                mma(s1, kf[1][ds], qf[ds][mt]);
-            }
-            const int m = 16 * mt + c;
-            float sv[8];
-            bool vis[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int key = kb0 + (i < 4 ? 4 * g + i : 16 + 4 * g + (i - 4));
-                bool v = key < Tb && m < q;
-                if (a.mask) v = v && (key < L || ((mrow[mt] >> (key - L)) & 1ull));
-                else v = v && key <= L + m;
-                vis[i] = v;
-                sv[i] = (i < 4 ? s0[i] : s1[i - 4]) * a.scale;
-            }
-            float bm = -INFINITY;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) if (vis[i]) bm = fmaxf(bm, sv[i]);
-            bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
-            bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
-            const float nmax = fmaxf(rmax[mt], bm);
-            const float alpha = rmax[mt] == -INFINITY ? 0.f : expf(rmax[mt] - nmax);
-            float p[8];
-            float ps = 0.f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                p[i] = vis[i] ? expf(sv[i] - nmax) : 0.f;
-                ps += p[i];
-            }
-            rsum[mt] = rsum[mt] * alpha + ps;
-            rmax[mt] = nmax;
-            const Frag<T> pf = Frag<T>::from_f32(p);
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) {
-                o[dt][mt] *= alpha;
-                mma(o[dt][mt], vf[dt], pf);
-            }
+    if (blo < bhi) {
+        Frag<T> kA[2][NDS], kB[2][NDS], vA[NDT], vB[NDT];
+        load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, blo, c, g);
+        for (int blk = blo; blk < bhi; blk += 2) {
+            // next block in flight (clamped: a duplicate load past the run is not used)
+            load_kv<T, NDS, NDT>(kB, vB, kbase, vbase, min(blk + 1, bhi - 1), c, g);
+            attend_block<T, NDS, NDT, MT>(kA, vA, qf, mrow, blk, L, Tb, q, tree, a.scale, c, g, rmax, rsum, o);
+            load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, min(blk + 2, bhi - 1), c, g);
+            if (blk + 1 < bhi)
+                attend_block<T, NDS, NDT, MT>(kB, vB, qf, mrow, blk + 1, L, Tb, q, tree, a.scale, c, g, rmax, rsum,
+                                              o);
         }
     }
-    // o[dt][mt][r] = unnormalised O^T[d = 16dt + 4g + r][m = 16mt + c]
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
         rsum[mt] += __shfl_xor(rsum[mt], 16, 64);
         rsum[mt] += __shfl_xor(rsum[mt], 32, 64);
-    }
-
-    if (n_chunks > 1) {
-        const int rows = MT * 16;
-        float* part = a.part + ((size_t)bh * kMaxChunks + chunk) * rows * (DH + 4);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const int m = 16 * mt + c;
-            float* pr = part + (size_t)m * (DH + 4);
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt)
-                *reinterpret_cast<f32x4_t*>(pr + 16 * dt + 4 * g) = o[dt][mt];
-            if (g == 0) { pr[DH] = rmax[mt]; pr[DH + 1] = rsum[mt]; }
+        if (g == 0) {
+            s_max[wave][16 * mt + c] = rmax[mt];
+            s_sum[wave][16 * mt + c] = rsum[mt];
         }
-        __threadfence();
-        __shared__ int s_last;
-        if (lane == 0) s_last = atomicAdd(&a.counter[bh], 1) == n_chunks - 1;
-        __syncthreads();
-        if (!s_last) return;
-        __threadfence();
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const int m = 16 * mt + c;
-            float gmax = -INFINITY;
-            for (int ch = 0; ch < n_chunks; ++ch) {
-                const float* pr = a.part + (((size_t)bh * kMaxChunks + ch) * rows + m) * (DH + 4);
-                gmax = fmaxf(gmax, pr[DH]);
-            }
-            float den = 0.f;
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) o[dt][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            for (int ch = 0; ch < n_chunks; ++ch) {
-                const float* pr = a.part + (((size_t)bh * kMaxChunks + ch) * rows + m) * (DH + 4);
-                const float cm = pr[DH];
-                const float w = cm == -INFINITY ? 0.f : expf(cm - gmax);
-                den += w * pr[DH + 1];
-#pragma unroll
-                for (int dt = 0; dt < NDT; ++dt)
-                    o[dt][mt] += w * *reinterpret_cast<const f32x4_t*>(pr + 16 * dt + 4 * g);
-            }
-            rsum[mt] = den;
-        }
-        if (lane == 0) a.counter[bh] = 0;
     }
-    // normalise and store O[b*q + m][h*DH + d]
+    __syncthreads();
+    // rescale this wave's partial to the common maximum and park it in LDS
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
         const int m = 16 * mt + c;
-        if (m >= q) continue;
-        const float inv = 1.0f / rsum[mt];
-        const size_t row = ((size_t)b * q + m) * a.H * DH + (size_t)h * DH;
+        float gmax = -INFINITY;
+        for (int w = 0; w < nw; ++w) gmax = fmaxf(gmax, s_max[w][m]);
+        const float alpha = rmax[mt] == -INFINITY ? 0.f : expf(rmax[mt] - gmax);
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-            const int d = 16 * dt + 4 * g;
-            if (a.out_f32) {
-                float* po = reinterpret_cast<float*>(a.out) + row + d;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) po[r] = o[dt][mt][r] * inv;
-            } else {
-                T* po = reinterpret_cast<T*>(a.out) + row + d;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) po[r] = to_elem<T>(o[dt][mt][r] * inv);
-            }
+        for (int dt = 0; dt < NDT; ++dt) opart[((wave * NDT + dt) * MT + mt) * 64 + lane] = o[dt][mt] * alpha;
+    }
+    __syncthreads();
+    // sum the partials in wave order; output tiles are spread over the waves
+    for (int t = wave; t < NDT * MT; t += nw) {
+        const int dt = t / MT, mt = t % MT;
+        const int m = 16 * mt + c;
+        float gmax = -INFINITY;
+        for (int w = 0; w < nw; ++w) gmax = fmaxf(gmax, s_max[w][m]);
+        float den = 0.f;
+        f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int w = 0; w < nw; ++w) {
+            const float wm = s_max[w][m];
+            den += wm == -INFINITY ? 0.f : expf(wm - gmax) * s_sum[w][m];
+            acc += opart[((w * NDT + dt) * MT + mt) * 64 + lane];
         }
+        const int d = 16 * dt + 4 * g;
+        if (a.splits > 1) {
+            // partial of this workgroup: O scaled to its row maximum, the maximum, the sum
+            float* pr = a.part + (((size_t)bh * a.splits + sp) * (MT * 16) + m) * (DH + 4);
+            *reinterpret_cast<f32x4_t*>(pr + d) = acc;
+            if (dt == 0 && g == 0) { pr[DH] = gmax; pr[DH + 1] = den; }
+            continue;
+        }
+        if (m >= q) continue;
+        const float inv = 1.0f / den;
+        const size_t row = ((size_t)b * q + m) * a.ldo + (size_t)h * DH;
+        if (a.out_f32) {
+            float* po = reinterpret_cast<float*>(a.out) + row + d;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) po[r] = acc[r] * inv;
+        } else {
+            T* po = reinterpret_cast<T*>(a.out) + row + d;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) po[r] = to_elem<T>(acc[r] * inv);
+        }
+    }
+}
+
+// Combine the split partials: one thread per (b, h, row, 4 head dims),
+// log-sum-exp over the splits in split order, all partial loads in flight at once.
+template <typename T, int DH>
+__global__ void __launch_bounds__(64) attn_combine_kernel(AttnArgs a, int rows) {
+    constexpr int D4 = DH / 4;
+    const int e = blockIdx.x * 64 + threadIdx.x;          // over B*H*q*D4
+    if (e >= a.B * a.H * a.q * D4) return;
+    const int d = 4 * (e % D4);
+    const int m = (e / D4) % a.q;
+    const int bh = e / (D4 * a.q);
+    const int b = bh / a.H, h = bh % a.H;
+    if (a.cache_len[b] + a.q > a.S_max) return;   // flagged by the partial kernel
+    const float* base = a.part + ((size_t)bh * a.splits * rows + m) * (DH + 4);
+    const size_t sstride = (size_t)rows * (DH + 4);
+    float mx[kMaxSplits], sm[kMaxSplits];
+    f32x4_t ov[kMaxSplits];
+#pragma unroll
+    for (int sp = 0; sp < kMaxSplits; ++sp) {
+        if (sp < a.splits) {
+            const float* pr = base + sp * sstride;
+            mx[sp] = pr[DH];
+            sm[sp] = pr[DH + 1];
+            ov[sp] = *reinterpret_cast<const f32x4_t*>(pr + d);
+        }
+    }
+    float gmax = -INFINITY;
+#pragma unroll
+    for (int sp = 0; sp < kMaxSplits; ++sp) if (sp < a.splits) gmax = fmaxf(gmax, mx[sp]);
+    float den = 0.f;
+    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int sp = 0; sp < kMaxSplits; ++sp) {
+        if (sp < a.splits) {
+            const float w = mx[sp] == -INFINITY ? 0.f : expf(mx[sp] - gmax);
+            den += w * sm[sp];
+            acc += w * ov[sp];
+        }
+    }
+    const float inv = 1.0f / den;
+    const size_t row = ((size_t)b * a.q + m) * a.ldo + (size_t)h * DH + d;
+    if (a.out_f32) {
+        float* po = reinterpret_cast<float*>(a.out) + row;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) po[r] = acc[r] * inv;
+    } else {
+        T* po = reinterpret_cast<T*>(a.out) + row;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) po[r] = to_elem<T>(acc[r] * inv);
     }
 }
 
 template <typename T, int DH>
-static hipError_t launch_dh(const AttnArgs& a, int grid, hipStream_t s) {
+static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s) {
     const int mt = (a.q + 15) / 16;
+    const dim3 grid(p.grid), block(64 * p.waves);
     switch (mt) {
-        case 1: hipLaunchKernelGGL((attn_kernel<T, DH, 1>), dim3(grid), dim3(64), 0, s, a); break;
-        case 2: hipLaunchKernelGGL((attn_kernel<T, DH, 2>), dim3(grid), dim3(64), 0, s, a); break;
-        case 3: hipLaunchKernelGGL((attn_kernel<T, DH, 3>), dim3(grid), dim3(64), 0, s, a); break;
-        case 4: hipLaunchKernelGGL((attn_kernel<T, DH, 4>), dim3(grid), dim3(64), 0, s, a); break;
+        case 1: hipLaunchKernelGGL((attn_kernel<T, DH, 1>), grid, block, p.lds_bytes, s, a); break;
+        case 2: hipLaunchKernelGGL((attn_kernel<T, DH, 2>), grid, block, p.lds_bytes, s, a); break;
+        case 3: hipLaunchKernelGGL((attn_kernel<T, DH, 3>), grid, block, p.lds_bytes, s, a); break;
+        case 4: hipLaunchKernelGGL((attn_kernel<T, DH, 4>), grid, block, p.lds_bytes, s, a); break;
         default: return hipErrorInvalidValue;
     }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.splits <= 1) return e;
+    const int n = a.B * a.H * a.q * (DH / 4);
+    hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3((n + 63) / 64), dim3(64), 0, s, a, mt * 16);
     return hipGetLastError();
 }
 
-hipError_t launch_attention(int dtype, int head_dim, const AttnArgs& a, hipStream_t s) {
-    const int grid = a.B * a.H * a.n_chunks;
-    if (a.q < 1 || a.q > 64 || a.n_chunks > kMaxChunks) return hipErrorInvalidValue;
+hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s) {
+    if (a.q < 1 || a.q > 64 || p.waves < 1 || p.waves > kMaxWaves || a.splits < 1 || a.splits > kMaxSplits ||
+        a.splits != p.splits || (a.splits > 1 && !a.part))
+        return hipErrorInvalidValue;
     if (dtype == 1) {
-        if (head_dim == 128) return launch_dh<uint16_t, 128>(a, grid, s);
-        if (head_dim == 64) return launch_dh<uint16_t, 64>(a, grid, s);
+        if (head_dim == 128) return launch_dh<uint16_t, 128>(p, a, s);
+        if (head_dim == 64) return launch_dh<uint16_t, 64>(p, a, s);
     } else {
-        if (head_dim == 128) return launch_dh<float, 128>(a, grid, s);
-        if (head_dim == 64) return launch_dh<float, 64>(a, grid, s);
+        if (head_dim == 128) return launch_dh<float, 128>(p, a, s);
+        if (head_dim == 64) return launch_dh<float, 64>(p, a, s);
     }
     return hipErrorInvalidValue;
 }

@@ -5,20 +5,21 @@
 //
 //  * W is pre-packed (launch_pack) into 16-column x 32-k tiles laid out in lane
 //    order, so every wave-wide load is one contiguous 1 KiB (bf16) run and each
-//    lane's 16 bytes is directly its matrix-core B fragment: no LDS for W.
-//  * A workgroup = 4 waves = 4 adjacent column tiles (64 outputs) over one
-//    k-chunk.  The chunk of X (normalised and rounded to the matrix-core input
-//    type when the prologue is an RMSNorm) is staged once in LDS and shared by
-//    the 4 waves.
-//  * Split-K over workgroups gives ~1000 workgroups per launch, enough loads in
-//    flight on 256 CUs.  Partial tiles go to scratch; the last workgroup of a
-//    column group (device-scope counter) sums them in split order, so results
-//    are deterministic, and runs the fused epilogue:
+//    lane's 16 bytes is directly its matrix-core B fragment.  RMSNorm gains are
+//    folded into the packed columns, so a normalised input is the raw residual
+//    row times a per-row scale applied in the epilogue.
+//  * One workgroup per column tile.  Its waves split the contraction into
+//    contiguous slices, stream their slice with two batches of loads in flight,
+//    read the X fragments for the same steps straight from global memory (the
+//    few X rows stay in L2), and reduce their partial tiles through LDS in
+//    wave order: deterministic, with no device-scope fences or atomics.
+//  * Fused epilogues, run by wave 0 on the reduced tile:
 //      EP_STORE   float output (LM-head logits)
 //      EP_QKV     RoPE on Q and K columns, Q to its buffer, K and V into the
 //                 cache slots of the block rows (positions cache_len[b] + r)
-//      EP_RESID   residual add into the float residual stream, plus per-tile
-//                 sums of squares that the next RMSNorm prologue reduces
+//      EP_RESID   residual add into the float residual stream, a copy in the
+//                 matrix element type for the next GEMM, and per-tile sums of
+//                 squares that the next RMSNorm reduces
 //      EP_SWIGLU  silu(gate) * up, rounded to the activation type
 #include "device.h"
 #include "kernels.h"
@@ -60,7 +61,12 @@ __global__ void pack_kernel(PackArgs a) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         const int k = 32 * ks + 8 * g + e;
-        dst[e] = (src && k < a.K) ? src[r * a.K + k] : T(0);
+        float v = 0.f;
+        if (src && k < a.K) {
+            v = to_f32<T>(src[r * a.K + k]);
+            if (a.gain) v *= a.gain[k];
+        }
+        dst[e] = to_elem<T>(v);
     }
 }
 
@@ -71,135 +77,155 @@ void launch_pack(const PackArgs& a, hipStream_t s) {
     else hipLaunchKernelGGL(pack_kernel<float>, dim3(blocks), dim3(256), 0, s, a);
 }
 
-int gemm_groups(int n_tiles) { return (n_tiles + 3) / 4; }
-
-static constexpr int kLdsBudget = 48 * 1024;
-static constexpr int kTargetWorkgroups = 1024;
-
-GemmPlan plan_gemm(int dtype, int M, int n_tiles, int k_steps) {
+// Waves per workgroup (measured on MI355X at M = 6 with weights streamed from
+// HBM): 8 for the narrow [d, d] / [d, F] matrices, 4 for the wide ones; at
+// least 4 contraction steps per wave; at most 8 waves when M > 32 (LDS for the
+// cross-wave reduction).
+GemmPlan plan_gemm(int M, int n_tiles, int k_steps) {
     GemmPlan p;
     p.mt = (M + 15) / 16;
-    const int groups = gemm_groups(n_tiles);
-    const int esz = dtype == 1 ? 2 : 4;
-    int splits = (kTargetWorkgroups + groups - 1) / groups;
-    splits = splits < 1 ? 1 : splits;
-    const int max_splits = k_steps / 4 > 0 ? k_steps / 4 : 1;
-    if (splits > max_splits) splits = max_splits;
-    int chunk = (k_steps + splits - 1) / splits;
-    // the LDS copy of the X chunk must fit
-    const int max_chunk = kLdsBudget / (M * (32 * esz) + 16 * M);
-    if (chunk > max_chunk) chunk = max_chunk > 0 ? max_chunk : 1;
-    splits = (k_steps + chunk - 1) / chunk;
-    p.splits = splits;
-    p.chunk_steps = chunk;
-    p.grid = groups * splits;
-    p.lds_bytes = M * (chunk * 32 * esz + 16);
+    int w = n_tiles <= 512 ? 8 : 4;
+    while (w > 1 && k_steps < 4 * w) w /= 2;
+    p.waves = w;
+    p.grid = n_tiles;
+    p.lds_bytes = w * p.mt * 64 * 16;
     return p;
 }
 
-size_t gemm_partial_floats(const GemmPlan& p, int n_tiles) {
-    if (p.splits <= 1) return 0;
-    return (size_t)gemm_groups(n_tiles) * p.splits * 4 * p.mt * 64 * 4;
+// Steps per load batch (two batches in flight), sized so both batches of
+// weight and X fragments fit the 128-VGPR budget of 16 waves per CU.
+template <typename T, int MT> struct Batch {
+    static constexpr int U = sizeof(T) == 2 ? (MT == 1 ? 4 : 2) : (MT == 1 ? 2 : 1);
+};
+
+template <typename T, int MT, int U>
+__device__ __forceinline__ void load_batch(Frag<T> (&w)[U], Frag<T> (&x)[U][MT], const T* wp,
+                                           const T* const (&xr)[MT], const bool (&xok)[MT], int s, int nks) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int st = min(s + u, nks - 1);   // past the slice: reload the last step, with zero X
+        w[u] = Frag<T>::load_nt(wp + (size_t)st * 512);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            x[u][mt] = (xok[mt] && s + u < nks) ? Frag<T>::load(xr[mt] + st * 32) : Frag<T>::zero();
+    }
 }
 
-template <typename T, int XS, int EP, int MT>
-__global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
-    extern __shared__ __align__(16) unsigned char smem_raw[];
-    T* xs = reinterpret_cast<T*>(smem_raw);
-    __shared__ float s_inv[64];
-    __shared__ int s_last;
+template <typename T, int MT, int U>
+__device__ __forceinline__ void mma_batch(f32x4_t (&acc)[MT], const Frag<T> (&w)[U], const Frag<T> (&x)[U][MT]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) mma(acc[mt], x[u][mt], w[u]);
+}
 
+template <typename T, int EP, int MT>
+__global__ void __launch_bounds__(1024) gemm_kernel(GemmArgs a) {
+    constexpr int U = Batch<T, MT>::U;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    f32x4_t* red = reinterpret_cast<f32x4_t*>(smem_raw);   // [waves][MT][64]
+    __shared__ float s_inv[64];
+
+    const int nw = blockDim.x >> 6;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int c = lane & 15, g = lane >> 4;
-    const int group = blockIdx.x / a.splits, split = blockIdx.x % a.splits;
-    const int ks0 = split * a.chunk_steps;
-    const int ks1 = min(a.k_steps, ks0 + a.chunk_steps);
-    const int nks = ks1 - ks0;
-    const int kc = nks * 32;
-    const int ldl = kc + 16 / (int)sizeof(T);   // LDS row stride in elements (+16 bytes)
+    const int tile = blockIdx.x;
     const int M = a.M;
 
-    // ---- prologue: X chunk -> LDS (rows < M only)
-    if (XS == XS_NORM) {
-        for (int m = wave; m < M; m += 4) {
-            float s = 0.f;
-            for (int t = lane; t < a.n_ssq; t += 64) s += a.ssq[(size_t)m * a.n_ssq + t];
-            s = wave_sum(s);
-            if (lane == 0) s_inv[m] = 1.0f / sqrtf(s / (float)a.K + a.eps);
-        }
-        __syncthreads();
-    }
-    const int kbase = ks0 * 32;
-    for (int idx = threadIdx.x * 4; idx < M * kc; idx += 256 * 4) {
-        const int m = idx / kc, kk = idx - m * kc;
-        const int k = kbase + kk;
-        T* d = xs + m * ldl + kk;
+    // this wave's contiguous slice of the contraction steps
+    const int chunk = (a.k_steps + nw - 1) / nw;
+    const int ks0 = wave * chunk;
+    const int nks = max(0, min(a.k_steps, ks0 + chunk) - ks0);
+    const T* wp = reinterpret_cast<const T*>(a.W) + (((size_t)tile * a.k_steps + ks0) * 64 + lane) * 8;
+    const T* xr[MT];
+    bool xok[MT];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            float v = 0.f;
-            if (k + j < a.K) {
-                if (XS == XS_ACT) {
-                    d[j] = reinterpret_cast<const T*>(a.xa)[(size_t)m * a.ldx + k + j];
-                    continue;
-                }
-                v = a.x[(size_t)m * a.ldx + k + j];
-                if (XS == XS_NORM) v = v * s_inv[m] * a.gain[k + j];
-            }
-            d[j] = to_elem<T>(v);
-        }
+    for (int mt = 0; mt < MT; ++mt) {
+        const int m = 16 * mt + c;
+        xok[mt] = m < M;
+        xr[mt] = reinterpret_cast<const T*>(a.xa) + (size_t)(xok[mt] ? m : 0) * a.ldx + ks0 * 32 + 8 * g;
     }
-    __syncthreads();
 
-    // ---- main loop: stream this wave's column tile over the k-chunk
-    const int tile = group * 4 + wave;
-    const bool tile_ok = tile < a.n_tiles;
+    // Loads whose values are only needed after the main loop are issued first:
+    // RMSNorm partial sums (wave w takes rows w, w+nw, ... <= 2 per wave),
+    // and wave 0's epilogue inputs (residual values, cache lengths, rotary
+    // inverse frequencies).  vmcnt is in order, so they never stall the stream.
+    constexpr int NSQ = 4;   // ssq partials per lane and row (n_ssq <= 256)
+    float sq[2][NSQ];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int t = 0; t < NSQ; ++t) {
+            const int m = wave + j * nw, col = lane + 64 * t;
+            sq[j][t] = (a.ssq && m < M && col < a.n_ssq) ? a.ssq[(size_t)m * a.n_ssq + col] : 0.f;
+        }
+    float ep_in[MT][4];    // EP_RESID: residual value; EP_QKV: cache_len of the row's sequence
+    double inv_freq = 0.0; // EP_QKV: rotary inverse frequency of this lane's column pair
+    if (wave == 0) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = 16 * mt + 4 * g + r;
+                ep_in[mt][r] = 0.f;
+                if (EP == EP_RESID && m < M && tile * 16 + c < a.N)
+                    ep_in[mt][r] = a.resid[(size_t)m * a.ldy + tile * 16 + c];
+                if (EP == EP_QKV && m < M) ep_in[mt][r] = __int_as_float(a.cache_len[m / a.q]);
+            }
+        if (EP == EP_QKV) inv_freq = a.inv_freq[8 * (tile % (a.Dh / 16)) + (c & 7)];
+    }
+
     f32x4_t acc[MT];
 #pragma unroll
-    for (int i = 0; i < MT; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    if (tile_ok) {
-        const T* wp = reinterpret_cast<const T*>(a.W) + (((size_t)tile * a.k_steps + ks0) * 64 + lane) * 8;
-        constexpr int U = 8;
-        for (int s = 0; s < nks; s += U) {
-            Frag<T> w[U];
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    Frag<T> w0[U], w1[U];
+    Frag<T> x0[U][MT], x1[U][MT];
+    if (nks > 0) {
+        load_batch<T, MT, U>(w0, x0, wp, xr, xok, 0, nks);
+        for (int s = 0; s < nks; s += 2 * U) {
+            if (s + U < nks) load_batch<T, MT, U>(w1, x1, wp, xr, xok, s + U, nks);
+            mma_batch<T, MT, U>(acc, w0, x0);
+            if (s + 2 * U < nks) load_batch<T, MT, U>(w0, x0, wp, xr, xok, s + 2 * U, nks);
+            if (s + U < nks) mma_batch<T, MT, U>(acc, w1, x1);
+        }
+    }
+    // RMSNorm row scales (rows past the prefetched ones, and partials past
+    // 64 * NSQ columns, are read now)
+    if (a.ssq) {
+        for (int m = wave, j = 0; m < M; m += nw, ++j) {
+            float v = 0.f;
+            if (j < 2) {
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (s + u < nks) w[u] = Frag<T>::load_nt(wp + (size_t)(s + u) * 512);
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                if (s + u < nks) {
-#pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) {
-                        const int m = 16 * mt + c;
-                        Frag<T> xf = m < M ? Frag<T>::load(xs + m * ldl + (s + u) * 32 + 8 * g) : Frag<T>::zero();
-                        mma(acc[mt], xf, w[u]);
-                    }
-                }
+                for (int t = 0; t < NSQ; ++t) v += sq[j < 1 ? 0 : 1][t];
+                for (int col = lane + 64 * NSQ; col < a.n_ssq; col += 64) v += a.ssq[(size_t)m * a.n_ssq + col];
+            } else {
+                for (int col = lane; col < a.n_ssq; col += 64) v += a.ssq[(size_t)m * a.n_ssq + col];
             }
+            v = wave_sum(v);
+            if (lane == 0) s_inv[m] = 1.0f / sqrtf(v / (float)a.K + a.eps);
         }
     }
 
-    // ---- split-K reduction: last arriving workgroup of the column group finishes
-    if (a.splits > 1) {
-        f32x4_t* part = reinterpret_cast<f32x4_t*>(a.partial);
-        const size_t base = (((size_t)group * a.splits + split) * 4 + wave) * MT * 64;
+    // cross-wave reduction in wave order
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) part[base + mt * 64 + lane] = acc[mt];
-        __threadfence();
-        __syncthreads();
-        if (threadIdx.x == 0) s_last = atomicAdd(&a.counter[group], 1) == a.splits - 1;
-        __syncthreads();
-        if (!s_last) return;
-        __threadfence();
+    for (int mt = 0; mt < MT; ++mt) red[(wave * MT + mt) * 64 + lane] = acc[mt];
+    __syncthreads();
+    if (wave != 0) return;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        for (int sp = 0; sp < a.splits; ++sp) {
-            const size_t b2 = (((size_t)group * a.splits + sp) * 4 + wave) * MT * 64;
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) acc[mt] += part[b2 + mt * 64 + lane];
-        }
-        if (threadIdx.x == 0) a.counter[group] = 0;
+    for (int mt = 0; mt < MT; ++mt) {
+        f32x4_t v = red[mt * 64 + lane];
+        for (int w = 1; w < nw; ++w) v += red[(w * MT + mt) * 64 + lane];
+        acc[mt] = v;
     }
-    if (!tile_ok) return;
+    if (a.ssq) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = 16 * mt + 4 * g + r;
+                if (m < M) acc[mt][r] *= s_inv[m];
+            }
+    }
 
     // ---- epilogues.  acc[mt][r] = Y[m = 16mt + 4g + r][column c of this tile]
     if (EP == EP_STORE) {
@@ -213,6 +239,7 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
             }
     } else if (EP == EP_RESID) {
         const int n = tile * 16 + c;
+        T* xb = reinterpret_cast<T*>(a.xb);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -220,9 +247,9 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
                 const int m = 16 * mt + 4 * g + r;
                 float ss = 0.f;
                 if (m < M && n < a.N) {
-                    float* px = a.resid + (size_t)m * a.ldy + n;
-                    const float v = *px + acc[mt][r];
-                    *px = v;
+                    const float v = ep_in[mt][r] + acc[mt][r];
+                    a.resid[(size_t)m * a.ldy + n] = v;
+                    xb[(size_t)m * a.ldxb + n] = to_elem<T>(v);
                     ss = v * v;
                 }
                 ss += __shfl_xor(ss, 8, 64);
@@ -243,7 +270,7 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
                 const float other = __shfl_xor(mine, 8, 64);
                 if (c < 8 && m < M && f < a.F) {
                     const float gate = mine, up = other;
-                    u[(size_t)m * a.F + f] = to_elem<T>(gate / (1.0f + expf(-gate)) * up);
+                    u[(size_t)m * a.ldu + f] = to_elem<T>(gate / (1.0f + expf(-gate)) * up);
                 }
             }
     } else if (EP == EP_QKV) {
@@ -262,7 +289,8 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
                 const float other = __shfl_xor(mine, 8, 64);
                 if (m >= M || sec > 2) continue;
                 const int b = m / a.q, row = m - b * a.q;
-                const int pos = a.cache_len[b] + row;   // cache slot of this block row
+                const int L = __float_as_int(ep_in[mt][r]);
+                const int pos = L + row;                // cache slot of this block row
                 if (pos >= a.S_max) {                   // the host checks capacity; never write past the cache
                     atomicOr(a.err, 4);
                     continue;
@@ -270,10 +298,13 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
                 float out = mine;
                 if (sec < 2) {
                     // rotary position: the row's depth in the block (its ancestors
-                    // counted by the tree mask; row index for a chain)
-                    const int rpos = a.mask ? a.cache_len[b] + __popcll(a.mask[m]) - 1 : pos;
-                    const float cs = a.rope_cos[(size_t)rpos * half + pi];
-                    const float sn = a.rope_sin[(size_t)rpos * half + pi];
+                    // counted by the tree mask; row index for a chain).  The angle
+                    // pos * base^(-2i/Dh) is formed in double and cos / sin are
+                    // rounded to float, as a float table built in double would hold.
+                    const int rpos = a.mask ? L + __popcll(a.mask[m]) - 1 : pos;
+                    double sd, cd;
+                    sincos((double)rpos * inv_freq, &sd, &cd);
+                    const float cs = (float)cd, sn = (float)sd;
                     out = c < 8 ? mine * cs - other * sn : other * sn + mine * cs;
                 }
                 if (sec == 0) {
@@ -288,31 +319,33 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
     }
 }
 
-template <typename T, int XS, int EP>
+template <typename T, int EP>
 static hipError_t launch_mt(const GemmPlan& p, const GemmArgs& a, hipStream_t s) {
+    const dim3 grid(p.grid), block(64 * p.waves);
     switch (p.mt) {
-        case 1: hipLaunchKernelGGL((gemm_kernel<T, XS, EP, 1>), dim3(p.grid), dim3(256), p.lds_bytes, s, a); break;
-        case 2: hipLaunchKernelGGL((gemm_kernel<T, XS, EP, 2>), dim3(p.grid), dim3(256), p.lds_bytes, s, a); break;
-        case 3: hipLaunchKernelGGL((gemm_kernel<T, XS, EP, 3>), dim3(p.grid), dim3(256), p.lds_bytes, s, a); break;
-        case 4: hipLaunchKernelGGL((gemm_kernel<T, XS, EP, 4>), dim3(p.grid), dim3(256), p.lds_bytes, s, a); break;
+        case 1: hipLaunchKernelGGL((gemm_kernel<T, EP, 1>), grid, block, p.lds_bytes, s, a); break;
+        case 2: hipLaunchKernelGGL((gemm_kernel<T, EP, 2>), grid, block, p.lds_bytes, s, a); break;
+        case 3: hipLaunchKernelGGL((gemm_kernel<T, EP, 3>), grid, block, p.lds_bytes, s, a); break;
+        case 4: hipLaunchKernelGGL((gemm_kernel<T, EP, 4>), grid, block, p.lds_bytes, s, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 template <typename T>
-static hipError_t launch_t(int xs, int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s) {
-    if (xs == XS_NORM && ep == EP_QKV) return launch_mt<T, XS_NORM, EP_QKV>(p, a, s);
-    if (xs == XS_NORM && ep == EP_SWIGLU) return launch_mt<T, XS_NORM, EP_SWIGLU>(p, a, s);
-    if (xs == XS_NORM && ep == EP_STORE) return launch_mt<T, XS_NORM, EP_STORE>(p, a, s);
-    if (xs == XS_ACT && ep == EP_RESID) return launch_mt<T, XS_ACT, EP_RESID>(p, a, s);
-    if (xs == XS_F32 && ep == EP_STORE) return launch_mt<T, XS_F32, EP_STORE>(p, a, s);
-    return hipErrorInvalidValue;
+static hipError_t launch_t(int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s) {
+    switch (ep) {
+        case EP_STORE: return launch_mt<T, EP_STORE>(p, a, s);
+        case EP_QKV: return launch_mt<T, EP_QKV>(p, a, s);
+        case EP_RESID: return launch_mt<T, EP_RESID>(p, a, s);
+        case EP_SWIGLU: return launch_mt<T, EP_SWIGLU>(p, a, s);
+        default: return hipErrorInvalidValue;
+    }
 }
 
-hipError_t launch_gemm(int dtype, int xs, int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s) {
-    if (a.M < 1 || a.M > 64) return hipErrorInvalidValue;
-    return dtype == 1 ? launch_t<uint16_t>(xs, ep, p, a, s) : launch_t<float>(xs, ep, p, a, s);
+hipError_t launch_gemm(int dtype, int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s) {
+    if (a.M < 1 || a.M > 64 || p.waves < 1 || p.waves > 16) return hipErrorInvalidValue;
+    return dtype == 1 ? launch_t<uint16_t>(ep, p, a, s) : launch_t<float>(ep, p, a, s);
 }
 
 }  // namespace sdsat

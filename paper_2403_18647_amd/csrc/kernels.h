@@ -30,48 +30,46 @@ struct PackArgs {
     const void* src1;   // rows [N0, N0+N1) (stacked second matrix) or null
     const void* src2;
     int N0, N1;         // row counts of src0, src1 (src2 takes the rest)
+    const float* gain;  // optional per-column scale folded in: packed W[n][k] = W[n][k] * gain[k]
     void* dst;
 };
 void launch_pack(const PackArgs& a, hipStream_t s);
 size_t packed_elems(int n_tiles, int k_steps);
 
 // ---------------------------------------------------------------- skinny GEMM
-enum XSource { XS_NORM = 0, XS_ACT = 1, XS_F32 = 2 };
+// One workgroup per 16-column tile; its waves split the contraction and
+// reduce through LDS.  X rows are read straight from global memory as
+// matrix-core fragments: X is stored in the matrix element type with a row
+// stride that covers the 32-padded contraction length, zero past K.
 enum Epilogue { EP_STORE = 0, EP_QKV = 1, EP_RESID = 2, EP_SWIGLU = 3 };
 
 struct GemmArgs {
     int M, N, K;             // rows of X; real output columns; real contraction length
     int n_tiles, k_steps;    // packed tile counts
-    int splits, chunk_steps; // split-K: WG (group, split) covers k-steps [split*chunk, ...)
     const void* W;           // packed weights
-    // X source
-    const float* x;          // XS_NORM / XS_F32: float [M][ldx]
-    const void* xa;          // XS_ACT: T [M][ldx]
+    const void* xa;          // T [M][ldx]
     int ldx;
-    const float* ssq;        // XS_NORM: partial sums of squares [M][n_ssq]
-    int n_ssq;
-    float eps;
-    const float* gain;       // XS_NORM: float [K]
+    // RMSNorm folded into the epilogue: y[m][:] *= 1/sqrt(sum_t ssq[m][t] / K + eps)
+    // (the gain is folded into W).  ssq null: no scaling.
+    const float* ssq; int n_ssq; float eps;
     // epilogues
     float* y; int ldy;                   // EP_STORE: float [M][ldy]
-    float* resid; float* ssq_out;        // EP_RESID: resid [M][ldy] (+=), ssq_out [M][n_tiles]
+    float* resid;                        // EP_RESID: float [M][ldy] (+=)
+    void* xb; int ldxb;                  // EP_RESID: T copy of the updated rows [M][ldxb]
+    float* ssq_out;                      // EP_RESID: per-tile sums of squares [M][n_tiles]
     void* qbuf; void* kc; void* vc;      // EP_QKV: Q [M][H][Dh]; layer base of K and V caches
     const int* cache_len; int q, H, Dh, S_max;
     const uint64_t* mask;                // [M] ancestor masks or null (chain)
-    const float* rope_cos; const float* rope_sin;   // [S_max][Dh/2]
-    void* uout; int F;                   // EP_SWIGLU: T [M][F]
-    // split-K scratch
-    float* partial; int* counter;
+    const double* inv_freq;              // [Dh/2] rotary inverse frequencies base^(-2i/Dh)
+    void* uout; int F; int ldu;          // EP_SWIGLU: T [M][ldu]
     int* err;                            // device error flags (bit 4: write past the cache)
 };
 
 struct GemmPlan {
-    int splits, chunk_steps, mt, grid, lds_bytes;
+    int waves, mt, grid, lds_bytes;
 };
-GemmPlan plan_gemm(int dtype, int M, int n_tiles, int k_steps);
-size_t gemm_partial_floats(const GemmPlan& p, int n_tiles);
-int gemm_groups(int n_tiles);
-hipError_t launch_gemm(int dtype, int xs, int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s);
+GemmPlan plan_gemm(int M, int n_tiles, int k_steps);
+hipError_t launch_gemm(int dtype, int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- attention
 struct AttnArgs {
@@ -80,22 +78,24 @@ struct AttnArgs {
     const void* vc;          // T V cache of one layer: [B][H][S_max/32][Dh][32] (keys permuted, vperm)
     const int* cache_len;
     const uint64_t* mask;    // [B*q] or null
-    int B, q, H, S_max, chunk_keys, n_chunks;
+    int B, q, H, S_max;
     float scale;
-    float* part;             // scratch
-    int* counter;            // [B*H]
-    void* out;               // T (or float if out_f32) [B*q][H*Dh]
-    int out_f32;
+    int splits;              // workgroups per (b, h); > 1: partials to `part`, then a combine kernel
+    float* part;             // [B*H][splits][16*MT rows][Dh + 4]: unnormalised O, row max, row sum
+    void* out;               // T (or float if out_f32) [B*q][ldo], head h at columns h*Dh..
+    int out_f32, ldo;
     int* err;                // device error flags (bit 4: read past the cache)
 };
-struct AttnPlan { int chunk_keys, n_chunks, grid; };
-AttnPlan plan_attention(int B, int H, int q, int max_len);
+// `splits` workgroups of `waves` waves per (sequence, head)
+struct AttnPlan { int waves, splits, grid, lds_bytes; };
+AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len);
 size_t attention_partial_floats(int B, int H, int q_max, int head_dim);
-hipError_t launch_attention(int dtype, int head_dim, const AttnArgs& a, hipStream_t s);
+hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- misc kernels
 hipError_t launch_embed(int dtype, const void* embed, int n_rows_emb, int d, const int* tokens, int M,
-                        float* x, float* ssq, int n_ssq, int* err, hipStream_t s);
+                        float* x, void* xb, int ldxb, float* ssq, int n_ssq, int* err, hipStream_t s);
+hipError_t launch_to_elem_rows(int dtype, const float* src, int rows, int cols, void* dst, int ld, hipStream_t s);
 hipError_t launch_kv_write(int dtype, void* kc, void* vc, int B, int n, int H, int Dh, int S_max,
                            const float* k, const float* v, const int* pos, hipStream_t s);
 hipError_t launch_to_elem(int dtype, const float* src, void* dst, size_t n, hipStream_t s);

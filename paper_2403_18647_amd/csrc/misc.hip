@@ -7,12 +7,12 @@
 
 namespace sdsat {
 
-// x[m] = E[token[m]] as float, plus per-16-column sums of squares (the
-// partials the first RMSNorm prologue reduces).  Out-of-range ids set *err
-// and read row 0.
+// x[m] = E[token[m]] as float, its copy xb in the matrix element type (the
+// first QKV GEMM's input), plus per-16-column sums of squares (the partials
+// its RMSNorm scale reduces).  Out-of-range ids set *err and read row 0.
 template <typename T>
-__global__ void embed_kernel(const T* emb, int n_rows, int d, const int* tokens, float* x, float* ssq,
-                             int n_ssq, int* err) {
+__global__ void embed_kernel(const T* emb, int n_rows, int d, const int* tokens, float* x, T* xb, int ldxb,
+                             float* ssq, int n_ssq, int* err) {
     const int m = blockIdx.x;
     int tok = tokens[m];
     if (tok < 0 || tok >= n_rows) {
@@ -25,8 +25,10 @@ __global__ void embed_kernel(const T* emb, int n_rows, int d, const int* tokens,
         for (int j = 0; j < 16; ++j) {
             const int k = 16 * t + j;
             if (k < d) {
-                const float v = to_f32<T>(src[k]);
+                const T e = src[k];
+                const float v = to_f32<T>(e);
                 x[(size_t)m * d + k] = v;
+                xb[(size_t)m * ldxb + k] = e;
                 ss += v * v;
             }
         }
@@ -35,13 +37,35 @@ __global__ void embed_kernel(const T* emb, int n_rows, int d, const int* tokens,
 }
 
 hipError_t launch_embed(int dtype, const void* embed, int n_rows_emb, int d, const int* tokens, int M,
-                        float* x, float* ssq, int n_ssq, int* err, hipStream_t s) {
+                        float* x, void* xb, int ldxb, float* ssq, int n_ssq, int* err, hipStream_t s) {
     if (dtype == 1)
         hipLaunchKernelGGL(embed_kernel<uint16_t>, dim3(M), dim3(256), 0, s, (const uint16_t*)embed, n_rows_emb,
-                           d, tokens, x, ssq, n_ssq, err);
+                           d, tokens, x, (uint16_t*)xb, ldxb, ssq, n_ssq, err);
     else
         hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, (const float*)embed, n_rows_emb, d,
-                           tokens, x, ssq, n_ssq, err);
+                           tokens, x, (float*)xb, ldxb, ssq, n_ssq, err);
+    return hipGetLastError();
+}
+
+// float rows [rows][cols] -> element rows [rows][ld], zero in columns cols..ld-1
+template <typename T>
+__global__ void to_elem_rows_kernel(const float* src, int rows, int cols, T* dst, int ld) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (size_t)rows * ld) return;
+    const int r = (int)(i / ld), c = (int)(i % ld);
+    dst[i] = to_elem<T>(c < cols ? src[(size_t)r * cols + c] : 0.f);
+}
+
+hipError_t launch_to_elem_rows(int dtype, const float* src, int rows, int cols, void* dst, int ld, hipStream_t s) {
+    const size_t n = (size_t)rows * ld;
+    const int blocks = (int)((n + 255) / 256);
+    if (blocks == 0) return hipSuccess;
+    if (dtype == 1)
+        hipLaunchKernelGGL(to_elem_rows_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s, src, rows, cols,
+                           (uint16_t*)dst, ld);
+    else
+        hipLaunchKernelGGL(to_elem_rows_kernel<float>, dim3(blocks), dim3(256), 0, s, src, rows, cols, (float*)dst,
+                           ld);
     return hipGetLastError();
 }
 

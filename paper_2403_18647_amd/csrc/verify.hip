@@ -29,13 +29,23 @@ __device__ int block_argmax(const float* row, int V, float* s_val, int* s_idx) {
     float bv = -INFINITY;
     int bi = 0x7fffffff;
     if ((V & 3) == 0) {
+        // all of a round's loads are issued before any is compared
+        constexpr int PF = 8;
         const float4* r4 = reinterpret_cast<const float4*>(row);
-        for (int i = threadIdx.x; i < V / 4; i += NT) {
-            const float4 v = r4[i];
-            if (better(v.x, 4 * i, bv, bi)) { bv = v.x; bi = 4 * i; }
-            if (better(v.y, 4 * i + 1, bv, bi)) { bv = v.y; bi = 4 * i + 1; }
-            if (better(v.z, 4 * i + 2, bv, bi)) { bv = v.z; bi = 4 * i + 2; }
-            if (better(v.w, 4 * i + 3, bv, bi)) { bv = v.w; bi = 4 * i + 3; }
+        const int n4 = V / 4;
+        for (int i0 = threadIdx.x; i0 < n4; i0 += NT * PF) {
+            float4 v[PF];
+#pragma unroll
+            for (int p = 0; p < PF; ++p) v[p] = r4[min(i0 + p * NT, n4 - 1)];
+#pragma unroll
+            for (int p = 0; p < PF; ++p) {
+                const int i = i0 + p * NT;
+                if (i >= n4) break;
+                if (better(v[p].x, 4 * i, bv, bi)) { bv = v[p].x; bi = 4 * i; }
+                if (better(v[p].y, 4 * i + 1, bv, bi)) { bv = v[p].y; bi = 4 * i + 1; }
+                if (better(v[p].z, 4 * i + 2, bv, bi)) { bv = v[p].z; bi = 4 * i + 2; }
+                if (better(v[p].w, 4 * i + 3, bv, bi)) { bv = v[p].w; bi = 4 * i + 3; }
+            }
         }
     } else {
         for (int i = threadIdx.x; i < V; i += NT) {
@@ -84,20 +94,20 @@ __device__ void finish_sequence(int b, int q, const int* drafts, int drafts_ld, 
     counter[b] = 0;
 }
 
-__global__ void __launch_bounds__(256) verify_greedy_kernel(const float* logits, int q, int V, const int* drafts,
-                                                            int drafts_ld, int* tokens_out, int* n_accept,
-                                                            int* counter) {
-    __shared__ float s_val[4];
-    __shared__ int s_idx[4];
+__global__ void __launch_bounds__(1024) verify_greedy_kernel(const float* logits, int q, int V, const int* drafts,
+                                                             int drafts_ld, int* tokens_out, int* n_accept,
+                                                             int* counter) {
+    __shared__ float s_val[16];
+    __shared__ int s_idx[16];
     const int row = blockIdx.x, b = row / q;
-    const int t = block_argmax<256>(logits + (size_t)row * V, V, s_val, s_idx);
+    const int t = block_argmax<1024>(logits + (size_t)row * V, V, s_val, s_idx);
     if (threadIdx.x == 0) tokens_out[row] = t;
     finish_sequence(b, q, drafts, drafts_ld, tokens_out, n_accept, counter);
 }
 
 hipError_t launch_verify_greedy(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,
                                 int* tokens_out, int* n_accept, int* counter, hipStream_t s) {
-    hipLaunchKernelGGL(verify_greedy_kernel, dim3(B * q), dim3(256), 0, s, logits, q, V, drafts, drafts_ld,
+    hipLaunchKernelGGL(verify_greedy_kernel, dim3(B * q), dim3(1024), 0, s, logits, q, V, drafts, drafts_ld,
                        tokens_out, n_accept, counter);
     return hipGetLastError();
 }

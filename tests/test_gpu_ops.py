@@ -252,3 +252,11 @@ def test_commit_chain_and_tree_gather():
                           r(V[b, keep]).astype(np.float64), M.chain_visibility(1), 1.0 / math.sqrt(Dh))
         assert np.abs(got[b] - ref).max() < 2e-2
     ctx.close()
+
+
+def test_attention_many_heads_single_workgroup_per_head():
+    """B * H >= 256: one workgroup per (sequence, head), no key split."""
+    shape = synth.small_shape(n_layers=1, d_model=4096, n_heads=32, head_dim=128, d_ffn=64, vocab=64,
+                              n_adaptive=2, rope_base=1e6, dtype="bf16")
+    wl = synth.Workload("heads32", shape, seed=5, batch=8, k=5, prompt_len=1, max_new=1)
+    _attn_case(wl, [300, 0, 31, 64, 129, 5, 250, 77], 6)
