@@ -42,9 +42,27 @@ def block_bytes(sh, B, q, ctx_len):
 
 
 def gateup_bytes(sh, M):
-    """Algorithmic bytes of one gate/up launch: [2F, d] bf16 weights, the float
-    residual rows and gain it normalises, the bf16 SwiGLU output."""
-    return 2 * sh.d_ffn * sh.d_model * 2 + M * sh.d_model * 4 + sh.d_model * 4 + M * sh.d_ffn * 2
+    """Algorithmic bytes of one gate/up launch: the [2F, d] bf16 weight tiles (RMSNorm gain folded in),
+    the M bf16 residual rows, their per-16-column sums of squares, and the bf16 SwiGLU output."""
+    d, F = sh.d_model, sh.d_ffn
+    return 2 * F * d * 2 + M * d * 2 + M * (d // 16) * 4 + M * F * 2
+
+
+def profiled_traffic():
+    """HBM bytes per gate/up launch from the committed rocprofv3 counter summary, if that summary
+    was taken from the current GEMM source (else None)."""
+    import hashlib
+    prof = os.path.join(ROOT, "profiles", "gateup_gemm_7b_decode.md")
+    src = os.path.join(ROOT, "paper_2403_18647_amd", "csrc", "gemm.hip")
+    try:
+        text = open(prof).read()
+        fields = dict(line.split(": ", 1) for line in text.splitlines()
+                      if line.startswith(("traffic_bytes_per_launch: ", "gemm_source_sha256: ")))
+        if fields.get("gemm_source_sha256", "").strip() != hashlib.sha256(open(src, "rb").read()).hexdigest():
+            return None
+        return int(fields["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(wl, m_bar, n_layers_sample=2, n_blocks=3):
@@ -107,6 +125,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="7b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mb", type=int, default=0,
+                    help="first run one device-to-device copy of this many MiB (a plain copy kernel of known "
+                         "size, for scaling hardware traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build runs the decode path on a single MI355X "
@@ -124,6 +145,14 @@ def main():
     sh = wl.shape
     q = wl.k + 1
     torch.cuda.set_device(0)
+    if args.calibrate_copy_mb:
+        n = args.calibrate_copy_mb << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {n} bytes device to device")
+        del src, dst
     t0 = time.time()
     weights = synth.device_weights(wl, "cuda:0")
     torch.cuda.synchronize()
@@ -201,7 +230,7 @@ def main():
                    "global_batch": wl.batch, "seq_len": wl.prompt_len + wl.max_new, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": "gate/up GEMM + SwiGLU (M=%d)" % M_rows,
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": profiled_traffic(),
                      "bytes_per_launch": gu_bytes, "avg_launch_us": round(gu_avg_s * 1e6, 3),
                      "launches": gu_n},
         "decode": {"tokens_per_s": round(wl.max_new * wl.batch / (decode_ms / 1e3), 3),

@@ -180,8 +180,9 @@ void prof_begin(sdsat_ctx* c, int kind, hipEvent_t* out) {
     if (c->prof_kind != kind) return;
     if (c->ev_used + 2 > c->events.size()) {
         for (int i = 0; i < 64; ++i) {
+            // no system-scope fence on record: the interval then covers the kernel, not a cache flush
             hipEvent_t ev;
-            if (hipEventCreate(&ev) != hipSuccess) return;
+            if (hipEventCreateWithFlags(&ev, hipEventDisableSystemFence) != hipSuccess) return;
             c->events.push_back(ev);
         }
     }
