@@ -242,7 +242,7 @@ int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask,
     const AttnPlan p = plan_attention(B, D.H, q, D.Dh, max_hint(c, B));
     AttnArgs a{};
     a.qbuf = qbuf; a.kc = layer_k(c, layer); a.vc = layer_v(c, layer);
-    a.cache_len = c->cache_len; a.mask = mask;
+    a.cache_len = c->cache_len; a.len_bound = max_hint(c, B); a.mask = mask;
     a.B = B; a.q = q; a.H = D.H; a.S_max = D.S;
     a.scale = (float)(1.0 / std::sqrt((double)D.Dh));
     a.splits = p.splits; a.part = c->attn_part;

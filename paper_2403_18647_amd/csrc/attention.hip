@@ -6,15 +6,18 @@
 //   the block rows r may see (0..r, or the rows set in its ancestor mask).
 // The block's own K/V rows were written into slots L_b.. by the QKV epilogue.
 //
-// One workgroup per (b, h).  Its waves take contiguous runs of 32-key blocks.
-// Per block a wave computes the 32 x q score tile S^T = K Q^T on the matrix
-// cores (A = K rows straight from the cache, B = Q^T from registers), runs an
-// online softmax per query row (query rows live in lanes, keys in registers
-// and lane groups), and accumulates O^T = V^T P^T with A = V^T read from the
-// cache's key-permuted 32-key blocks (vperm) and B = P^T taken from the score
-// registers as they are.  The next block's K and V are in flight while the
-// current one is computed.  The waves' partial results are merged in LDS with
-// a log-sum-exp combine in wave order (deterministic; no global scratch).
+// Workgroups per (b, h): one, or a few key splits when the (b, h) pairs alone
+// cannot fill the GPU and the context is long.  Waves take the workgroup's
+// 32-key blocks round-robin.  Per block a wave computes the 32 x q score tile
+// S^T = K Q^T on the matrix cores (A = K rows straight from the cache, B = Q^T
+// from registers), runs an online softmax per query row (query rows live in
+// lanes, keys in registers and lane groups), and accumulates O^T = V^T P^T
+// with A = V^T read from the cache's key-permuted 32-key blocks (vperm) and
+// B = P^T taken from the score registers as they are.  The next block's K and
+// V are in flight while the current one is computed; the first two are
+// requested from the host's upper bound of the cache length before the true
+// length has arrived.  The waves' partial results are merged in LDS with a
+// log-sum-exp combine in wave order (deterministic).
 #include "device.h"
 #include "kernels.h"
 
@@ -23,20 +26,30 @@ namespace sdsat {
 static constexpr int kMaxWaves = 8;
 static constexpr int kMaxSplits = 8;
 
-// When the (b, h) pairs alone cannot fill the GPU, each pair's key blocks are
-// split over up to 8 workgroups.  Waves per workgroup: about two 32-key blocks
-// each, at most 8 / MT (LDS holds waves x Dh/16 x MT tiles of 1 KiB).
+// Key splits only pay when the (b, h) pairs leave most compute units idle and
+// each pair has many key blocks; otherwise the combine kernel costs more than
+// the parallelism gains.  Waves per workgroup: one per 32-key block up to
+// 8 / MT (LDS holds waves x Dh/16 x MT tiles of 1 KiB).
+#ifndef SDSAT_ATTN_SPLIT_MIN_BLOCKS
+#define SDSAT_ATTN_SPLIT_MIN_BLOCKS 48
+#endif
+#ifndef SDSAT_ATTN_BLOCKS_PER_SPLIT
+#define SDSAT_ATTN_BLOCKS_PER_SPLIT 16
+#endif
 AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len) {
     AttnPlan p;
     const int mt = (q + 15) / 16;
     const int nblk = (max_len + q + 31) / 32;
     const int pairs = B * H;
-    int splits = pairs >= 256 ? 1 : (256 + pairs - 1) / pairs;
-    if (splits > kMaxSplits) splits = kMaxSplits;
-    if (splits > nblk) splits = nblk;
-    if (splits < 1) splits = 1;
+    int splits = 1;
+    if (pairs < 256 && nblk >= SDSAT_ATTN_SPLIT_MIN_BLOCKS) {
+        splits = (256 + pairs - 1) / pairs;
+        if (splits > kMaxSplits) splits = kMaxSplits;
+        if (splits > nblk / SDSAT_ATTN_BLOCKS_PER_SPLIT) splits = nblk / SDSAT_ATTN_BLOCKS_PER_SPLIT;
+        if (splits < 1) splits = 1;
+    }
     const int per_split = (nblk + splits - 1) / splits;
-    int w = (per_split + 1) / 2;
+    int w = per_split;
     if (w > kMaxWaves / mt) w = kMaxWaves / mt;
     if (w < 1) w = 1;
     p.waves = w;
@@ -126,10 +139,45 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     __shared__ float s_max[kMaxWaves][64], s_sum[kMaxWaves][64];
 
     const int nw = blockDim.x >> 6;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, c = lane & 15, g = lane >> 4;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63, c = lane & 15, g = lane >> 4;
     const int bh = blockIdx.x / a.splits, sp = blockIdx.x % a.splits;
     const int b = bh / a.H, h = bh % a.H;
     const int q = a.q;
+    const T* kbase = reinterpret_cast<const T*>(a.kc) + ((size_t)b * a.H + h) * a.S_max * DH;
+    const T* vbase = reinterpret_cast<const T*>(a.vc) + ((size_t)b * a.H + h) * a.S_max * DH;
+    const bool tree = a.mask != nullptr;
+
+    // Query rows (rows past q read row q-1: their scores are masked out) and
+    // ancestor masks are requested first, then the wave's first two K/V
+    // blocks.  Every load ahead of the block loop is unconditional, so the
+    // compiler's wait counts stay exact and nothing waits for more than it uses.
+    const T* qb = reinterpret_cast<const T*>(a.qbuf);
+    Frag<T> qf[NDS][MT];
+    uint64_t mrow[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const int m = min(16 * mt + c, q - 1);
+        mrow[mt] = tree ? a.mask[(size_t)b * q + m] : 0ull;
+#pragma unroll
+        for (int ds = 0; ds < NDS; ++ds)
+            qf[ds][mt] = Frag<T>::load(qb + (((size_t)b * q + m) * a.H + h) * DH + ds * 32 + 8 * g);
+    }
+
+    // Split sp owns blocks [wlo, wlo + per_wg) of the partition the host's
+    // length bound gives (the last split runs on to the true end, so a stale
+    // bound costs time, never keys).  The wave's blocks are first + i * nw;
+    // the first two are requested before the true length is known (indices
+    // clamped into the cache; a block past the length is loaded, not used).
+    const int nb_bound = min((a.len_bound + q + 31) / 32, a.S_max / 32);
+    const int per_wg = max(1, (nb_bound + a.splits - 1) / a.splits);
+    const int wlo = sp * per_wg;
+    const int first = wlo + wave;
+    const int last_blk = a.S_max / 32 - 1;
+    Frag<T> kA[2][NDS], kB[2][NDS], vA[NDT], vB[NDT];
+    load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, min(first, last_blk), c, g);
+    load_kv<T, NDS, NDT>(kB, vB, kbase, vbase, min(first + nw, last_blk), c, g);
+
     const int L = a.cache_len[b];
     const int Tb = L + q;
     if (Tb > a.S_max) {   // the host checks capacity; never read past this sequence's cache
@@ -137,27 +185,7 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
         return;
     }
     const int nblk = (Tb + 31) / 32;
-    const int per_wg = (nblk + a.splits - 1) / a.splits;   // this workgroup: blocks [wlo, whi)
-    const int wlo = sp * per_wg, whi = min(nblk, wlo + per_wg);
-    const int per = (max(0, whi - wlo) + nw - 1) / nw;
-    const int blo = wlo + wave * per;
-    const int bhi = min(whi, blo + per);
-
-    const T* qb = reinterpret_cast<const T*>(a.qbuf);
-    Frag<T> qf[NDS][MT];
-    uint64_t mrow[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int m = 16 * mt + c;
-        mrow[mt] = (a.mask && m < q) ? a.mask[(size_t)b * q + m] : 0ull;
-#pragma unroll
-        for (int ds = 0; ds < NDS; ++ds)
-            qf[ds][mt] = m < q ? Frag<T>::load(qb + (((size_t)b * q + m) * a.H + h) * DH + ds * 32 + 8 * g)
-                               : Frag<T>::zero();
-    }
-    const T* kbase = reinterpret_cast<const T*>(a.kc) + ((size_t)b * a.H + h) * a.S_max * DH;
-    const T* vbase = reinterpret_cast<const T*>(a.vc) + ((size_t)b * a.H + h) * a.S_max * DH;
-    const bool tree = a.mask != nullptr;
+    const int whi = sp == a.splits - 1 ? nblk : min(nblk, wlo + per_wg);
 
     float rmax[MT], rsum[MT];
     f32x4_t o[NDT][MT];
@@ -169,19 +197,27 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
         for (int dt = 0; dt < NDT; ++dt) o[dt][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
 
-    if (blo < bhi) {
-        Frag<T> kA[2][NDS], kB[2][NDS], vA[NDT], vB[NDT];
-        load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, blo, c, g);
-        for (int blk = blo; blk < bhi; blk += 2) {
-            // next block in flight (clamped: a duplicate load past the run is not used)
-            load_kv<T, NDS, NDT>(kB, vB, kbase, vbase, min(blk + 1, bhi - 1), c, g);
-            attend_block<T, NDS, NDT, MT>(kA, vA, qf, mrow, blk, L, Tb, q, tree, a.scale, c, g, rmax, rsum, o);
-            load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, min(blk + 2, bhi - 1), c, g);
-            if (blk + 1 < bhi)
-                attend_block<T, NDS, NDT, MT>(kB, vB, qf, mrow, blk + 1, L, Tb, q, tree, a.scale, c, g, rmax, rsum,
-                                              o);
-        }
+    // this wave's blocks: first + i * nw for i < cnt; buffers A and B alternate
+    const int cnt = first < whi ? (whi - first + nw - 1) / nw : 0;
+    int i = 0;
+    // steady state (unconditional loads): blocks i and i + 1 are loaded
+    for (; i + 4 <= cnt; i += 2) {
+        attend_block<T, NDS, NDT, MT>(kA, vA, qf, mrow, first + i * nw, L, Tb, q, tree, a.scale, c, g, rmax, rsum, o);
+        load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, first + (i + 2) * nw, c, g);
+        attend_block<T, NDS, NDT, MT>(kB, vB, qf, mrow, first + (i + 1) * nw, L, Tb, q, tree, a.scale, c, g, rmax,
+                                      rsum, o);
+        load_kv<T, NDS, NDT>(kB, vB, kbase, vbase, first + (i + 3) * nw, c, g);
     }
+    // 0 .. 3 blocks left
+    if (i < cnt)
+        attend_block<T, NDS, NDT, MT>(kA, vA, qf, mrow, first + i * nw, L, Tb, q, tree, a.scale, c, g, rmax, rsum, o);
+    if (i + 2 < cnt) load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, first + (i + 2) * nw, c, g);
+    if (i + 1 < cnt)
+        attend_block<T, NDS, NDT, MT>(kB, vB, qf, mrow, first + (i + 1) * nw, L, Tb, q, tree, a.scale, c, g, rmax,
+                                      rsum, o);
+    if (i + 2 < cnt)
+        attend_block<T, NDS, NDT, MT>(kA, vA, qf, mrow, first + (i + 2) * nw, L, Tb, q, tree, a.scale, c, g, rmax,
+                                      rsum, o);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
         rsum[mt] += __shfl_xor(rsum[mt], 16, 64);
@@ -217,6 +253,7 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
             acc += opart[((w * NDT + dt) * MT + mt) * 64 + lane];
         }
         const int d = 16 * dt + 4 * g;
+        if (m >= q) continue;
         if (a.splits > 1) {
             // partial of this workgroup: O scaled to its row maximum, the maximum, the sum
             float* pr = a.part + (((size_t)bh * a.splits + sp) * (MT * 16) + m) * (DH + 4);
@@ -224,7 +261,6 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
             if (dt == 0 && g == 0) { pr[DH] = gmax; pr[DH + 1] = den; }
             continue;
         }
-        if (m >= q) continue;
         const float inv = 1.0f / den;
         const size_t row = ((size_t)b * q + m) * a.ldo + (size_t)h * DH;
         if (a.out_f32) {
@@ -310,7 +346,7 @@ static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s)
 
 hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s) {
     if (a.q < 1 || a.q > 64 || p.waves < 1 || p.waves > kMaxWaves || a.splits < 1 || a.splits > kMaxSplits ||
-        a.splits != p.splits || (a.splits > 1 && !a.part))
+        a.splits != p.splits || (a.splits > 1 && !a.part) || p.grid != a.B * a.H * a.splits)
         return hipErrorInvalidValue;
     if (dtype == 1) {
         if (head_dim == 128) return launch_dh<uint16_t, 128>(p, a, s);

@@ -98,16 +98,24 @@ template <typename T, int MT> struct Batch {
     static constexpr int U = sizeof(T) == 2 ? (MT == 1 ? 4 : 2) : (MT == 1 ? 2 : 1);
 };
 
-template <typename T, int MT, int U>
+// One batch of U contraction steps: the weight fragments (streamed, non-
+// temporal) and the X fragments of every row tile.  Rows past M read row 0
+// (their output rows are never stored).  TAIL batches may run past the
+// wave's slice: those steps reload the last step with X zeroed.  Loads of
+// the steady-state loop are unconditional so that the compiler's wait
+// counts stay exact and two batches really are in flight.
+template <typename T, int MT, int U, bool TAIL>
 __device__ __forceinline__ void load_batch(Frag<T> (&w)[U], Frag<T> (&x)[U][MT], const T* wp,
-                                           const T* const (&xr)[MT], const bool (&xok)[MT], int s, int nks) {
+                                           const T* const (&xr)[MT], int s, int nks) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        const int st = min(s + u, nks - 1);   // past the slice: reload the last step, with zero X
+        const int st = TAIL ? min(s + u, nks - 1) : s + u;
         w[u] = Frag<T>::load_nt(wp + (size_t)st * 512);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-            x[u][mt] = (xok[mt] && s + u < nks) ? Frag<T>::load(xr[mt] + st * 32) : Frag<T>::zero();
+        for (int mt = 0; mt < MT; ++mt) {
+            x[u][mt] = Frag<T>::load(xr[mt] + st * 32);
+            if (TAIL && s + u >= nks) x[u][mt] = Frag<T>::zero();
+        }
     }
 }
 
@@ -127,7 +135,7 @@ __global__ void __launch_bounds__(1024) gemm_kernel(GemmArgs a) {
     __shared__ float s_inv[64];
 
     const int nw = blockDim.x >> 6;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int c = lane & 15, g = lane >> 4;
     const int tile = blockIdx.x;
     const int M = a.M;
@@ -138,12 +146,10 @@ __global__ void __launch_bounds__(1024) gemm_kernel(GemmArgs a) {
     const int nks = max(0, min(a.k_steps, ks0 + chunk) - ks0);
     const T* wp = reinterpret_cast<const T*>(a.W) + (((size_t)tile * a.k_steps + ks0) * 64 + lane) * 8;
     const T* xr[MT];
-    bool xok[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
         const int m = 16 * mt + c;
-        xok[mt] = m < M;
-        xr[mt] = reinterpret_cast<const T*>(a.xa) + (size_t)(xok[mt] ? m : 0) * a.ldx + ks0 * 32 + 8 * g;
+        xr[mt] = reinterpret_cast<const T*>(a.xa) + (size_t)(m < M ? m : 0) * a.ldx + ks0 * 32 + 8 * g;
     }
 
     // Loads whose values are only needed after the main loop are issued first:
@@ -181,13 +187,22 @@ __global__ void __launch_bounds__(1024) gemm_kernel(GemmArgs a) {
     Frag<T> w0[U], w1[U];
     Frag<T> x0[U][MT], x1[U][MT];
     if (nks > 0) {
-        load_batch<T, MT, U>(w0, x0, wp, xr, xok, 0, nks);
-        for (int s = 0; s < nks; s += 2 * U) {
-            if (s + U < nks) load_batch<T, MT, U>(w1, x1, wp, xr, xok, s + U, nks);
+        load_batch<T, MT, U, true>(w0, x0, wp, xr, 0, nks);
+        int s = 0;
+        // steady state: batches s and s + U are in flight, s + 2U is requested
+        // as soon as s has been consumed
+        for (; s + 3 * U <= nks; s += 2 * U) {
+            load_batch<T, MT, U, false>(w1, x1, wp, xr, s + U, nks);
             mma_batch<T, MT, U>(acc, w0, x0);
-            if (s + 2 * U < nks) load_batch<T, MT, U>(w0, x0, wp, xr, xok, s + 2 * U, nks);
-            if (s + U < nks) mma_batch<T, MT, U>(acc, w1, x1);
+            load_batch<T, MT, U, false>(w0, x0, wp, xr, s + 2 * U, nks);
+            mma_batch<T, MT, U>(acc, w1, x1);
         }
+        // tail: 1 .. 3U steps left, the first batch of them already loaded
+        if (s + U < nks) load_batch<T, MT, U, true>(w1, x1, wp, xr, s + U, nks);
+        mma_batch<T, MT, U>(acc, w0, x0);
+        if (s + 2 * U < nks) load_batch<T, MT, U, true>(w0, x0, wp, xr, s + 2 * U, nks);
+        if (s + U < nks) mma_batch<T, MT, U>(acc, w1, x1);
+        if (s + 2 * U < nks) mma_batch<T, MT, U>(acc, w0, x0);
     }
     // RMSNorm row scales (rows past the prefetched ones, and partials past
     // 64 * NSQ columns, are read now)

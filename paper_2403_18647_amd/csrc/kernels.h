@@ -77,6 +77,7 @@ struct AttnArgs {
     const void* kc;          // T K cache of one layer: [B][H][S_max][Dh]
     const void* vc;          // T V cache of one layer: [B][H][S_max/32][Dh][32] (keys permuted, vperm)
     const int* cache_len;
+    int len_bound;           // host's upper bound of cache_len[b] (sets the key partition and the early loads)
     const uint64_t* mask;    // [B*q] or null
     int B, q, H, S_max;
     float scale;
