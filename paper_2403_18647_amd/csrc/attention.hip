@@ -7,8 +7,10 @@
 // The block's own K/V rows were written into slots L_b.. by the QKV epilogue.
 //
 // Workgroups per (b, h): one, or a few key splits when the (b, h) pairs alone
-// cannot fill the GPU and the context is long.  Waves take the workgroup's
-// 32-key blocks round-robin.  Per block a wave computes the 32 x q score tile
+// cannot fill the GPU.  Waves take the workgroup's 32-key blocks round-robin.
+// Query rows are handled 16 at a time (one matrix-core tile); a block of more
+// rows (a prefill chunk) loops over its row tiles and re-reads the keys, which
+// then come from L2.  Per block a wave computes the 32 x 16 score tile
 // S^T = K Q^T on the matrix cores (A = K rows straight from the cache, B = Q^T
 // from registers), runs an online softmax per query row (query rows live in
 // lanes, keys in registers and lane groups), and accumulates O^T = V^T P^T
@@ -26,36 +28,28 @@ namespace sdsat {
 static constexpr int kMaxWaves = 8;
 static constexpr int kMaxSplits = 8;
 
-// Key splits only pay when the (b, h) pairs leave most compute units idle and
-// each pair has many key blocks; otherwise the combine kernel costs more than
-// the parallelism gains.  Waves per workgroup: one per 32-key block up to
-// 8 / MT (LDS holds waves x Dh/16 x MT tiles of 1 KiB).
-#ifndef SDSAT_ATTN_SPLIT_MIN_BLOCKS
-#define SDSAT_ATTN_SPLIT_MIN_BLOCKS 48
-#endif
-#ifndef SDSAT_ATTN_BLOCKS_PER_SPLIT
-#define SDSAT_ATTN_BLOCKS_PER_SPLIT 16
-#endif
+// Decode blocks (q <= 16): key splits only pay when the (b, h) pairs leave most
+// compute units idle and each pair has many key blocks; below that the combine
+// kernel costs more than the parallelism gains (measured on MI355X).  Longer
+// blocks (prefill chunks) do q/16 passes over the keys per workgroup and take
+// splits of at least two blocks.  Waves per workgroup: one per 32-key block of
+// the split, at most 8 (LDS holds waves x Dh/16 tiles of 1 KiB).
 AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len) {
     AttnPlan p;
-    const int mt = (q + 15) / 16;
     const int nblk = (max_len + q + 31) / 32;
     const int pairs = B * H;
     int splits = 1;
-    if (pairs < 256 && nblk >= SDSAT_ATTN_SPLIT_MIN_BLOCKS) {
-        splits = (256 + pairs - 1) / pairs;
-        if (splits > kMaxSplits) splits = kMaxSplits;
-        if (splits > nblk / SDSAT_ATTN_BLOCKS_PER_SPLIT) splits = nblk / SDSAT_ATTN_BLOCKS_PER_SPLIT;
-        if (splits < 1) splits = 1;
+    if (pairs < 256) {
+        const int want = (256 + pairs - 1) / pairs;
+        if (q > 16) splits = std::min(want, nblk / 2);
+        else if (nblk >= 48) splits = std::min(want, nblk / 16);
+        splits = std::max(1, std::min(splits, kMaxSplits));
     }
     const int per_split = (nblk + splits - 1) / splits;
-    int w = per_split;
-    if (w > kMaxWaves / mt) w = kMaxWaves / mt;
-    if (w < 1) w = 1;
-    p.waves = w;
+    p.waves = std::max(1, std::min(per_split, kMaxWaves));
     p.splits = splits;
     p.grid = pairs * splits;
-    p.lds_bytes = w * (head_dim / 16) * mt * 64 * 16;
+    p.lds_bytes = p.waves * (head_dim / 16) * 64 * 16;
     return p;
 }
 
@@ -78,65 +72,63 @@ __device__ __forceinline__ void load_kv(Frag<T> (&kf)[2][NDS], Frag<T> (&vf)[NDT
     for (int dt = 0; dt < NDT; ++dt) vf[dt] = Frag<T>::load(vblk + (size_t)(dt * 16 + c) * 32 + 8 * g);
 }
 
-template <typename T, int NDS, int NDT, int MT>
+// One 32-key block for the 16 query rows of this lane group (lane column c is
+// block row m = m0 + c).
+template <typename T, int NDS, int NDT>
 __device__ __forceinline__ void attend_block(const Frag<T> (&kf)[2][NDS], const Frag<T> (&vf)[NDT],
-                                             const Frag<T> (&qf)[NDS][MT], const uint64_t (&mrow)[MT], int blk,
-                                             int L, int Tb, int q, bool tree, float scale, int c, int g,
-                                             float (&rmax)[MT], float (&rsum)[MT], f32x4_t (&o)[NDT][MT]) {
+                                             const Frag<T> (&qf)[NDS], uint64_t mrow, int blk, int m, int L, int Tb,
+                                             int q, bool tree, float scale, int g, float& rmax, float& rsum,
+                                             f32x4_t (&o)[NDT]) {
     const int kb0 = blk * 32;
+    f32x4_t s0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, s1 = s0;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        f32x4_t s0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+    for (int ds = 0; ds < NDS; ++ds) {
+        mma(s0, kf[0][ds], qf[ds]);
+        mma(s1, kf[1][ds], qf[ds]);
+    }
+    // s0[r], s1[r] = S^T[key = kb0 + 16kt + 4g + r][row m]
+    float sv[8];
+    bool vis[8];
 #pragma unroll
-        for (int ds = 0; ds < NDS; ++ds) {
-            mma(s0, kf[0][ds], qf[ds][mt]);
-            mma(s1, kf[1][ds], qf[ds][mt]);
-        }
-        // s0[r], s1[r] = S^T[key = kb0 + 16kt + 4g + r][m = 16mt + c]
-        const int m = 16 * mt + c;
-        float sv[8];
-        bool vis[8];
+    for (int i = 0; i < 8; ++i) {
+        const int key = kb0 + (i < 4 ? 4 * g + i : 16 + 4 * g + (i - 4));
+        bool v = key < Tb && m < q;
+        if (tree) v = v && (key < L || ((mrow >> (key - L)) & 1ull));
+        else v = v && key <= L + m;
+        vis[i] = v;
+        sv[i] = (i < 4 ? s0[i] : s1[i - 4]) * scale;
+    }
+    float bm = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int key = kb0 + (i < 4 ? 4 * g + i : 16 + 4 * g + (i - 4));
-            bool v = key < Tb && m < q;
-            if (tree) v = v && (key < L || ((mrow[mt] >> (key - L)) & 1ull));
-            else v = v && key <= L + m;
-            vis[i] = v;
-            sv[i] = (i < 4 ? s0[i] : s1[i - 4]) * scale;
-        }
-        float bm = -INFINITY;
+    for (int i = 0; i < 8; ++i) if (vis[i]) bm = fmaxf(bm, sv[i]);
+    bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
+    bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+    const float nmax = fmaxf(rmax, bm);
+    const float alpha = rmax == -INFINITY ? 0.f : expf(rmax - nmax);
+    float p[8];
+    float ps = 0.f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) if (vis[i]) bm = fmaxf(bm, sv[i]);
-        bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
-        bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
-        const float nmax = fmaxf(rmax[mt], bm);
-        const float alpha = rmax[mt] == -INFINITY ? 0.f : expf(rmax[mt] - nmax);
-        float p[8];
-        float ps = 0.f;
+    for (int i = 0; i < 8; ++i) {
+        p[i] = vis[i] ? expf(sv[i] - nmax) : 0.f;
+        ps += p[i];
+    }
+    rsum = rsum * alpha + ps;
+    rmax = nmax;
+    const Frag<T> pf = Frag<T>::from_f32(p);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            p[i] = vis[i] ? expf(sv[i] - nmax) : 0.f;
-            ps += p[i];
-        }
-        rsum[mt] = rsum[mt] * alpha + ps;
-        rmax[mt] = nmax;
-        const Frag<T> pf = Frag<T>::from_f32(p);
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-            o[dt][mt] *= alpha;
-            mma(o[dt][mt], vf[dt], pf);
-        }
+    for (int dt = 0; dt < NDT; ++dt) {
+        o[dt] *= alpha;
+        mma(o[dt], vf[dt], pf);
     }
 }
 
-template <typename T, int DH, int MT>
+template <typename T, int DH>
 __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     constexpr int NDS = DH / 32;   // 32-wide steps over the head dimension
     constexpr int NDT = DH / 16;   // 16-row output tiles over the head dimension
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    f32x4_t* opart = reinterpret_cast<f32x4_t*>(smem_raw);   // [waves][NDT][MT][64]
-    __shared__ float s_max[kMaxWaves][64], s_sum[kMaxWaves][64];
+    f32x4_t* opart = reinterpret_cast<f32x4_t*>(smem_raw);   // [waves][NDT][64]
+    __shared__ float s_max[kMaxWaves][16], s_sum[kMaxWaves][16];
 
     const int nw = blockDim.x >> 6;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -146,23 +138,8 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     const int q = a.q;
     const T* kbase = reinterpret_cast<const T*>(a.kc) + ((size_t)b * a.H + h) * a.S_max * DH;
     const T* vbase = reinterpret_cast<const T*>(a.vc) + ((size_t)b * a.H + h) * a.S_max * DH;
-    const bool tree = a.mask != nullptr;
-
-    // Query rows (rows past q read row q-1: their scores are masked out) and
-    // ancestor masks are requested first, then the wave's first two K/V
-    // blocks.  Every load ahead of the block loop is unconditional, so the
-    // compiler's wait counts stay exact and nothing waits for more than it uses.
     const T* qb = reinterpret_cast<const T*>(a.qbuf);
-    Frag<T> qf[NDS][MT];
-    uint64_t mrow[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int m = min(16 * mt + c, q - 1);
-        mrow[mt] = tree ? a.mask[(size_t)b * q + m] : 0ull;
-#pragma unroll
-        for (int ds = 0; ds < NDS; ++ds)
-            qf[ds][mt] = Frag<T>::load(qb + (((size_t)b * q + m) * a.H + h) * DH + ds * 32 + 8 * g);
-    }
+    const bool tree = a.mask != nullptr;
 
     // Split sp owns blocks [wlo, wlo + per_wg) of the partition the host's
     // length bound gives (the last split runs on to the true end, so a stale
@@ -174,109 +151,118 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     const int wlo = sp * per_wg;
     const int first = wlo + wave;
     const int last_blk = a.S_max / 32 - 1;
-    Frag<T> kA[2][NDS], kB[2][NDS], vA[NDT], vB[NDT];
-    load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, min(first, last_blk), c, g);
-    load_kv<T, NDS, NDT>(kB, vB, kbase, vbase, min(first + nw, last_blk), c, g);
+    const int n_rt = (q + 15) / 16;
+    int L = 0, whi = 0;
 
-    const int L = a.cache_len[b];
-    const int Tb = L + q;
-    if (Tb > a.S_max) {   // the host checks capacity; never read past this sequence's cache
-        if (threadIdx.x == 0) atomicOr(a.err, 4);
-        return;
-    }
-    const int nblk = (Tb + 31) / 32;
-    const int whi = sp == a.splits - 1 ? nblk : min(nblk, wlo + per_wg);
+    for (int rt = 0; rt < n_rt; ++rt) {
+        // Query rows of this tile (rows past q read row q-1: their scores are
+        // masked out) and ancestor masks come first, then the wave's first two
+        // K/V blocks.  Every load ahead of the block loop is unconditional, so
+        // the compiler's wait counts stay exact.
+        const int m = 16 * rt + c;
+        const int mr = min(m, q - 1);
+        const uint64_t mrow = tree ? a.mask[(size_t)b * q + mr] : 0ull;
+        Frag<T> qf[NDS];
+#pragma unroll
+        for (int ds = 0; ds < NDS; ++ds)
+            qf[ds] = Frag<T>::load(qb + (((size_t)b * q + mr) * a.H + h) * DH + ds * 32 + 8 * g);
+        Frag<T> kA[2][NDS], kB[2][NDS], vA[NDT], vB[NDT];
+        load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, min(first, last_blk), c, g);
+        load_kv<T, NDS, NDT>(kB, vB, kbase, vbase, min(first + nw, last_blk), c, g);
+        if (rt == 0) {
+            L = a.cache_len[b];
+            if (L + q > a.S_max) {   // the host checks capacity; never read past this sequence's cache
+                if (threadIdx.x == 0) atomicOr(a.err, 4);
+                return;
+            }
+            const int nblk = (L + q + 31) / 32;
+            whi = sp == a.splits - 1 ? nblk : min(nblk, wlo + per_wg);
+        }
+        const int Tb = L + q;
 
-    float rmax[MT], rsum[MT];
-    f32x4_t o[NDT][MT];
+        float rmax = -INFINITY, rsum = 0.f;
+        f32x4_t o[NDT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        rmax[mt] = -INFINITY;
-        rsum[mt] = 0.f;
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) o[dt][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    }
+        for (int dt = 0; dt < NDT; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    // this wave's blocks: first + i * nw for i < cnt; buffers A and B alternate
-    const int cnt = first < whi ? (whi - first + nw - 1) / nw : 0;
-    int i = 0;
-    // steady state (unconditional loads): blocks i and i + 1 are loaded
-    for (; i + 4 <= cnt; i += 2) {
-        attend_block<T, NDS, NDT, MT>(kA, vA, qf, mrow, first + i * nw, L, Tb, q, tree, a.scale, c, g, rmax, rsum, o);
-        load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, first + (i + 2) * nw, c, g);
-        attend_block<T, NDS, NDT, MT>(kB, vB, qf, mrow, first + (i + 1) * nw, L, Tb, q, tree, a.scale, c, g, rmax,
+        // this wave's blocks: first + i * nw for i < cnt; buffers A and B alternate
+        const int cnt = first < whi ? (whi - first + nw - 1) / nw : 0;
+        int i = 0;
+        // steady state (unconditional loads): blocks i and i + 1 are loaded
+        for (; i + 4 <= cnt; i += 2) {
+            attend_block<T, NDS, NDT>(kA, vA, qf, mrow, first + i * nw, m, L, Tb, q, tree, a.scale, g, rmax, rsum, o);
+            load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, first + (i + 2) * nw, c, g);
+            attend_block<T, NDS, NDT>(kB, vB, qf, mrow, first + (i + 1) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
                                       rsum, o);
-        load_kv<T, NDS, NDT>(kB, vB, kbase, vbase, first + (i + 3) * nw, c, g);
-    }
-    // 0 .. 3 blocks left
-    if (i < cnt)
-        attend_block<T, NDS, NDT, MT>(kA, vA, qf, mrow, first + i * nw, L, Tb, q, tree, a.scale, c, g, rmax, rsum, o);
-    if (i + 2 < cnt) load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, first + (i + 2) * nw, c, g);
-    if (i + 1 < cnt)
-        attend_block<T, NDS, NDT, MT>(kB, vB, qf, mrow, first + (i + 1) * nw, L, Tb, q, tree, a.scale, c, g, rmax,
+            load_kv<T, NDS, NDT>(kB, vB, kbase, vbase, first + (i + 3) * nw, c, g);
+        }
+        // 0 .. 3 blocks left
+        if (i < cnt)
+            attend_block<T, NDS, NDT>(kA, vA, qf, mrow, first + i * nw, m, L, Tb, q, tree, a.scale, g, rmax, rsum, o);
+        if (i + 2 < cnt) load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, first + (i + 2) * nw, c, g);
+        if (i + 1 < cnt)
+            attend_block<T, NDS, NDT>(kB, vB, qf, mrow, first + (i + 1) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
                                       rsum, o);
-    if (i + 2 < cnt)
-        attend_block<T, NDS, NDT, MT>(kA, vA, qf, mrow, first + (i + 2) * nw, L, Tb, q, tree, a.scale, c, g, rmax,
+        if (i + 2 < cnt)
+            attend_block<T, NDS, NDT>(kA, vA, qf, mrow, first + (i + 2) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
                                       rsum, o);
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        rsum[mt] += __shfl_xor(rsum[mt], 16, 64);
-        rsum[mt] += __shfl_xor(rsum[mt], 32, 64);
+
+        rsum += __shfl_xor(rsum, 16, 64);
+        rsum += __shfl_xor(rsum, 32, 64);
+        if (rt > 0) __syncthreads();   // the previous tile's merge has read LDS
         if (g == 0) {
-            s_max[wave][16 * mt + c] = rmax[mt];
-            s_sum[wave][16 * mt + c] = rsum[mt];
+            s_max[wave][c] = rmax;
+            s_sum[wave][c] = rsum;
         }
-    }
-    __syncthreads();
-    // rescale this wave's partial to the common maximum and park it in LDS
+        __syncthreads();
+        // rescale this wave's partial to the common maximum and park it in LDS
+        {
+            float gmax = -INFINITY;
+            for (int w = 0; w < nw; ++w) gmax = fmaxf(gmax, s_max[w][c]);
+            const float alpha = rmax == -INFINITY ? 0.f : expf(rmax - gmax);
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int m = 16 * mt + c;
-        float gmax = -INFINITY;
-        for (int w = 0; w < nw; ++w) gmax = fmaxf(gmax, s_max[w][m]);
-        const float alpha = rmax[mt] == -INFINITY ? 0.f : expf(rmax[mt] - gmax);
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) opart[((wave * NDT + dt) * MT + mt) * 64 + lane] = o[dt][mt] * alpha;
-    }
-    __syncthreads();
-    // sum the partials in wave order; output tiles are spread over the waves
-    for (int t = wave; t < NDT * MT; t += nw) {
-        const int dt = t / MT, mt = t % MT;
-        const int m = 16 * mt + c;
-        float gmax = -INFINITY;
-        for (int w = 0; w < nw; ++w) gmax = fmaxf(gmax, s_max[w][m]);
-        float den = 0.f;
-        f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        for (int w = 0; w < nw; ++w) {
-            const float wm = s_max[w][m];
-            den += wm == -INFINITY ? 0.f : expf(wm - gmax) * s_sum[w][m];
-            acc += opart[((w * NDT + dt) * MT + mt) * 64 + lane];
+            for (int dt = 0; dt < NDT; ++dt) opart[(wave * NDT + dt) * 64 + lane] = o[dt] * alpha;
         }
-        const int d = 16 * dt + 4 * g;
-        if (m >= q) continue;
-        if (a.splits > 1) {
-            // partial of this workgroup: O scaled to its row maximum, the maximum, the sum
-            float* pr = a.part + (((size_t)bh * a.splits + sp) * (MT * 16) + m) * (DH + 4);
-            *reinterpret_cast<f32x4_t*>(pr + d) = acc;
-            if (dt == 0 && g == 0) { pr[DH] = gmax; pr[DH + 1] = den; }
-            continue;
-        }
-        const float inv = 1.0f / den;
-        const size_t row = ((size_t)b * q + m) * a.ldo + (size_t)h * DH;
-        if (a.out_f32) {
-            float* po = reinterpret_cast<float*>(a.out) + row + d;
+        __syncthreads();
+        // sum the partials in wave order; output tiles are spread over the waves
+        for (int dt = wave; dt < NDT; dt += nw) {
+            float gmax = -INFINITY;
+            for (int w = 0; w < nw; ++w) gmax = fmaxf(gmax, s_max[w][c]);
+            float den = 0.f;
+            f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            for (int w = 0; w < nw; ++w) {
+                const float wm = s_max[w][c];
+                den += wm == -INFINITY ? 0.f : expf(wm - gmax) * s_sum[w][c];
+                acc += opart[(w * NDT + dt) * 64 + lane];
+            }
+            if (m >= q) continue;
+            const int d = 16 * dt + 4 * g;
+            if (a.splits > 1) {
+                // partial of this workgroup: O scaled to its row maximum, the maximum, the sum
+                float* pr = a.part + (((size_t)bh * a.splits + sp) * (n_rt * 16) + m) * (DH + 4);
+                *reinterpret_cast<f32x4_t*>(pr + d) = acc;
+                if (dt == 0 && g == 0) { pr[DH] = gmax; pr[DH + 1] = den; }
+                continue;
+            }
+            const float inv = 1.0f / den;
+            const size_t row = ((size_t)b * q + m) * a.ldo + (size_t)h * DH;
+            if (a.out_f32) {
+                float* po = reinterpret_cast<float*>(a.out) + row + d;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) po[r] = acc[r] * inv;
-        } else {
-            T* po = reinterpret_cast<T*>(a.out) + row + d;
+                for (int r = 0; r < 4; ++r) po[r] = acc[r] * inv;
+            } else {
+                T* po = reinterpret_cast<T*>(a.out) + row + d;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) po[r] = to_elem<T>(acc[r] * inv);
+                for (int r = 0; r < 4; ++r) po[r] = to_elem<T>(acc[r] * inv);
+            }
         }
     }
 }
 
 // Combine the split partials: one thread per (b, h, row, 4 head dims),
-// log-sum-exp over the splits in split order, all partial loads in flight at once.
+// log-sum-exp over the splits in split order, all partial loads in flight at
+// once.  (Rows of a sequence whose cache overflowed were flagged by the
+// partial kernel; their output is then unspecified.)
 template <typename T, int DH>
 __global__ void __launch_bounds__(64) attn_combine_kernel(AttnArgs a, int rows) {
     constexpr int D4 = DH / 4;
@@ -286,7 +272,6 @@ __global__ void __launch_bounds__(64) attn_combine_kernel(AttnArgs a, int rows) 
     const int m = (e / D4) % a.q;
     const int bh = e / (D4 * a.q);
     const int b = bh / a.H, h = bh % a.H;
-    if (a.cache_len[b] + a.q > a.S_max) return;   // flagged by the partial kernel
     const float* base = a.part + ((size_t)bh * a.splits * rows + m) * (DH + 4);
     const size_t sstride = (size_t)rows * (DH + 4);
     float mx[kMaxSplits], sm[kMaxSplits];
@@ -328,19 +313,11 @@ __global__ void __launch_bounds__(64) attn_combine_kernel(AttnArgs a, int rows) 
 
 template <typename T, int DH>
 static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s) {
-    const int mt = (a.q + 15) / 16;
-    const dim3 grid(p.grid), block(64 * p.waves);
-    switch (mt) {
-        case 1: hipLaunchKernelGGL((attn_kernel<T, DH, 1>), grid, block, p.lds_bytes, s, a); break;
-        case 2: hipLaunchKernelGGL((attn_kernel<T, DH, 2>), grid, block, p.lds_bytes, s, a); break;
-        case 3: hipLaunchKernelGGL((attn_kernel<T, DH, 3>), grid, block, p.lds_bytes, s, a); break;
-        case 4: hipLaunchKernelGGL((attn_kernel<T, DH, 4>), grid, block, p.lds_bytes, s, a); break;
-        default: return hipErrorInvalidValue;
-    }
+    hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.splits <= 1) return e;
     const int n = a.B * a.H * a.q * (DH / 4);
-    hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3((n + 63) / 64), dim3(64), 0, s, a, mt * 16);
+    hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3((n + 63) / 64), dim3(64), 0, s, a, (a.q + 15) / 16 * 16);
     return hipGetLastError();
 }
 

@@ -79,38 +79,45 @@ void launch_pack(const PackArgs& a, hipStream_t s) {
 
 // Waves per workgroup (measured on MI355X at M = 6 with weights streamed from
 // HBM): 8 for the narrow [d, d] / [d, F] matrices, 4 for the wide ones; at
-// least 4 contraction steps per wave; at most 8 waves when M > 32 (LDS for the
-// cross-wave reduction).
+// least 4 contraction steps per wave.  Blocks of more than 16 rows (prefill
+// chunks) reload their X fragments for every weight fragment; for the wide
+// matrices a workgroup of 4 waves then takes 4 column tiles so that one X
+// load feeds 4 tiles' matrix-core steps (measured at M = 64: QKV 55 -> 37 us,
+// gate/up 103 -> 62 us); the narrow ones keep one tile per workgroup, which
+// keeps all compute units streaming.
 GemmPlan plan_gemm(int M, int n_tiles, int k_steps) {
     GemmPlan p;
     p.mt = (M + 15) / 16;
-    int w = n_tiles <= 512 ? 8 : 4;
+    p.ntw = (p.mt > 1 && n_tiles > 512) ? 4 : 1;
+    int w = p.ntw > 1 ? 4 : (n_tiles <= 512 ? 8 : 4);
     while (w > 1 && k_steps < 4 * w) w /= 2;
     p.waves = w;
-    p.grid = n_tiles;
+    p.grid = (n_tiles + p.ntw - 1) / p.ntw;
     p.lds_bytes = w * p.mt * 64 * 16;
     return p;
 }
 
 // Steps per load batch (two batches in flight), sized so both batches of
-// weight and X fragments fit the 128-VGPR budget of 16 waves per CU.
+// weight and X fragments fit the register budget (128 VGPRs at 16 waves per
+// CU for one tile per wave; 4-tile workgroups have 4 waves).
 template <typename T, int MT> struct Batch {
     static constexpr int U = sizeof(T) == 2 ? (MT == 1 ? 4 : 2) : (MT == 1 ? 2 : 1);
 };
 
-// One batch of U contraction steps: the weight fragments (streamed, non-
-// temporal) and the X fragments of every row tile.  Rows past M read row 0
-// (their output rows are never stored).  TAIL batches may run past the
-// wave's slice: those steps reload the last step with X zeroed.  Loads of
-// the steady-state loop are unconditional so that the compiler's wait
-// counts stay exact and two batches really are in flight.
-template <typename T, int MT, int U, bool TAIL>
-__device__ __forceinline__ void load_batch(Frag<T> (&w)[U], Frag<T> (&x)[U][MT], const T* wp,
+// One batch of U contraction steps: the weight fragments of the NTW tiles
+// (streamed, non-temporal) and the X fragments of every row tile.  Rows past
+// M read row 0 (their output rows are never stored).  TAIL batches may run
+// past the wave's slice: those steps reload the last step with X zeroed.
+// Loads of the steady-state loop are unconditional so that the compiler's
+// wait counts stay exact and two batches really are in flight.
+template <typename T, int MT, int NTW, int U, bool TAIL>
+__device__ __forceinline__ void load_batch(Frag<T> (&w)[U][NTW], Frag<T> (&x)[U][MT], const T* const (&wp)[NTW],
                                            const T* const (&xr)[MT], int s, int nks) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int st = TAIL ? min(s + u, nks - 1) : s + u;
-        w[u] = Frag<T>::load_nt(wp + (size_t)st * 512);
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) w[u][j] = Frag<T>::load_nt(wp[j] + (size_t)st * 512);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
             x[u][mt] = Frag<T>::load(xr[mt] + st * 32);
@@ -119,130 +126,23 @@ __device__ __forceinline__ void load_batch(Frag<T> (&w)[U], Frag<T> (&x)[U][MT],
     }
 }
 
-template <typename T, int MT, int U>
-__device__ __forceinline__ void mma_batch(f32x4_t (&acc)[MT], const Frag<T> (&w)[U], const Frag<T> (&x)[U][MT]) {
+template <typename T, int MT, int NTW, int U>
+__device__ __forceinline__ void mma_batch(f32x4_t (&acc)[NTW][MT], const Frag<T> (&w)[U][NTW],
+                                          const Frag<T> (&x)[U][MT]) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) mma(acc[mt], x[u][mt], w[u]);
+        for (int j = 0; j < NTW; ++j)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) mma(acc[j][mt], x[u][mt], w[u][j]);
 }
 
+// Fused epilogue of one reduced tile (run by wave 0).
+// acc[mt][r] = Y[m = 16mt + 4g + r][column c of the tile]
 template <typename T, int EP, int MT>
-__global__ void __launch_bounds__(1024) gemm_kernel(GemmArgs a) {
-    constexpr int U = Batch<T, MT>::U;
-    extern __shared__ __align__(16) unsigned char smem_raw[];
-    f32x4_t* red = reinterpret_cast<f32x4_t*>(smem_raw);   // [waves][MT][64]
-    __shared__ float s_inv[64];
-
-    const int nw = blockDim.x >> 6;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
-    const int c = lane & 15, g = lane >> 4;
-    const int tile = blockIdx.x;
+__device__ __forceinline__ void epilogue(const GemmArgs& a, int tile, const f32x4_t (&acc)[MT],
+                                         const float (&ep_in)[MT][4], double inv_freq, int c, int g) {
     const int M = a.M;
-
-    // this wave's contiguous slice of the contraction steps
-    const int chunk = (a.k_steps + nw - 1) / nw;
-    const int ks0 = wave * chunk;
-    const int nks = max(0, min(a.k_steps, ks0 + chunk) - ks0);
-    const T* wp = reinterpret_cast<const T*>(a.W) + (((size_t)tile * a.k_steps + ks0) * 64 + lane) * 8;
-    const T* xr[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int m = 16 * mt + c;
-        xr[mt] = reinterpret_cast<const T*>(a.xa) + (size_t)(m < M ? m : 0) * a.ldx + ks0 * 32 + 8 * g;
-    }
-
-    // Loads whose values are only needed after the main loop are issued first:
-    // RMSNorm partial sums (wave w takes rows w, w+nw, ... <= 2 per wave),
-    // and wave 0's epilogue inputs (residual values, cache lengths, rotary
-    // inverse frequencies).  vmcnt is in order, so they never stall the stream.
-    constexpr int NSQ = 4;   // ssq partials per lane and row (n_ssq <= 256)
-    float sq[2][NSQ];
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int t = 0; t < NSQ; ++t) {
-            const int m = wave + j * nw, col = lane + 64 * t;
-            sq[j][t] = (a.ssq && m < M && col < a.n_ssq) ? a.ssq[(size_t)m * a.n_ssq + col] : 0.f;
-        }
-    float ep_in[MT][4];    // EP_RESID: residual value; EP_QKV: cache_len of the row's sequence
-    double inv_freq = 0.0; // EP_QKV: rotary inverse frequency of this lane's column pair
-    if (wave == 0) {
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int m = 16 * mt + 4 * g + r;
-                ep_in[mt][r] = 0.f;
-                if (EP == EP_RESID && m < M && tile * 16 + c < a.N)
-                    ep_in[mt][r] = a.resid[(size_t)m * a.ldy + tile * 16 + c];
-                if (EP == EP_QKV && m < M) ep_in[mt][r] = __int_as_float(a.cache_len[m / a.q]);
-            }
-        if (EP == EP_QKV) inv_freq = a.inv_freq[8 * (tile % (a.Dh / 16)) + (c & 7)];
-    }
-
-    f32x4_t acc[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    Frag<T> w0[U], w1[U];
-    Frag<T> x0[U][MT], x1[U][MT];
-    if (nks > 0) {
-        load_batch<T, MT, U, true>(w0, x0, wp, xr, 0, nks);
-        int s = 0;
-        // steady state: batches s and s + U are in flight, s + 2U is requested
-        // as soon as s has been consumed
-        for (; s + 3 * U <= nks; s += 2 * U) {
-            load_batch<T, MT, U, false>(w1, x1, wp, xr, s + U, nks);
-            mma_batch<T, MT, U>(acc, w0, x0);
-            load_batch<T, MT, U, false>(w0, x0, wp, xr, s + 2 * U, nks);
-            mma_batch<T, MT, U>(acc, w1, x1);
-        }
-        // tail: 1 .. 3U steps left, the first batch of them already loaded
-        if (s + U < nks) load_batch<T, MT, U, true>(w1, x1, wp, xr, s + U, nks);
-        mma_batch<T, MT, U>(acc, w0, x0);
-        if (s + 2 * U < nks) load_batch<T, MT, U, true>(w0, x0, wp, xr, s + 2 * U, nks);
-        if (s + U < nks) mma_batch<T, MT, U>(acc, w1, x1);
-        if (s + 2 * U < nks) mma_batch<T, MT, U>(acc, w0, x0);
-    }
-    // RMSNorm row scales (rows past the prefetched ones, and partials past
-    // 64 * NSQ columns, are read now)
-    if (a.ssq) {
-        for (int m = wave, j = 0; m < M; m += nw, ++j) {
-            float v = 0.f;
-            if (j < 2) {
-#pragma unroll
-                for (int t = 0; t < NSQ; ++t) v += sq[j < 1 ? 0 : 1][t];
-                for (int col = lane + 64 * NSQ; col < a.n_ssq; col += 64) v += a.ssq[(size_t)m * a.n_ssq + col];
-            } else {
-                for (int col = lane; col < a.n_ssq; col += 64) v += a.ssq[(size_t)m * a.n_ssq + col];
-            }
-            v = wave_sum(v);
-            if (lane == 0) s_inv[m] = 1.0f / sqrtf(v / (float)a.K + a.eps);
-        }
-    }
-
-    // cross-wave reduction in wave order
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) red[(wave * MT + mt) * 64 + lane] = acc[mt];
-    __syncthreads();
-    if (wave != 0) return;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        f32x4_t v = red[mt * 64 + lane];
-        for (int w = 1; w < nw; ++w) v += red[(w * MT + mt) * 64 + lane];
-        acc[mt] = v;
-    }
-    if (a.ssq) {
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int m = 16 * mt + 4 * g + r;
-                if (m < M) acc[mt][r] *= s_inv[m];
-            }
-    }
-
-    // ---- epilogues.  acc[mt][r] = Y[m = 16mt + 4g + r][column c of this tile]
     if (EP == EP_STORE) {
         const int n = tile * 16 + c;
 #pragma unroll
@@ -334,14 +234,165 @@ __global__ void __launch_bounds__(1024) gemm_kernel(GemmArgs a) {
     }
 }
 
+template <typename T, int EP, int MT, int NTW>
+__global__ void __launch_bounds__(NTW == 1 ? 1024 : 512) gemm_kernel(GemmArgs a) {
+    constexpr int U = Batch<T, MT>::U;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    f32x4_t* red = reinterpret_cast<f32x4_t*>(smem_raw);   // [waves][MT][64]
+    __shared__ float s_inv[64];
+
+    const int nw = blockDim.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int c = lane & 15, g = lane >> 4;
+    const int tile0 = blockIdx.x * NTW;
+    const int M = a.M;
+
+    // this wave's contiguous slice of the contraction steps
+    const int chunk = (a.k_steps + nw - 1) / nw;
+    const int ks0 = wave * chunk;
+    const int nks = max(0, min(a.k_steps, ks0 + chunk) - ks0);
+    const T* wp[NTW];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) {
+        const int t = min(tile0 + j, a.n_tiles - 1);   // a tile past the end is read, not stored
+        wp[j] = reinterpret_cast<const T*>(a.W) + (((size_t)t * a.k_steps + ks0) * 64 + lane) * 8;
+    }
+    const T* xr[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const int m = 16 * mt + c;
+        xr[mt] = reinterpret_cast<const T*>(a.xa) + (size_t)(m < M ? m : 0) * a.ldx + ks0 * 32 + 8 * g;
+    }
+
+    // Loads whose values are only needed after the main loop are issued first:
+    // RMSNorm partial sums (wave w takes rows w, w+nw, ... <= 2 per wave),
+    // and wave 0's epilogue inputs (residual values, cache lengths, rotary
+    // inverse frequencies).  vmcnt is in order, so they never stall the stream.
+    constexpr int NSQ = 4;   // ssq partials per lane and row (n_ssq <= 256)
+    float sq[2][NSQ];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int t = 0; t < NSQ; ++t) {
+            const int m = wave + j * nw, col = lane + 64 * t;
+            sq[j][t] = (a.ssq && m < M && col < a.n_ssq) ? a.ssq[(size_t)m * a.n_ssq + col] : 0.f;
+        }
+    // EP_RESID: residual values per tile; EP_QKV: cache_len of each row's
+    // sequence (the same for every tile) and the rotary inverse frequency of
+    // this lane's column pair per tile
+    constexpr int NEP = EP == EP_RESID ? NTW : 1;
+    float ep_in[NEP][MT][4];
+    double inv_freq[NTW];
+#pragma unroll
+    for (int j = 0; j < NEP; ++j)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) ep_in[j][mt][r] = 0.f;
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) inv_freq[j] = 0.0;
+    if (wave == 0) {
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) {
+            const int tile = tile0 + j;
+            if (tile >= a.n_tiles) break;
+            if (EP == EP_QKV) inv_freq[j] = a.inv_freq[8 * (tile % (a.Dh / 16)) + (c & 7)];
+            if (EP != EP_RESID && j > 0) continue;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int m = 16 * mt + 4 * g + r;
+                    if (EP == EP_RESID && m < M && tile * 16 + c < a.N)
+                        ep_in[j < NEP ? j : 0][mt][r] = a.resid[(size_t)m * a.ldy + tile * 16 + c];
+                    if (EP == EP_QKV && m < M) ep_in[0][mt][r] = __int_as_float(a.cache_len[m / a.q]);
+                }
+        }
+    }
+
+    f32x4_t acc[NTW][MT];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    Frag<T> w0[U][NTW], w1[U][NTW];
+    Frag<T> x0[U][MT], x1[U][MT];
+    if (nks > 0) {
+        load_batch<T, MT, NTW, U, true>(w0, x0, wp, xr, 0, nks);
+        int s = 0;
+        // steady state: batches s and s + U are in flight, s + 2U is requested
+        // as soon as s has been consumed
+        for (; s + 3 * U <= nks; s += 2 * U) {
+            load_batch<T, MT, NTW, U, false>(w1, x1, wp, xr, s + U, nks);
+            mma_batch<T, MT, NTW, U>(acc, w0, x0);
+            load_batch<T, MT, NTW, U, false>(w0, x0, wp, xr, s + 2 * U, nks);
+            mma_batch<T, MT, NTW, U>(acc, w1, x1);
+        }
+        // tail: 1 .. 3U steps left, the first batch of them already loaded
+        if (s + U < nks) load_batch<T, MT, NTW, U, true>(w1, x1, wp, xr, s + U, nks);
+        mma_batch<T, MT, NTW, U>(acc, w0, x0);
+        if (s + 2 * U < nks) load_batch<T, MT, NTW, U, true>(w0, x0, wp, xr, s + 2 * U, nks);
+        if (s + U < nks) mma_batch<T, MT, NTW, U>(acc, w1, x1);
+        if (s + 2 * U < nks) mma_batch<T, MT, NTW, U>(acc, w0, x0);
+    }
+    // RMSNorm row scales (rows past the prefetched ones, and partials past
+    // 64 * NSQ columns, are read now)
+    if (a.ssq) {
+        for (int m = wave, j = 0; m < M; m += nw, ++j) {
+            float v = 0.f;
+            if (j < 2) {
+#pragma unroll
+                for (int t = 0; t < NSQ; ++t) v += sq[j < 1 ? 0 : 1][t];
+                for (int col = lane + 64 * NSQ; col < a.n_ssq; col += 64) v += a.ssq[(size_t)m * a.n_ssq + col];
+            } else {
+                for (int col = lane; col < a.n_ssq; col += 64) v += a.ssq[(size_t)m * a.n_ssq + col];
+            }
+            v = wave_sum(v);
+            if (lane == 0) s_inv[m] = 1.0f / sqrtf(v / (float)a.K + a.eps);
+        }
+    }
+
+    // cross-wave reduction in wave order, one tile at a time (LDS holds
+    // waves x MT fragments); wave 0 runs the tile's epilogue
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) {
+        if (tile0 + j >= a.n_tiles) break;
+        if (j > 0) __syncthreads();   // wave 0 has read the previous tile
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) red[(wave * MT + mt) * 64 + lane] = acc[j][mt];
+        __syncthreads();
+        if (wave != 0) continue;
+        f32x4_t t_acc[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            f32x4_t v = red[mt * 64 + lane];
+            for (int w = 1; w < nw; ++w) v += red[(w * MT + mt) * 64 + lane];
+            if (a.ssq) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int m = 16 * mt + 4 * g + r;
+                    if (m < M) v[r] *= s_inv[m];
+                }
+            }
+            t_acc[mt] = v;
+        }
+        epilogue<T, EP, MT>(a, tile0 + j, t_acc, ep_in[j < NEP ? j : 0], inv_freq[j], c, g);
+    }
+}
+
 template <typename T, int EP>
 static hipError_t launch_mt(const GemmPlan& p, const GemmArgs& a, hipStream_t s) {
     const dim3 grid(p.grid), block(64 * p.waves);
-    switch (p.mt) {
-        case 1: hipLaunchKernelGGL((gemm_kernel<T, EP, 1>), grid, block, p.lds_bytes, s, a); break;
-        case 2: hipLaunchKernelGGL((gemm_kernel<T, EP, 2>), grid, block, p.lds_bytes, s, a); break;
-        case 3: hipLaunchKernelGGL((gemm_kernel<T, EP, 3>), grid, block, p.lds_bytes, s, a); break;
-        case 4: hipLaunchKernelGGL((gemm_kernel<T, EP, 4>), grid, block, p.lds_bytes, s, a); break;
+    const int key = p.mt * 10 + p.ntw;
+    if (p.ntw > 1 && p.waves > 8) return hipErrorInvalidValue;
+    switch (key) {
+        case 11: hipLaunchKernelGGL((gemm_kernel<T, EP, 1, 1>), grid, block, p.lds_bytes, s, a); break;
+        case 21: hipLaunchKernelGGL((gemm_kernel<T, EP, 2, 1>), grid, block, p.lds_bytes, s, a); break;
+        case 31: hipLaunchKernelGGL((gemm_kernel<T, EP, 3, 1>), grid, block, p.lds_bytes, s, a); break;
+        case 41: hipLaunchKernelGGL((gemm_kernel<T, EP, 4, 1>), grid, block, p.lds_bytes, s, a); break;
+        case 24: hipLaunchKernelGGL((gemm_kernel<T, EP, 2, 4>), grid, block, p.lds_bytes, s, a); break;
+        case 34: hipLaunchKernelGGL((gemm_kernel<T, EP, 3, 4>), grid, block, p.lds_bytes, s, a); break;
+        case 44: hipLaunchKernelGGL((gemm_kernel<T, EP, 4, 4>), grid, block, p.lds_bytes, s, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -66,7 +66,7 @@ struct GemmArgs {
 };
 
 struct GemmPlan {
-    int waves, mt, grid, lds_bytes;
+    int waves, mt, ntw, grid, lds_bytes;   // ntw: 16-column tiles per workgroup
 };
 GemmPlan plan_gemm(int M, int n_tiles, int k_steps);
 hipError_t launch_gemm(int dtype, int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s);
