@@ -204,9 +204,12 @@ int sdsat_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const float* d_
 /* Per-kernel timing with HIP events on the context's stream.  kind: 0 off,
  * 1 gate/up GEMM, 2 QKV GEMM, 3 attention, 4 down GEMM, 5 O GEMM, 6 LM head,
  * 7 whole block forward with logits (draft / verify blocks), 8 whole block
- * forward without logits (prefill).  sdsat_kernel_time synchronizes the stream
- * and returns the summed milliseconds and launch count since the last call. */
-int sdsat_profile_kernel(sdsat_ctx* ctx, int32_t kind);
+ * forward without logits (prefill).  period >= 1: one launch of that kind in
+ * every `period` is bracketed by a pair of events (each pair costs a few
+ * microseconds of queue time, so a period > 1 keeps timed runs undisturbed).
+ * sdsat_kernel_time synchronizes the stream and returns the summed
+ * milliseconds and the number of timed launches since the last call. */
+int sdsat_profile_kernel(sdsat_ctx* ctx, int32_t kind, int32_t period);
 int sdsat_kernel_time(sdsat_ctx* ctx, double* total_ms, int64_t* launches);
 
 /* Release the context (not the caller's buffers).  NULL is accepted. */

@@ -58,7 +58,7 @@ _SIGNATURES = {
     "sdsat_linear_pack": ([_I32, _I32, _I32, _VP, _VP, _VP], _I32),
     "sdsat_linear_scratch_bytes": ([_I32, _I32, _I32], _SZ),
     "sdsat_linear": ([_I32, _I32, _I32, _I32, _VP, _VP, _VP, _VP, _VP], _I32),
-    "sdsat_profile_kernel": ([_VP, _I32], _I32),
+    "sdsat_profile_kernel": ([_VP, _I32, _I32], _I32),
     "sdsat_kernel_time": ([_VP, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64)], _I32),
     "sdsat_destroy": ([_VP], _I32),
     "sdsat_last_error": ([_VP], ctypes.c_char_p),
@@ -204,8 +204,8 @@ def sdsat_linear(dtype, M, N, K, x, packed, y, scratch, stream=None):
     _check(lib().sdsat_linear(dtype, M, N, K, _ptr(x), _ptr(packed), _ptr(y), _ptr(scratch), _stream(stream)))
 
 
-def sdsat_profile_kernel(ctx, kind):
-    _check(lib().sdsat_profile_kernel(ctx, PROFILE_KINDS.get(kind, kind)), ctx)
+def sdsat_profile_kernel(ctx, kind, period=1):
+    _check(lib().sdsat_profile_kernel(ctx, PROFILE_KINDS.get(kind, kind), period), ctx)
 
 
 def sdsat_kernel_time(ctx):

@@ -98,7 +98,7 @@ struct sdsat_ctx {
     double* inv_freq = nullptr;   // rotary inverse frequencies [Dh/2]
     // activations
     float* x = nullptr; float* ssq = nullptr;
-    void* xb = nullptr;   // x in the matrix element type, row stride d_pad (zero pad)
+    float* xg = nullptr;  // x o (next RMSNorm gain), float, row stride d_pad (zero pad)
     void* qbuf = nullptr; void* obuf = nullptr; void* ubuf = nullptr;
     // scratch
     float* attn_part = nullptr;
@@ -113,6 +113,8 @@ struct sdsat_ctx {
     std::vector<int> len_hint;
     // profiling
     int prof_kind = PK_OFF;
+    int prof_period = 1;
+    int64_t prof_seen = 0;
     std::vector<hipEvent_t> events;
     size_t ev_used = 0;
 };
@@ -149,8 +151,8 @@ void carve(sdsat_ctx* c, Carver& cv) {
     c->inv_freq = (double*)cv.take((size_t)(D.Dh / 2) * 8);
     c->x = (float*)cv.take((size_t)D.maxM * D.d * 4);
     c->ssq = (float*)cv.take((size_t)D.maxM * D.n_ssq * 4);
-    c->xb = cv.take((size_t)D.maxM * D.d_pad * e);
-    c->qbuf = cv.take((size_t)D.maxB * D.maxQ * D.d * e);
+    c->xg = (float*)cv.take((size_t)D.maxM * D.d_pad * 4);
+    c->qbuf = cv.take((size_t)D.maxB * D.maxQ * D.d * 4);
     c->obuf = cv.take((size_t)D.maxM * D.d_pad * e);
     c->ubuf = cv.take((size_t)D.maxM * D.F_pad * e);
     c->attn_part = (float*)cv.take(attention_partial_floats(D.maxB, D.H, D.maxQ, D.Dh) * 4);
@@ -178,6 +180,7 @@ void* layer_v(sdsat_ctx* c, int l) { return (char*)c->vc + (size_t)l * c->layer_
 void prof_begin(sdsat_ctx* c, int kind, hipEvent_t* out) {
     *out = nullptr;
     if (c->prof_kind != kind) return;
+    if (c->prof_seen++ % c->prof_period != 0) return;
     if (c->ev_used + 2 > c->events.size()) {
         for (int i = 0; i < 64; ++i) {
             // no system-scope fence on record: the interval then covers the kernel, not a cache flush
@@ -236,7 +239,7 @@ int fits(sdsat_ctx* c, int B, int q, bool* ok) {
     return SDSAT_OK;
 }
 
-int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask, const void* qbuf, void* out,
+int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask, const float* qbuf, void* out,
                     int out_f32, int ldo) {
     const Dims& D = c->D;
     const AttnPlan p = plan_attention(B, D.H, q, D.Dh, max_hint(c, B));
@@ -259,39 +262,40 @@ int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const 
     const int M = B * q;
     hipEvent_t evb;
     prof_begin(c, logits ? PK_BLOCK : PK_PREFILL, &evb);
-    HIPCHK(c, launch_embed(D.dtype, c->embed, D.V + D.A, D.d, tokens, M, c->x, c->xb, D.d_pad, c->ssq, D.n_ssq,
-                           c->err_flag, c->stream));
+    HIPCHK(c, launch_embed(D.dtype, c->embed, D.V + D.A, D.d, tokens, M, c->x, c->xg, c->attn_norm[0], D.d_pad,
+                           c->ssq, D.n_ssq, c->err_flag, c->stream));
     for (int l = 0; l < D.L; ++l) {
-        // attention sub-block: RMSNorm -> QKV (+RoPE, KV write) -> attention -> O (+residual)
+        // attention sub-block: RMSNorm -> QKV (+RoPE, KV write) -> attention -> O (+residual);
+        // xg holds x o (the gain of the RMSNorm the next GEMM applies)
         GemmArgs a{};
-        a.xa = c->xb; a.ldx = D.d_pad; a.ssq = c->ssq; a.n_ssq = D.n_ssq; a.eps = c->cfg.rms_eps;
+        a.xf = c->xg; a.ldx = D.d_pad; a.ssq = c->ssq; a.n_ssq = D.n_ssq; a.eps = c->cfg.rms_eps;
         a.qbuf = c->qbuf; a.kc = layer_k(c, l); a.vc = layer_v(c, l);
         a.cache_len = c->cache_len; a.q = q; a.H = D.H; a.Dh = D.Dh; a.S_max = D.S; a.mask = mask;
         a.inv_freq = c->inv_freq;
         int rc = run_gemm(c, PK_QKV, EP_QKV, M, D.nt_qkv, D.ks_d, 3 * D.d, D.d, c->w_qkv[l], a);
         if (rc) return rc;
-        rc = attention_layer(c, l, B, q, mask, c->qbuf, c->obuf, 0, D.d_pad);
+        rc = attention_layer(c, l, B, q, mask, (const float*)c->qbuf, c->obuf, 0, D.d_pad);
         if (rc) return rc;
         GemmArgs o{};
-        o.xa = c->obuf; o.ldx = D.d_pad; o.resid = c->x; o.ldy = D.d; o.xb = c->xb; o.ldxb = D.d_pad;
-        o.ssq_out = c->ssq;
+        o.xa = c->obuf; o.ldx = D.d_pad; o.resid = c->x; o.ldy = D.d; o.xg_out = c->xg; o.ldxg = D.d_pad;
+        o.gnext = c->ffn_norm[l]; o.ssq_out = c->ssq;
         rc = run_gemm(c, PK_O, EP_RESID, M, D.nt_o, D.ks_d, D.d, D.d, c->w_o[l], o);
         if (rc) return rc;
         // feed-forward sub-block: RMSNorm -> gate/up (+SwiGLU) -> down (+residual)
         GemmArgs f{};
-        f.xa = c->xb; f.ldx = D.d_pad; f.ssq = c->ssq; f.n_ssq = D.n_ssq; f.eps = c->cfg.rms_eps;
+        f.xf = c->xg; f.ldx = D.d_pad; f.ssq = c->ssq; f.n_ssq = D.n_ssq; f.eps = c->cfg.rms_eps;
         f.uout = c->ubuf; f.F = D.F; f.ldu = D.F_pad;
         rc = run_gemm(c, PK_GATEUP, EP_SWIGLU, M, D.nt_gu, D.ks_d, 2 * D.F, D.d, c->w_gu[l], f);
         if (rc) return rc;
         GemmArgs dn{};
-        dn.xa = c->ubuf; dn.ldx = D.F_pad; dn.resid = c->x; dn.ldy = D.d; dn.xb = c->xb; dn.ldxb = D.d_pad;
-        dn.ssq_out = c->ssq;
+        dn.xa = c->ubuf; dn.ldx = D.F_pad; dn.resid = c->x; dn.ldy = D.d; dn.xg_out = c->xg; dn.ldxg = D.d_pad;
+        dn.gnext = l + 1 < D.L ? c->attn_norm[l + 1] : c->final_norm; dn.ssq_out = c->ssq;
         rc = run_gemm(c, PK_DOWN, EP_RESID, M, D.nt_down, D.ks_f, D.d, D.F, c->w_down[l], dn);
         if (rc) return rc;
     }
     if (logits) {
         GemmArgs h{};
-        h.xa = c->xb; h.ldx = D.d_pad; h.ssq = c->ssq; h.n_ssq = D.n_ssq; h.eps = c->cfg.rms_eps;
+        h.xf = c->xg; h.ldx = D.d_pad; h.ssq = c->ssq; h.n_ssq = D.n_ssq; h.eps = c->cfg.rms_eps;
         h.y = logits; h.ldy = D.V;
         int rc = run_gemm(c, PK_LM, EP_STORE, M, D.nt_lm, D.ks_d, D.V, D.d, c->w_lm, h);
         if (rc) return rc;
@@ -374,26 +378,25 @@ int sdsat_init(const sdsat_config* cfg, const void* const* weights, int32_t n_we
         PackArgs p{};
         p.dtype = D.dtype; p.K = D.d; p.k_steps = D.ks_d; p.head_dim = D.Dh; p.F = D.F;
         // Wq, Wk, Wv stacked, rows grouped for RoPE pairs
-        // Wq, Wk, Wv stacked, rows grouped for RoPE pairs, attn_norm gain folded in
         p.perm = PACK_ROPE; p.N = 3 * D.d; p.n_tiles = D.nt_qkv; p.src0 = w[1]; p.src1 = w[2]; p.src2 = w[3];
-        p.N0 = D.d; p.N1 = D.d; p.gain = (const float*)w[0]; p.dst = c->w_qkv[l];
+        p.N0 = D.d; p.N1 = D.d; p.dst = c->w_qkv[l];
         launch_pack(p, c->stream);
         p.perm = PACK_PLAIN; p.N = D.d; p.n_tiles = D.nt_o; p.src0 = w[4]; p.src1 = p.src2 = nullptr;
-        p.N0 = D.d; p.N1 = 0; p.gain = nullptr; p.dst = c->w_o[l];
+        p.N0 = D.d; p.N1 = 0; p.dst = c->w_o[l];
         launch_pack(p, c->stream);
-        // gate and up interleaved per tile, ffn_norm gain folded in
+        // gate and up interleaved per tile
         p.perm = PACK_GATEUP; p.N = 2 * D.F; p.n_tiles = D.nt_gu; p.src0 = w[6]; p.src1 = w[7];
-        p.N0 = D.F; p.N1 = D.F; p.gain = (const float*)w[5]; p.dst = c->w_gu[l];
+        p.N0 = D.F; p.N1 = D.F; p.dst = c->w_gu[l];
         launch_pack(p, c->stream);
         p.perm = PACK_PLAIN; p.N = D.d; p.K = D.F; p.k_steps = D.ks_f; p.n_tiles = D.nt_down; p.src0 = w[8];
-        p.src1 = nullptr; p.N0 = D.d; p.N1 = 0; p.gain = nullptr; p.dst = c->w_down[l];
+        p.src1 = nullptr; p.N0 = D.d; p.N1 = 0; p.dst = c->w_down[l];
         launch_pack(p, c->stream);
     }
     c->final_norm = (const float*)weights[1 + 9 * D.L];
     {
         PackArgs p{};
         p.dtype = D.dtype; p.K = D.d; p.k_steps = D.ks_d; p.perm = PACK_PLAIN; p.N = D.V; p.n_tiles = D.nt_lm;
-        p.src0 = weights[2 + 9 * D.L]; p.N0 = D.V; p.gain = (const float*)weights[1 + 9 * D.L]; p.dst = c->w_lm;
+        p.src0 = weights[2 + 9 * D.L]; p.N0 = D.V; p.dst = c->w_lm;
         launch_pack(p, c->stream);
     }
     auto init_fail = [&](int code) { std::string m = c->err; delete c; return fail(nullptr, code, m); };
@@ -421,7 +424,7 @@ int sdsat_init(const sdsat_config* cfg, const void* const* weights, int32_t n_we
             return init_fail(SDSAT_EDEVICE);
         }
         // activation pads must read as zero
-        (void)launch_fill_i32((int*)c->xb, (size_t)D.maxM * D.d_pad * D.esz / 4, 0, c->stream);
+        (void)launch_fill_i32((int*)c->xg, (size_t)D.maxM * D.d_pad, 0, c->stream);
         (void)launch_fill_i32((int*)c->obuf, (size_t)D.maxM * D.d_pad * D.esz / 4, 0, c->stream);
         (void)launch_fill_i32((int*)c->ubuf, (size_t)D.maxM * D.F_pad * D.esz / 4, 0, c->stream);
         (void)launch_fill_i32(c->verify_cnt, D.maxB, 0, c->stream);
@@ -665,8 +668,8 @@ int sdsat_attention(sdsat_ctx* c, int32_t layer, int32_t batch, int32_t q, const
     rc = fits(c, batch, q, &ok);
     if (rc) return rc;
     if (!ok) return fail(c, SDSAT_ECAPACITY, "cache_len + q exceeds max_ctx");
-    HIPCHK(c, launch_to_elem(D.dtype, d_q, c->qbuf, (size_t)batch * q * D.d, c->stream));
-    return attention_layer(c, layer, batch, q, d_ancestor_mask, c->qbuf, d_out, 1, D.d);
+    HIPCHK(c, hipMemcpyAsync(c->qbuf, d_q, (size_t)batch * q * D.d * 4, hipMemcpyDeviceToDevice, c->stream));
+    return attention_layer(c, layer, batch, q, d_ancestor_mask, (const float*)c->qbuf, d_out, 1, D.d);
 }
 
 size_t sdsat_linear_packed_bytes(int32_t dtype, int32_t N, int32_t K) {
@@ -707,11 +710,14 @@ int sdsat_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const float* d_
     return SDSAT_OK;
 }
 
-int sdsat_profile_kernel(sdsat_ctx* c, int32_t kind) {
+int sdsat_profile_kernel(sdsat_ctx* c, int32_t kind, int32_t period) {
     if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
     if (kind < 0 || kind > 8) return fail(c, SDSAT_EINVAL, "bad kernel kind");
+    if (period < 1) return fail(c, SDSAT_EINVAL, "period must be >= 1");
     HIPCHK(c, hipStreamSynchronize(c->stream));
     c->prof_kind = kind;
+    c->prof_period = period;
+    c->prof_seen = 0;
     c->ev_used = 0;
     return SDSAT_OK;
 }

@@ -8,6 +8,11 @@
 //
 // Workgroups per (b, h): one, or a few key splits when the (b, h) pairs alone
 // cannot fill the GPU.  Waves take the workgroup's 32-key blocks round-robin.
+// Q arrives in float and the probabilities are formed in float; on bf16
+// models each enters the matrix cores as a pair of bf16 fragments (value and
+// rounding remainder, about 16 significant bits), so neither is rounded to
+// bf16 on its way: the scores and the weighted sum of V keep float accuracy
+// (K and V are bf16 as stored).
 // Query rows are handled 16 at a time (one matrix-core tile); a block of more
 // rows (a prefill chunk) loops over its row tiles and re-reads the keys, which
 // then come from L2.  Per block a wave computes the 32 x 16 score tile
@@ -72,19 +77,54 @@ __device__ __forceinline__ void load_kv(Frag<T> (&kf)[2][NDS], Frag<T> (&vf)[NDT
     for (int dt = 0; dt < NDT; ++dt) vf[dt] = Frag<T>::load(vblk + (size_t)(dt * 16 + c) * 32 + 8 * g);
 }
 
+// x as the matrix-core operand pair hi + lo (lo = the bf16 rounding remainder;
+// float models use x itself and no second fragment).
+template <typename T>
+__device__ __forceinline__ void split_frag(const float (&x)[8], Frag<T>& hi, Frag<T>& lo) {
+    hi = Frag<T>::from_f32(x);
+    if constexpr (sizeof(T) == 2) {
+        float r[8];
+        const uint32_t w[4] = {hi.v.x, hi.v.y, hi.v.z, hi.v.w};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) r[i] = x[i] - bf16_to_f32((uint16_t)(w[i / 2] >> (16 * (i % 2))));
+        lo = Frag<T>::from_f32(r);
+    }
+}
+
 // One 32-key block for the 16 query rows of this lane group (lane column c is
 // block row m = m0 + c).
+// Q fragments of the current row tile, in LDS: [hi / lo][ds][lane].  They are
+// read where they are used, which keeps them out of the register budget.
+template <typename T>
+__device__ __forceinline__ Frag<T> lds_frag(const Frag<T>* qs, int idx) {
+    Frag<T> f;
+    if constexpr (sizeof(T) == 2) {
+        f.v = *reinterpret_cast<const volatile u32x4_t*>(&qs[idx].v);
+    } else {
+        f.lo = *reinterpret_cast<const volatile f32x4_t*>(&qs[idx].lo);
+        f.hi = *reinterpret_cast<const volatile f32x4_t*>(&qs[idx].hi);
+    }
+    return f;
+}
+
 template <typename T, int NDS, int NDT>
 __device__ __forceinline__ void attend_block(const Frag<T> (&kf)[2][NDS], const Frag<T> (&vf)[NDT],
-                                             const Frag<T> (&qf)[NDS], uint64_t mrow, int blk, int m, int L, int Tb,
-                                             int q, bool tree, float scale, int g, float& rmax, float& rsum,
-                                             f32x4_t (&o)[NDT]) {
+                                             const Frag<T>* qs, int lane, uint64_t mrow,
+                                             int blk, int m, int L, int Tb, int q, bool tree, float scale, int g,
+                                             float& rmax, float& rsum, f32x4_t (&o)[NDT]) {
+    constexpr bool two = sizeof(T) == 2;
     const int kb0 = blk * 32;
     f32x4_t s0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, s1 = s0;
 #pragma unroll
     for (int ds = 0; ds < NDS; ++ds) {
-        mma(s0, kf[0][ds], qf[ds]);
-        mma(s1, kf[1][ds], qf[ds]);
+        const Frag<T> qh = lds_frag<T>(qs, ds * 64 + lane);
+        mma(s0, kf[0][ds], qh);
+        mma(s1, kf[1][ds], qh);
+        if constexpr (two) {
+            const Frag<T> ql = lds_frag<T>(qs, (NDS + ds) * 64 + lane);
+            mma(s0, kf[0][ds], ql);
+            mma(s1, kf[1][ds], ql);
+        }
     }
     // s0[r], s1[r] = S^T[key = kb0 + 16kt + 4g + r][row m]
     float sv[8];
@@ -114,11 +154,13 @@ __device__ __forceinline__ void attend_block(const Frag<T> (&kf)[2][NDS], const 
     }
     rsum = rsum * alpha + ps;
     rmax = nmax;
-    const Frag<T> pf = Frag<T>::from_f32(p);
+    Frag<T> ph, pl;
+    split_frag<T>(p, ph, pl);
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) {
         o[dt] *= alpha;
-        mma(o[dt], vf[dt], pf);
+        mma(o[dt], vf[dt], ph);
+        if constexpr (two) mma(o[dt], vf[dt], pl);
     }
 }
 
@@ -129,6 +171,7 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     f32x4_t* opart = reinterpret_cast<f32x4_t*>(smem_raw);   // [waves][NDT][64]
     __shared__ float s_max[kMaxWaves][16], s_sum[kMaxWaves][16];
+    __shared__ Frag<T> s_q[2 * NDS * 64];                      // Q of the row tile: [hi / lo][ds][lane]
 
     const int nw = blockDim.x >> 6;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -138,7 +181,7 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     const int q = a.q;
     const T* kbase = reinterpret_cast<const T*>(a.kc) + ((size_t)b * a.H + h) * a.S_max * DH;
     const T* vbase = reinterpret_cast<const T*>(a.vc) + ((size_t)b * a.H + h) * a.S_max * DH;
-    const T* qb = reinterpret_cast<const T*>(a.qbuf);
+    const float* qb = a.qbuf;
     const bool tree = a.mask != nullptr;
 
     // Split sp owns blocks [wlo, wlo + per_wg) of the partition the host's
@@ -162,10 +205,17 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
         const int m = 16 * rt + c;
         const int mr = min(m, q - 1);
         const uint64_t mrow = tree ? a.mask[(size_t)b * q + mr] : 0ull;
-        Frag<T> qf[NDS];
-#pragma unroll
-        for (int ds = 0; ds < NDS; ++ds)
-            qf[ds] = Frag<T>::load(qb + (((size_t)b * q + mr) * a.H + h) * DH + ds * 32 + 8 * g);
+        if (rt > 0) __syncthreads();   // every wave is done with the previous tile's Q and merge
+        for (int ds = wave; ds < NDS; ds += nw) {   // Q columns 32ds.. of the tile's rows as hi / lo
+            const f32x4_t* src = reinterpret_cast<const f32x4_t*>(qb + (((size_t)b * q + mr) * a.H + h) * DH +
+                                                                  ds * 32 + 8 * g);
+            const f32x4_t lo4 = src[0], hi4 = src[1];
+            const float x8[8] = {lo4.x, lo4.y, lo4.z, lo4.w, hi4.x, hi4.y, hi4.z, hi4.w};
+            Frag<T> fh, fl;
+            split_frag<T>(x8, fh, fl);
+            s_q[ds * 64 + lane] = fh;
+            if constexpr (sizeof(T) == 2) s_q[(NDS + ds) * 64 + lane] = fl;
+        }
         Frag<T> kA[2][NDS], kB[2][NDS], vA[NDT], vB[NDT];
         load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, min(first, last_blk), c, g);
         load_kv<T, NDS, NDT>(kB, vB, kbase, vbase, min(first + nw, last_blk), c, g);
@@ -179,6 +229,7 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
             whi = sp == a.splits - 1 ? nblk : min(nblk, wlo + per_wg);
         }
         const int Tb = L + q;
+        __syncthreads();   // the tile's Q fragments are in LDS
 
         float rmax = -INFINITY, rsum = 0.f;
         f32x4_t o[NDT];
@@ -190,26 +241,25 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
         int i = 0;
         // steady state (unconditional loads): blocks i and i + 1 are loaded
         for (; i + 4 <= cnt; i += 2) {
-            attend_block<T, NDS, NDT>(kA, vA, qf, mrow, first + i * nw, m, L, Tb, q, tree, a.scale, g, rmax, rsum, o);
+            attend_block<T, NDS, NDT>(kA, vA, s_q, lane, mrow, first + i * nw, m, L, Tb, q, tree, a.scale, g, rmax, rsum, o);
             load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, first + (i + 2) * nw, c, g);
-            attend_block<T, NDS, NDT>(kB, vB, qf, mrow, first + (i + 1) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
+            attend_block<T, NDS, NDT>(kB, vB, s_q, lane, mrow, first + (i + 1) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
                                       rsum, o);
             load_kv<T, NDS, NDT>(kB, vB, kbase, vbase, first + (i + 3) * nw, c, g);
         }
         // 0 .. 3 blocks left
         if (i < cnt)
-            attend_block<T, NDS, NDT>(kA, vA, qf, mrow, first + i * nw, m, L, Tb, q, tree, a.scale, g, rmax, rsum, o);
+            attend_block<T, NDS, NDT>(kA, vA, s_q, lane, mrow, first + i * nw, m, L, Tb, q, tree, a.scale, g, rmax, rsum, o);
         if (i + 2 < cnt) load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, first + (i + 2) * nw, c, g);
         if (i + 1 < cnt)
-            attend_block<T, NDS, NDT>(kB, vB, qf, mrow, first + (i + 1) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
+            attend_block<T, NDS, NDT>(kB, vB, s_q, lane, mrow, first + (i + 1) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
                                       rsum, o);
         if (i + 2 < cnt)
-            attend_block<T, NDS, NDT>(kA, vA, qf, mrow, first + (i + 2) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
+            attend_block<T, NDS, NDT>(kA, vA, s_q, lane, mrow, first + (i + 2) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
                                       rsum, o);
 
         rsum += __shfl_xor(rsum, 16, 64);
         rsum += __shfl_xor(rsum, 32, 64);
-        if (rt > 0) __syncthreads();   // the previous tile's merge has read LDS
         if (g == 0) {
             s_max[wave][c] = rmax;
             s_sum[wave][c] = rsum;

@@ -21,12 +21,17 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-// Round to nearest even (finite inputs).
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two floats to a packed bf16 pair (low half = a), round to nearest even: one
+// v_cvt_pk_bf16_f32 on gfx950.
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{a, b}), bf16x2_t));
 }
+
+// Round to nearest even.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) { return (uint16_t)f32x2_to_bf16x2(f, 0.f); }
 
 template <typename T> struct Frag;
 
@@ -38,13 +43,17 @@ template <> struct Frag<uint16_t> {
         Frag f; f.v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p)); return f;
     }
     __device__ __forceinline__ void store(uint16_t* p) const { *reinterpret_cast<u32x4_t*>(p) = v; }
+    __device__ __forceinline__ float get(int j) const {   // element j as float
+        const uint32_t w = v[j >> 1];
+        return __uint_as_float((j & 1) ? (w & 0xFFFF0000u) : (w << 16));
+    }
     // 8 floats rounded to bf16
     __device__ __forceinline__ static Frag from_f32(const float* x) {
         Frag f;
-        f.v.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
-        f.v.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
-        f.v.z = (uint32_t)f32_to_bf16(x[4]) | ((uint32_t)f32_to_bf16(x[5]) << 16);
-        f.v.w = (uint32_t)f32_to_bf16(x[6]) | ((uint32_t)f32_to_bf16(x[7]) << 16);
+        f.v.x = f32x2_to_bf16x2(x[0], x[1]);
+        f.v.y = f32x2_to_bf16x2(x[2], x[3]);
+        f.v.z = f32x2_to_bf16x2(x[4], x[5]);
+        f.v.w = f32x2_to_bf16x2(x[6], x[7]);
         return f;
     }
 };
@@ -66,6 +75,7 @@ template <> struct Frag<float> {
     __device__ __forceinline__ void store(float* p) const {
         reinterpret_cast<f32x4_t*>(p)[0] = lo; reinterpret_cast<f32x4_t*>(p)[1] = hi;
     }
+    __device__ __forceinline__ float get(int j) const { return j < 4 ? lo[j] : hi[j - 4]; }
     __device__ __forceinline__ static Frag from_f32(const float* x) {
         Frag f; f.lo = f32x4_t{x[0], x[1], x[2], x[3]}; f.hi = f32x4_t{x[4], x[5], x[6], x[7]}; return f;
     }

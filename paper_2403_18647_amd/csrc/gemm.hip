@@ -5,22 +5,28 @@
 //
 //  * W is pre-packed (launch_pack) into 16-column x 32-k tiles laid out in lane
 //    order, so every wave-wide load is one contiguous 1 KiB (bf16) run and each
-//    lane's 16 bytes is directly its matrix-core B fragment.  RMSNorm gains are
-//    folded into the packed columns, so a normalised input is the raw residual
-//    row times a per-row scale applied in the epilogue.
-//  * One workgroup per column tile.  Its waves split the contraction into
-//    contiguous slices, stream their slice with two batches of loads in flight,
-//    read the X fragments for the same steps straight from global memory (the
-//    few X rows stay in L2), and reduce their partial tiles through LDS in
-//    wave order: deterministic, with no device-scope fences or atomics.
+//    lane's 16 bytes is directly its matrix-core B fragment.
+//  * One workgroup per column tile (4 for prefill chunks).  Its waves split the
+//    contraction into contiguous slices, stream their slice with two batches of
+//    loads in flight, read the X fragments for the same steps straight from
+//    global memory (the few X rows stay in L2), and reduce their partial tiles
+//    through LDS in wave order: deterministic, with no device-scope fences or
+//    atomics.
+//  * An RMSNorm input arrives as the float rows x o g (gain applied by the
+//    producer); the kernel reduces the producer's per-tile sums of squares to
+//    each row's 1/rms before its first matrix-core step and rounds
+//    x o g / rms to the element type at the matrix-core input: the normalised
+//    activation a bf16 model stores, rounded once.
 //  * Fused epilogues, run by wave 0 on the reduced tile:
 //      EP_STORE   float output (LM-head logits)
-//      EP_QKV     RoPE on Q and K columns, Q to its buffer, K and V into the
-//                 cache slots of the block rows (positions cache_len[b] + r)
-//      EP_RESID   residual add into the float residual stream, a copy in the
-//                 matrix element type for the next GEMM, and per-tile sums of
-//                 squares that the next RMSNorm reduces
+//      EP_QKV     RoPE on Q and K columns, Q (float) to its buffer, K and V into
+//                 the cache slots of the block rows (positions cache_len[b] + r)
+//      EP_RESID   residual add into the float residual stream, the updated rows
+//                 times the next RMSNorm's gain, and per-tile sums of squares
+//                 that the next RMSNorm reduces
 //      EP_SWIGLU  silu(gate) * up, rounded to the activation type
+#include <type_traits>
+
 #include "device.h"
 #include "kernels.h"
 
@@ -62,10 +68,7 @@ __global__ void pack_kernel(PackArgs a) {
     for (int e = 0; e < 8; ++e) {
         const int k = 32 * ks + 8 * g + e;
         float v = 0.f;
-        if (src && k < a.K) {
-            v = to_f32<T>(src[r * a.K + k]);
-            if (a.gain) v *= a.gain[k];
-        }
+        if (src && k < a.K) v = to_f32<T>(src[r * a.K + k]);
         dst[e] = to_elem<T>(v);
     }
 }
@@ -77,14 +80,16 @@ void launch_pack(const PackArgs& a, hipStream_t s) {
     else hipLaunchKernelGGL(pack_kernel<float>, dim3(blocks), dim3(256), 0, s, a);
 }
 
-// Waves per workgroup (measured on MI355X at M = 6 with weights streamed from
-// HBM): 8 for the narrow [d, d] / [d, F] matrices, 4 for the wide ones; at
-// least 4 contraction steps per wave.  Blocks of more than 16 rows (prefill
-// chunks) reload their X fragments for every weight fragment; for the wide
-// matrices a workgroup of 4 waves then takes 4 column tiles so that one X
-// load feeds 4 tiles' matrix-core steps (measured at M = 64: QKV 55 -> 37 us,
-// gate/up 103 -> 62 us); the narrow ones keep one tile per workgroup, which
-// keeps all compute units streaming.
+// Plans (measured on MI355X with weights streamed from HBM):
+//  * blocks of up to 16 rows: one column tile per workgroup, 8 waves for the
+//    narrow [d, d] / [d, F] matrices (256 tiles, one workgroup per compute
+//    unit), 4 for the wide ones; at least 4 contraction steps per wave
+//    (several tiles per workgroup, or X staged in LDS, measured slower);
+//  * blocks of more than 16 rows (prefill chunks) reload their X fragments
+//    for every weight fragment: for the wide matrices a workgroup of 4 waves
+//    takes 4 column tiles so that one X load feeds 4 tiles' matrix-core steps
+//    (M = 64: QKV 55 -> 37 us, gate/up 103 -> 62 us); the narrow ones keep one
+//    tile per workgroup.
 GemmPlan plan_gemm(int M, int n_tiles, int k_steps) {
     GemmPlan p;
     p.mt = (M + 15) / 16;
@@ -98,11 +103,28 @@ GemmPlan plan_gemm(int M, int n_tiles, int k_steps) {
 }
 
 // Steps per load batch (two batches in flight), sized so both batches of
-// weight and X fragments fit the register budget (128 VGPRs at 16 waves per
-// CU for one tile per wave; 4-tile workgroups have 4 waves).
-template <typename T, int MT> struct Batch {
-    static constexpr int U = sizeof(T) == 2 ? (MT == 1 ? 4 : 2) : (MT == 1 ? 2 : 1);
+// weight and X fragments fit the register budget (float X fragments of an
+// RMSNorm input take twice the registers of bf16 ones).
+template <typename T, int MT, bool XF> struct Batch {
+    static constexpr int U = MT == 1 ? (sizeof(T) == 2 ? (XF ? 3 : 4) : 2) : (sizeof(T) == 2 && !XF ? 2 : 1);
 };
+
+// X fragment as loaded: the element type, or raw floats of an RMSNorm input.
+template <typename T, bool XF> struct XIn { using type = Frag<T>; };
+template <typename T> struct XIn<T, true> { using type = Frag<float>; };
+
+// Matrix-core A fragment from a loaded X fragment: RMSNorm inputs are scaled
+// by the row's 1/rms and rounded to the element type here.
+template <typename T, bool XF, typename XT>
+__device__ __forceinline__ Frag<T> a_frag(const XT& x, float inv) {
+    if constexpr (XF) {
+        float v[8] = {x.lo.x * inv, x.lo.y * inv, x.lo.z * inv, x.lo.w * inv,
+                      x.hi.x * inv, x.hi.y * inv, x.hi.z * inv, x.hi.w * inv};
+        return Frag<T>::from_f32(v);
+    } else {
+        return x;
+    }
+}
 
 // One batch of U contraction steps: the weight fragments of the NTW tiles
 // (streamed, non-temporal) and the X fragments of every row tile.  Rows past
@@ -110,9 +132,10 @@ template <typename T, int MT> struct Batch {
 // past the wave's slice: those steps reload the last step with X zeroed.
 // Loads of the steady-state loop are unconditional so that the compiler's
 // wait counts stay exact and two batches really are in flight.
-template <typename T, int MT, int NTW, int U, bool TAIL>
-__device__ __forceinline__ void load_batch(Frag<T> (&w)[U][NTW], Frag<T> (&x)[U][MT], const T* const (&wp)[NTW],
-                                           const T* const (&xr)[MT], int s, int nks) {
+template <typename T, typename XT, int MT, int NTW, int U, bool TAIL>
+__device__ __forceinline__ void load_batch(Frag<T> (&w)[U][NTW], XT (&x)[U][MT], const T* const (&wp)[NTW],
+                                           const void* const (&xr)[MT], int s, int nks) {
+    using XE = typename std::conditional<sizeof(XT) == 32, float, T>::type;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int st = TAIL ? min(s + u, nks - 1) : s + u;
@@ -120,21 +143,23 @@ __device__ __forceinline__ void load_batch(Frag<T> (&w)[U][NTW], Frag<T> (&x)[U]
         for (int j = 0; j < NTW; ++j) w[u][j] = Frag<T>::load_nt(wp[j] + (size_t)st * 512);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            x[u][mt] = Frag<T>::load(xr[mt] + st * 32);
-            if (TAIL && s + u >= nks) x[u][mt] = Frag<T>::zero();
+            x[u][mt] = XT::load(reinterpret_cast<const XE*>(xr[mt]) + st * 32);
+            if (TAIL && s + u >= nks) x[u][mt] = XT::zero();
         }
     }
 }
 
-template <typename T, int MT, int NTW, int U>
+template <typename T, bool XF, typename XT, int MT, int NTW, int U>
 __device__ __forceinline__ void mma_batch(f32x4_t (&acc)[NTW][MT], const Frag<T> (&w)[U][NTW],
-                                          const Frag<T> (&x)[U][MT]) {
+                                          const XT (&x)[U][MT], const float (&inv)[MT]) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int j = 0; j < NTW; ++j)
+        for (int mt = 0; mt < MT; ++mt) {
+            const Frag<T> xa = a_frag<T, XF>(x[u][mt], inv[mt]);
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) mma(acc[j][mt], x[u][mt], w[u][j]);
+            for (int j = 0; j < NTW; ++j) mma(acc[j][mt], xa, w[u][j]);
+        }
 }
 
 // Fused epilogue of one reduced tile (run by wave 0).
@@ -154,7 +179,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int tile, const f32x
             }
     } else if (EP == EP_RESID) {
         const int n = tile * 16 + c;
-        T* xb = reinterpret_cast<T*>(a.xb);
+        const float gn = n < a.N ? a.gnext[n] : 0.f;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -164,7 +189,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int tile, const f32x
                 if (m < M && n < a.N) {
                     const float v = ep_in[mt][r] + acc[mt][r];
                     a.resid[(size_t)m * a.ldy + n] = v;
-                    xb[(size_t)m * a.ldxb + n] = to_elem<T>(v);
+                    a.xg_out[(size_t)m * a.ldxg + n] = v * gn;
                     ss = v * v;
                 }
                 ss += __shfl_xor(ss, 8, 64);
@@ -223,7 +248,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int tile, const f32x
                     out = c < 8 ? mine * cs - other * sn : other * sn + mine * cs;
                 }
                 if (sec == 0) {
-                    reinterpret_cast<T*>(a.qbuf)[((size_t)m * H + h) * Dh + dim] = to_elem<T>(out);
+                    reinterpret_cast<float*>(a.qbuf)[((size_t)m * H + h) * Dh + dim] = out;
                 } else if (sec == 1) {
                     reinterpret_cast<T*>(a.kc)[(((size_t)b * H + h) * a.S_max + pos) * Dh + dim] = to_elem<T>(out);
                 } else {
@@ -234,9 +259,10 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int tile, const f32x
     }
 }
 
-template <typename T, int EP, int MT, int NTW>
-__global__ void __launch_bounds__(NTW == 1 ? 1024 : 512) gemm_kernel(GemmArgs a) {
-    constexpr int U = Batch<T, MT>::U;
+template <typename T, int EP, int MT, int NTW, bool XF>
+__global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(GemmArgs a) {
+    constexpr int U = Batch<T, MT, XF>::U;
+    using XT = typename XIn<T, XF>::type;
     extern __shared__ __align__(16) unsigned char smem_raw[];
     f32x4_t* red = reinterpret_cast<f32x4_t*>(smem_raw);   // [waves][MT][64]
     __shared__ float s_inv[64];
@@ -257,17 +283,10 @@ __global__ void __launch_bounds__(NTW == 1 ? 1024 : 512) gemm_kernel(GemmArgs a)
         const int t = min(tile0 + j, a.n_tiles - 1);   // a tile past the end is read, not stored
         wp[j] = reinterpret_cast<const T*>(a.W) + (((size_t)t * a.k_steps + ks0) * 64 + lane) * 8;
     }
-    const T* xr[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int m = 16 * mt + c;
-        xr[mt] = reinterpret_cast<const T*>(a.xa) + (size_t)(m < M ? m : 0) * a.ldx + ks0 * 32 + 8 * g;
-    }
 
-    // Loads whose values are only needed after the main loop are issued first:
-    // RMSNorm partial sums (wave w takes rows w, w+nw, ... <= 2 per wave),
-    // and wave 0's epilogue inputs (residual values, cache lengths, rotary
-    // inverse frequencies).  vmcnt is in order, so they never stall the stream.
+    // RMSNorm partial sums (wave w reduces rows w, w+nw, ...; the first two
+    // are requested here, ahead of the weight stream) and wave 0's epilogue
+    // inputs (residual values, cache lengths, rotary inverse frequencies).
     constexpr int NSQ = 4;   // ssq partials per lane and row (n_ssq <= 256)
     float sq[2][NSQ];
 #pragma unroll
@@ -275,7 +294,7 @@ __global__ void __launch_bounds__(NTW == 1 ? 1024 : 512) gemm_kernel(GemmArgs a)
 #pragma unroll
         for (int t = 0; t < NSQ; ++t) {
             const int m = wave + j * nw, col = lane + 64 * t;
-            sq[j][t] = (a.ssq && m < M && col < a.n_ssq) ? a.ssq[(size_t)m * a.n_ssq + col] : 0.f;
+            sq[j][t] = (XF && m < M && col < a.n_ssq) ? a.ssq[(size_t)m * a.n_ssq + col] : 0.f;
         }
     // EP_RESID: residual values per tile; EP_QKV: cache_len of each row's
     // sequence (the same for every tile) and the rotary inverse frequency of
@@ -315,29 +334,29 @@ __global__ void __launch_bounds__(NTW == 1 ? 1024 : 512) gemm_kernel(GemmArgs a)
     for (int j = 0; j < NTW; ++j)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    // Both weight batches are in flight before anything waits, then the loop
+    // keeps two in flight.
     Frag<T> w0[U][NTW], w1[U][NTW];
-    Frag<T> x0[U][MT], x1[U][MT];
-    if (nks > 0) {
-        load_batch<T, MT, NTW, U, true>(w0, x0, wp, xr, 0, nks);
-        int s = 0;
-        // steady state: batches s and s + U are in flight, s + 2U is requested
-        // as soon as s has been consumed
-        for (; s + 3 * U <= nks; s += 2 * U) {
-            load_batch<T, MT, NTW, U, false>(w1, x1, wp, xr, s + U, nks);
-            mma_batch<T, MT, NTW, U>(acc, w0, x0);
-            load_batch<T, MT, NTW, U, false>(w0, x0, wp, xr, s + 2 * U, nks);
-            mma_batch<T, MT, NTW, U>(acc, w1, x1);
-        }
-        // tail: 1 .. 3U steps left, the first batch of them already loaded
-        if (s + U < nks) load_batch<T, MT, NTW, U, true>(w1, x1, wp, xr, s + U, nks);
-        mma_batch<T, MT, NTW, U>(acc, w0, x0);
-        if (s + 2 * U < nks) load_batch<T, MT, NTW, U, true>(w0, x0, wp, xr, s + 2 * U, nks);
-        if (s + U < nks) mma_batch<T, MT, NTW, U>(acc, w1, x1);
-        if (s + 2 * U < nks) mma_batch<T, MT, NTW, U>(acc, w0, x0);
+    XT x0[U][MT], x1[U][MT];
+    const void* xr[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const int m = 16 * mt + c;
+        const size_t off = (size_t)(m < M ? m : 0) * a.ldx + ks0 * 32 + 8 * g;
+        xr[mt] = XF ? (const void*)(a.xf + off) : (const void*)(reinterpret_cast<const T*>(a.xa) + off);
     }
-    // RMSNorm row scales (rows past the prefetched ones, and partials past
-    // 64 * NSQ columns, are read now)
-    if (a.ssq) {
+    if (nks > 0) {
+        load_batch<T, XT, MT, NTW, U, true>(w0, x0, wp, xr, 0, nks);
+        load_batch<T, XT, MT, NTW, U, true>(w1, x1, wp, xr, U, nks);
+    }
+
+    // row scales 1/rms, needed before the first matrix-core step (rows past
+    // the two prefetched ones, and partials past 64 * NSQ columns, are read now)
+    float inv[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) inv[mt] = 1.f;
+    if (XF) {
         for (int m = wave, j = 0; m < M; m += nw, ++j) {
             float v = 0.f;
             if (j < 2) {
@@ -350,6 +369,31 @@ __global__ void __launch_bounds__(NTW == 1 ? 1024 : 512) gemm_kernel(GemmArgs a)
             v = wave_sum(v);
             if (lane == 0) s_inv[m] = 1.0f / sqrtf(v / (float)a.K + a.eps);
         }
+        __syncthreads();
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const int m = 16 * mt + c;
+            inv[mt] = m < M ? s_inv[m] : 0.f;
+        }
+    }
+
+    if (nks > 0) {
+        // steady state: batches s (buffers 0) and s + U (buffers 1) are in
+        // flight; each is refilled with the batch two ahead once consumed
+        int s = 0;
+        for (; s + 4 * U <= nks; s += 2 * U) {
+            mma_batch<T, XF, XT, MT, NTW, U>(acc, w0, x0, inv);
+            load_batch<T, XT, MT, NTW, U, false>(w0, x0, wp, xr, s + 2 * U, nks);
+            mma_batch<T, XF, XT, MT, NTW, U>(acc, w1, x1, inv);
+            load_batch<T, XT, MT, NTW, U, false>(w1, x1, wp, xr, s + 3 * U, nks);
+        }
+        // tail: steps s .. nks-1 (fewer than 4U), the first two batches loaded
+        mma_batch<T, XF, XT, MT, NTW, U>(acc, w0, x0, inv);
+        if (s + 2 * U < nks) load_batch<T, XT, MT, NTW, U, true>(w0, x0, wp, xr, s + 2 * U, nks);
+        if (s + U < nks) mma_batch<T, XF, XT, MT, NTW, U>(acc, w1, x1, inv);
+        if (s + 3 * U < nks) load_batch<T, XT, MT, NTW, U, true>(w1, x1, wp, xr, s + 3 * U, nks);
+        if (s + 2 * U < nks) mma_batch<T, XF, XT, MT, NTW, U>(acc, w0, x0, inv);
+        if (s + 3 * U < nks) mma_batch<T, XF, XT, MT, NTW, U>(acc, w1, x1, inv);
     }
 
     // cross-wave reduction in wave order, one tile at a time (LDS holds
@@ -367,44 +411,40 @@ __global__ void __launch_bounds__(NTW == 1 ? 1024 : 512) gemm_kernel(GemmArgs a)
         for (int mt = 0; mt < MT; ++mt) {
             f32x4_t v = red[mt * 64 + lane];
             for (int w = 1; w < nw; ++w) v += red[(w * MT + mt) * 64 + lane];
-            if (a.ssq) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int m = 16 * mt + 4 * g + r;
-                    if (m < M) v[r] *= s_inv[m];
-                }
-            }
             t_acc[mt] = v;
         }
         epilogue<T, EP, MT>(a, tile0 + j, t_acc, ep_in[j < NEP ? j : 0], inv_freq[j], c, g);
     }
 }
 
-template <typename T, int EP>
+template <typename T, int EP, bool XF>
 static hipError_t launch_mt(const GemmPlan& p, const GemmArgs& a, hipStream_t s) {
     const dim3 grid(p.grid), block(64 * p.waves);
-    const int key = p.mt * 10 + p.ntw;
-    if (p.ntw > 1 && p.waves > 8) return hipErrorInvalidValue;
-    switch (key) {
-        case 11: hipLaunchKernelGGL((gemm_kernel<T, EP, 1, 1>), grid, block, p.lds_bytes, s, a); break;
-        case 21: hipLaunchKernelGGL((gemm_kernel<T, EP, 2, 1>), grid, block, p.lds_bytes, s, a); break;
-        case 31: hipLaunchKernelGGL((gemm_kernel<T, EP, 3, 1>), grid, block, p.lds_bytes, s, a); break;
-        case 41: hipLaunchKernelGGL((gemm_kernel<T, EP, 4, 1>), grid, block, p.lds_bytes, s, a); break;
-        case 24: hipLaunchKernelGGL((gemm_kernel<T, EP, 2, 4>), grid, block, p.lds_bytes, s, a); break;
-        case 34: hipLaunchKernelGGL((gemm_kernel<T, EP, 3, 4>), grid, block, p.lds_bytes, s, a); break;
-        case 44: hipLaunchKernelGGL((gemm_kernel<T, EP, 4, 4>), grid, block, p.lds_bytes, s, a); break;
+    if ((p.ntw > 1 || XF) && p.waves > 8) return hipErrorInvalidValue;
+    switch (p.mt * 10 + p.ntw) {
+        case 11: hipLaunchKernelGGL((gemm_kernel<T, EP, 1, 1, XF>), grid, block, p.lds_bytes, s, a); break;
+        case 21: hipLaunchKernelGGL((gemm_kernel<T, EP, 2, 1, XF>), grid, block, p.lds_bytes, s, a); break;
+        case 31: hipLaunchKernelGGL((gemm_kernel<T, EP, 3, 1, XF>), grid, block, p.lds_bytes, s, a); break;
+        case 41: hipLaunchKernelGGL((gemm_kernel<T, EP, 4, 1, XF>), grid, block, p.lds_bytes, s, a); break;
+        case 24: hipLaunchKernelGGL((gemm_kernel<T, EP, 2, 4, XF>), grid, block, p.lds_bytes, s, a); break;
+        case 34: hipLaunchKernelGGL((gemm_kernel<T, EP, 3, 4, XF>), grid, block, p.lds_bytes, s, a); break;
+        case 44: hipLaunchKernelGGL((gemm_kernel<T, EP, 4, 4, XF>), grid, block, p.lds_bytes, s, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
+// RMSNorm-input GEMMs (QKV, gate/up, LM head) read float x o g rows; O and
+// down read element-type rows (attention output, SwiGLU product).
 template <typename T>
 static hipError_t launch_t(int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s) {
+    const bool xf = a.xf != nullptr;
+    if (xf && !a.ssq) return hipErrorInvalidValue;
     switch (ep) {
-        case EP_STORE: return launch_mt<T, EP_STORE>(p, a, s);
-        case EP_QKV: return launch_mt<T, EP_QKV>(p, a, s);
-        case EP_RESID: return launch_mt<T, EP_RESID>(p, a, s);
-        case EP_SWIGLU: return launch_mt<T, EP_SWIGLU>(p, a, s);
+        case EP_STORE: return xf ? launch_mt<T, EP_STORE, true>(p, a, s) : launch_mt<T, EP_STORE, false>(p, a, s);
+        case EP_QKV: return xf ? launch_mt<T, EP_QKV, true>(p, a, s) : hipErrorInvalidValue;
+        case EP_RESID: return xf ? hipErrorInvalidValue : launch_mt<T, EP_RESID, false>(p, a, s);
+        case EP_SWIGLU: return xf ? launch_mt<T, EP_SWIGLU, true>(p, a, s) : hipErrorInvalidValue;
         default: return hipErrorInvalidValue;
     }
 }

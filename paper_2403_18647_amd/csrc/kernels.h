@@ -30,34 +30,39 @@ struct PackArgs {
     const void* src1;   // rows [N0, N0+N1) (stacked second matrix) or null
     const void* src2;
     int N0, N1;         // row counts of src0, src1 (src2 takes the rest)
-    const float* gain;  // optional per-column scale folded in: packed W[n][k] = W[n][k] * gain[k]
     void* dst;
 };
 void launch_pack(const PackArgs& a, hipStream_t s);
 size_t packed_elems(int n_tiles, int k_steps);
 
 // ---------------------------------------------------------------- skinny GEMM
-// One workgroup per 16-column tile; its waves split the contraction and
-// reduce through LDS.  X rows are read straight from global memory as
-// matrix-core fragments: X is stored in the matrix element type with a row
-// stride that covers the 32-padded contraction length, zero past K.
+// One workgroup per 16-column tile (or 4 tiles for prefill chunks); its waves
+// split the contraction and reduce through LDS.  X rows are read straight from
+// global memory as matrix-core fragments, either
+//  * stored in the matrix element type with a row stride that covers the
+//    32-padded contraction length, zero past K (xa), or
+//  * as the float rows x o g of an RMSNorm input (xf, gain already applied):
+//    each element is scaled by its row's 1/sqrt(mean(x^2) + eps) and rounded
+//    to the element type at the matrix-core input, the value a bf16 model
+//    stores as the normalised activation.
 enum Epilogue { EP_STORE = 0, EP_QKV = 1, EP_RESID = 2, EP_SWIGLU = 3 };
 
 struct GemmArgs {
     int M, N, K;             // rows of X; real output columns; real contraction length
     int n_tiles, k_steps;    // packed tile counts
     const void* W;           // packed weights
-    const void* xa;          // T [M][ldx]
+    const void* xa;          // T [M][ldx], or null when xf is given
+    const float* xf;         // float [M][ldx]: x o gain of the RMSNorm this GEMM consumes
     int ldx;
-    // RMSNorm folded into the epilogue: y[m][:] *= 1/sqrt(sum_t ssq[m][t] / K + eps)
-    // (the gain is folded into W).  ssq null: no scaling.
+    // RMSNorm row scales: 1/sqrt(sum_t ssq[m][t] / K + eps) (with xf)
     const float* ssq; int n_ssq; float eps;
     // epilogues
     float* y; int ldy;                   // EP_STORE: float [M][ldy]
     float* resid;                        // EP_RESID: float [M][ldy] (+=)
-    void* xb; int ldxb;                  // EP_RESID: T copy of the updated rows [M][ldxb]
+    float* xg_out; int ldxg;             // EP_RESID: updated rows times gnext (the next RMSNorm's gain)
+    const float* gnext;
     float* ssq_out;                      // EP_RESID: per-tile sums of squares [M][n_tiles]
-    void* qbuf; void* kc; void* vc;      // EP_QKV: Q [M][H][Dh]; layer base of K and V caches
+    void* qbuf; void* kc; void* vc;      // EP_QKV: Q float [M][H][Dh]; layer base of K and V caches
     const int* cache_len; int q, H, Dh, S_max;
     const uint64_t* mask;                // [M] ancestor masks or null (chain)
     const double* inv_freq;              // [Dh/2] rotary inverse frequencies base^(-2i/Dh)
@@ -73,7 +78,7 @@ hipError_t launch_gemm(int dtype, int ep, const GemmPlan& p, const GemmArgs& a, 
 
 // ---------------------------------------------------------------- attention
 struct AttnArgs {
-    const void* qbuf;        // T [B*q][H][Dh]
+    const float* qbuf;       // float [B*q][H][Dh]
     const void* kc;          // T K cache of one layer: [B][H][S_max][Dh]
     const void* vc;          // T V cache of one layer: [B][H][S_max/32][Dh][32] (keys permuted, vperm)
     const int* cache_len;
@@ -95,7 +100,8 @@ hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const At
 
 // ---------------------------------------------------------------- misc kernels
 hipError_t launch_embed(int dtype, const void* embed, int n_rows_emb, int d, const int* tokens, int M,
-                        float* x, void* xb, int ldxb, float* ssq, int n_ssq, int* err, hipStream_t s);
+                        float* x, float* xg, const float* gain, int ldxg, float* ssq, int n_ssq, int* err,
+                        hipStream_t s);
 hipError_t launch_to_elem_rows(int dtype, const float* src, int rows, int cols, void* dst, int ld, hipStream_t s);
 hipError_t launch_kv_write(int dtype, void* kc, void* vc, int B, int n, int H, int Dh, int S_max,
                            const float* k, const float* v, const int* pos, hipStream_t s);

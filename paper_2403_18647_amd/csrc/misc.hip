@@ -7,43 +7,66 @@
 
 namespace sdsat {
 
-// x[m] = E[token[m]] as float, its copy xb in the matrix element type (the
-// first QKV GEMM's input), plus per-16-column sums of squares (the partials
-// its RMSNorm scale reduces).  Out-of-range ids set *err and read row 0.
+// x[m] = E[token[m]] as float, x o g (g: the first RMSNorm's gain, the QKV
+// GEMM's input) and per-16-column sums of squares of x (the partials its
+// RMSNorm scale reduces).  One thread per 16-column tile, vector loads and
+// stores.  Out-of-range ids set *err and read row 0.
 template <typename T>
-__global__ void embed_kernel(const T* emb, int n_rows, int d, const int* tokens, float* x, T* xb, int ldxb,
-                             float* ssq, int n_ssq, int* err) {
-    const int m = blockIdx.x;
+__global__ void embed_kernel(const T* emb, int n_rows, int d, const int* tokens, float* x, float* xg,
+                             const float* gain, int ldxg, float* ssq, int n_ssq, int* err) {
+    const int m = blockIdx.y;
+    const int t = blockIdx.x * blockDim.x + threadIdx.x;   // 16-column tile
     int tok = tokens[m];
     if (tok < 0 || tok >= n_rows) {
-        if (threadIdx.x == 0) atomicOr(err, 1);
+        if (t == 0) atomicOr(err, 1);
         tok = 0;
     }
-    const T* src = emb + (size_t)tok * d;
-    for (int t = threadIdx.x; t < n_ssq; t += blockDim.x) {
-        float ss = 0.f;
+    if (t >= n_ssq) return;
+    const T* src = emb + (size_t)tok * d + 16 * t;
+    float v[16];
+    if ((d & 15) == 0) {
+        const Frag<T> a = Frag<T>::load(src), b = Frag<T>::load(src + 8);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) { v[j] = a.get(j); v[8 + j] = b.get(j); }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) v[j] = 16 * t + j < d ? to_f32<T>(src[j]) : 0.f;
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) ss += v[j] * v[j];
+    if ((d & 15) == 0 && (ldxg & 3) == 0 && ((uintptr_t)gain & 15) == 0) {
+        f32x4_t* xo = reinterpret_cast<f32x4_t*>(x + (size_t)m * d + 16 * t);
+        f32x4_t* go = reinterpret_cast<f32x4_t*>(xg + (size_t)m * ldxg + 16 * t);
+        const f32x4_t* gi = reinterpret_cast<const f32x4_t*>(gain + 16 * t);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const f32x4_t e = f32x4_t{v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]};
+            xo[i] = e;
+            go[i] = e * gi[i];
+        }
+    } else {
+#pragma unroll
         for (int j = 0; j < 16; ++j) {
             const int k = 16 * t + j;
             if (k < d) {
-                const T e = src[k];
-                const float v = to_f32<T>(e);
-                x[(size_t)m * d + k] = v;
-                xb[(size_t)m * ldxb + k] = e;
-                ss += v * v;
+                x[(size_t)m * d + k] = v[j];
+                xg[(size_t)m * ldxg + k] = v[j] * gain[k];
             }
         }
-        ssq[(size_t)m * n_ssq + t] = ss;
     }
+    ssq[(size_t)m * n_ssq + t] = ss;
 }
 
 hipError_t launch_embed(int dtype, const void* embed, int n_rows_emb, int d, const int* tokens, int M,
-                        float* x, void* xb, int ldxb, float* ssq, int n_ssq, int* err, hipStream_t s) {
+                        float* x, float* xg, const float* gain, int ldxg, float* ssq, int n_ssq, int* err,
+                        hipStream_t s) {
     if (dtype == 1)
-        hipLaunchKernelGGL(embed_kernel<uint16_t>, dim3(M), dim3(256), 0, s, (const uint16_t*)embed, n_rows_emb,
-                           d, tokens, x, (uint16_t*)xb, ldxb, ssq, n_ssq, err);
+        hipLaunchKernelGGL(embed_kernel<uint16_t>, dim3((n_ssq + 63) / 64, M), dim3(64), 0, s,
+                           (const uint16_t*)embed, n_rows_emb, d, tokens, x, xg, gain, ldxg, ssq, n_ssq, err);
     else
-        hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, (const float*)embed, n_rows_emb, d,
-                           tokens, x, (float*)xb, ldxb, ssq, n_ssq, err);
+        hipLaunchKernelGGL(embed_kernel<float>, dim3((n_ssq + 63) / 64, M), dim3(64), 0, s, (const float*)embed,
+                           n_rows_emb, d, tokens, x, xg, gain, ldxg, ssq, n_ssq, err);
     return hipGetLastError();
 }
 

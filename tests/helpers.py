@@ -31,3 +31,43 @@ def small_bf16(**kw):
                 gain_std=0.1)
     base.update(kw)
     return synth.Workload(**base)
+
+
+def replay(wl, tol, k=None, max_new=None, prefill_chunk=16):
+    """Replay the oracle's SDSAT block sequence on the GPU and compare logits."""
+    sh = wl.shape
+    k = wl.k if k is None else k
+    q = k + 1
+    max_new = wl.max_new if max_new is None else max_new
+    import torch
+    from oracle import decode as D
+    W = oracle_weights(wl)
+    bf16 = sh.dtype == "bf16"
+    prompt = synth.prompts(wl)[0]
+    ad = synth.adaptive_ids(sh, k)
+    tr = D.Trace()
+    D.generate_sdsat(sh, W, prompt, k, max_new, ad, bf16=bf16, trace=tr)
+    ctx = make_ctx(wl, max_batch=1, max_ctx=len(prompt) + max_new + 2 * q + 8, max_block=max(q, prefill_chunk))
+    h = ctx.handle
+    B.sdsat_reset(h, 1)
+    P = len(prompt)
+    for lo in range(0, P - 1, prefill_chunk):
+        t = torch.from_numpy(prompt[lo:min(P - 1, lo + prefill_chunk)].astype(np.int32)).cuda()
+        B.sdsat_forward_block(h, 1, len(t), t, None, None)
+        B.sdsat_commit_kv(h, 1, len(t), torch.tensor([len(t)], dtype=torch.int32, device="cuda"))
+    V = sh.vocab
+    worst = 0.0
+    for i, blk in enumerate(tr.blocks):
+        assert int(ctx.cache_len()[0]) == blk["cache_len"]
+        t = torch.from_numpy(blk["tokens"].astype(np.int32)).cuda()
+        lg = torch.empty((q, V), dtype=torch.float32, device="cuda")
+        B.sdsat_forward_block(h, 1, q, t, None, lg)
+        torch.cuda.synchronize()
+        err = float(np.abs(lg.cpu().numpy() - blk["logits"]).max())
+        worst = max(worst, err)
+        assert err <= tol, (i, err)
+        n = 1 if i % 2 == 0 else tr.loop_m[i // 2] + 1
+        B.sdsat_commit_kv(h, 1, q, torch.tensor([n], dtype=torch.int32, device="cuda"))
+    ctx.close()
+    print(f"{wl.name}: {len(tr.blocks)} blocks, max |logit diff| = {worst:.3g}")
+    return worst

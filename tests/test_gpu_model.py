@@ -27,55 +27,17 @@ def _gpu():
     B.lib()
 
 
-def _replay(wl, tol, k=None, batch_rows=None, max_new=None):
-    """Replay the oracle's SDSAT block sequence on the GPU and compare logits."""
-    sh = wl.shape
-    k = wl.k if k is None else k
-    q = k + 1
-    max_new = wl.max_new if max_new is None else max_new
-    W = helpers.oracle_weights(wl)
-    bf16 = sh.dtype == "bf16"
-    prompt = synth.prompts(wl)[0]
-    ad = synth.adaptive_ids(sh, k)
-    tr = D.Trace()
-    D.generate_sdsat(sh, W, prompt, k, max_new, ad, bf16=bf16, trace=tr)
-    ctx = helpers.make_ctx(wl, max_batch=1, max_ctx=len(prompt) + max_new + 2 * q + 8, max_block=max(q, 16))
-    h = ctx.handle
-    B.sdsat_reset(h, 1)
-    P = len(prompt)
-    for lo in range(0, P - 1, 16):
-        t = torch.from_numpy(prompt[lo:min(P - 1, lo + 16)].astype(np.int32)).cuda()
-        B.sdsat_forward_block(h, 1, len(t), t, None, None)
-        B.sdsat_commit_kv(h, 1, len(t), torch.tensor([len(t)], dtype=torch.int32, device="cuda"))
-    V = sh.vocab
-    worst = 0.0
-    for i, blk in enumerate(tr.blocks):
-        assert int(ctx.cache_len()[0]) == blk["cache_len"]
-        t = torch.from_numpy(blk["tokens"].astype(np.int32)).cuda()
-        lg = torch.empty((q, V), dtype=torch.float32, device="cuda")
-        B.sdsat_forward_block(h, 1, q, t, None, lg)
-        torch.cuda.synchronize()
-        err = float(np.abs(lg.cpu().numpy() - blk["logits"]).max())
-        worst = max(worst, err)
-        assert err <= tol, (i, err)
-        n = 1 if i % 2 == 0 else tr.loop_m[i // 2] + 1
-        B.sdsat_commit_kv(h, 1, q, torch.tensor([n], dtype=torch.int32, device="cuda"))
-    ctx.close()
-    print(f"{wl.name}: {len(tr.blocks)} blocks, max |logit diff| = {worst:.3g}")
-    return worst
-
-
 def test_teacher_forced_tiny_fp32():
-    _replay(synth.workload("tiny", max_new=40, gain_std=0.1), 1e-4)
+    helpers.replay(synth.workload("tiny", max_new=40, gain_std=0.1), 1e-4)
 
 
 def test_teacher_forced_small_bf16():
-    _replay(helpers.small_bf16(), 3e-2)
+    helpers.replay(helpers.small_bf16(), 3e-2)
 
 
 def test_teacher_forced_k0_and_k10():
-    _replay(synth.workload("tiny", max_new=12, gain_std=0.1), 1e-4, k=0)
-    _replay(helpers.small_bf16(max_new=24, shape=synth.small_shape(
+    helpers.replay(synth.workload("tiny", max_new=12, gain_std=0.1), 1e-4, k=0)
+    helpers.replay(helpers.small_bf16(max_new=24, shape=synth.small_shape(
         n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=688, vocab=1000, n_adaptive=10,
         rope_base=1e6, dtype="bf16")), 3e-2, k=10)
 
