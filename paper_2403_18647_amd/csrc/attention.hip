@@ -62,19 +62,24 @@ size_t attention_partial_floats(int B, int H, int q_max, int head_dim) {
     return (size_t)B * H * kMaxSplits * ((q_max + 15) / 16 * 16) * (head_dim + 4);
 }
 
+// K and V of one 32-key block through buffer resources over this (sequence,
+// head)'s cache rows: one 32-bit lane offset per 16-key half of K and one for
+// V, fragment offsets as wave-uniform constants (keeps the addresses out of
+// the register budget).
 template <typename T, int NDS, int NDT>
-__device__ __forceinline__ void load_kv(Frag<T> (&kf)[2][NDS], Frag<T> (&vf)[NDT], const T* kbase, const T* vbase,
-                                        int blk, int c, int g) {
+__device__ __forceinline__ void load_kv(Frag<T> (&kf)[2][NDS], Frag<T> (&vf)[NDT], __amdgpu_buffer_rsrc_t kr,
+                                        __amdgpu_buffer_rsrc_t vr, int blk, int c, int g) {
     constexpr int DH = NDS * 32;
-    const int kb0 = blk * 32;
+    constexpr uint32_t E = sizeof(T);
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < 2; ++kt) {
+        const uint32_t ko = ((uint32_t)(blk * 32 + 16 * kt + c) * DH + 8 * g) * E;
 #pragma unroll
-        for (int ds = 0; ds < NDS; ++ds)
-            kf[kt][ds] = Frag<T>::load(kbase + (size_t)(kb0 + 16 * kt + c) * DH + ds * 32 + 8 * g);
-    const T* vblk = vbase + (size_t)blk * DH * 32;
+        for (int ds = 0; ds < NDS; ++ds) kf[kt][ds] = buf_frag<T>(kr, ko, ds * 32 * E);
+    }
+    const uint32_t vo = ((uint32_t)blk * DH * 32 + c * 32 + 8 * g) * E;
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) vf[dt] = Frag<T>::load(vblk + (size_t)(dt * 16 + c) * 32 + 8 * g);
+    for (int dt = 0; dt < NDT; ++dt) vf[dt] = buf_frag<T>(vr, vo, dt * 16 * 32 * E);
 }
 
 // x as the matrix-core operand pair hi + lo (lo = the bf16 rounding remainder;
@@ -94,17 +99,14 @@ __device__ __forceinline__ void split_frag(const float (&x)[8], Frag<T>& hi, Fra
 // One 32-key block for the 16 query rows of this lane group (lane column c is
 // block row m = m0 + c).
 // Q fragments of the current row tile, in LDS: [hi / lo][ds][lane].  They are
-// read where they are used, which keeps them out of the register budget.
+// read where they are used, which keeps them out of the register budget: the
+// index passes through an empty asm statement, so the compiler cannot hoist
+// the reads out of the block loop (a volatile read would do the same but also
+// makes it wait for every outstanding global load, the next blocks' K and V).
 template <typename T>
 __device__ __forceinline__ Frag<T> lds_frag(const Frag<T>* qs, int idx) {
-    Frag<T> f;
-    if constexpr (sizeof(T) == 2) {
-        f.v = *reinterpret_cast<const volatile u32x4_t*>(&qs[idx].v);
-    } else {
-        f.lo = *reinterpret_cast<const volatile f32x4_t*>(&qs[idx].lo);
-        f.hi = *reinterpret_cast<const volatile f32x4_t*>(&qs[idx].hi);
-    }
-    return f;
+    asm volatile("" : "+v"(idx));
+    return qs[idx];
 }
 
 template <typename T, int NDS, int NDT>
@@ -164,7 +166,9 @@ __device__ __forceinline__ void attend_block(const Frag<T> (&kf)[2][NDS], const 
     }
 }
 
-template <typename T, int DH>
+// MULTI: more than 16 query rows (a loop over row tiles); decode blocks take
+// the single-tile instance, which keeps nothing live across tiles.
+template <typename T, int DH, bool MULTI>
 __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     constexpr int NDS = DH / 32;   // 32-wide steps over the head dimension
     constexpr int NDT = DH / 16;   // 16-row output tiles over the head dimension
@@ -179,8 +183,11 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     const int bh = blockIdx.x / a.splits, sp = blockIdx.x % a.splits;
     const int b = bh / a.H, h = bh % a.H;
     const int q = a.q;
-    const T* kbase = reinterpret_cast<const T*>(a.kc) + ((size_t)b * a.H + h) * a.S_max * DH;
-    const T* vbase = reinterpret_cast<const T*>(a.vc) + ((size_t)b * a.H + h) * a.S_max * DH;
+    const uint32_t slice_bytes = (uint32_t)a.S_max * DH * sizeof(T);
+    const __amdgpu_buffer_rsrc_t kr =
+        buf_rsrc(reinterpret_cast<const T*>(a.kc) + ((size_t)b * a.H + h) * a.S_max * DH, slice_bytes);
+    const __amdgpu_buffer_rsrc_t vr =
+        buf_rsrc(reinterpret_cast<const T*>(a.vc) + ((size_t)b * a.H + h) * a.S_max * DH, slice_bytes);
     const float* qb = a.qbuf;
     const bool tree = a.mask != nullptr;
 
@@ -194,33 +201,50 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     const int wlo = sp * per_wg;
     const int first = wlo + wave;
     const int last_blk = a.S_max / 32 - 1;
-    const int n_rt = (q + 15) / 16;
+    const int n_rt = MULTI ? (q + 15) / 16 : 1;
     int L = 0, whi = 0;
 
     for (int rt = 0; rt < n_rt; ++rt) {
-        // Query rows of this tile (rows past q read row q-1: their scores are
-        // masked out) and ancestor masks come first, then the wave's first two
-        // K/V blocks.  Every load ahead of the block loop is unconditional, so
-        // the compiler's wait counts stay exact.
+        // Issue order: the cache length (first tile), the ancestor mask, this
+        // wave's Q fragments, then its first two K/V blocks; Q is split and
+        // parked in LDS while the keys are in flight.  Query rows past q read
+        // row q-1 (their scores are masked out).  The loads ahead of the block
+        // loop are unconditional or wave-uniform, so the compiler's wait counts
+        // stay exact.
         const int m = 16 * rt + c;
         const int mr = min(m, q - 1);
-        const uint64_t mrow = tree ? a.mask[(size_t)b * q + mr] : 0ull;
         if (rt > 0) __syncthreads();   // every wave is done with the previous tile's Q and merge
-        for (int ds = wave; ds < NDS; ds += nw) {   // Q columns 32ds.. of the tile's rows as hi / lo
-            const f32x4_t* src = reinterpret_cast<const f32x4_t*>(qb + (((size_t)b * q + mr) * a.H + h) * DH +
-                                                                  ds * 32 + 8 * g);
-            const f32x4_t lo4 = src[0], hi4 = src[1];
-            const float x8[8] = {lo4.x, lo4.y, lo4.z, lo4.w, hi4.x, hi4.y, hi4.z, hi4.w};
+        int Lraw = 0;
+        if (rt == 0) Lraw = a.cache_len[b];
+        const uint64_t mrow = tree ? a.mask[(size_t)b * q + mr] : 0ull;
+        // wave w stages Q columns 32w.. (with fewer waves than such column
+        // groups, the rest follow the K/V requests)
+        const float* qrow = qb + (((size_t)b * q + mr) * a.H + h) * DH + 8 * g;
+        f32x4_t q0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, q1 = q0;
+        if (wave < NDS) {
+            const f32x4_t* src = reinterpret_cast<const f32x4_t*>(qrow + wave * 32);
+            q0 = src[0];
+            q1 = src[1];
+        }
+        Frag<T> kA[2][NDS], kB[2][NDS], vA[NDT], vB[NDT];
+        load_kv<T, NDS, NDT>(kA, vA, kr, vr, min(first, last_blk), c, g);
+        load_kv<T, NDS, NDT>(kB, vB, kr, vr, min(first + nw, last_blk), c, g);
+        // Q columns 32ds.. of the tile's rows as hi / lo; the first group's wait
+        // is for its own loads only (the K/V requests stay in flight)
+        auto stage_q = [&](int ds, f32x4_t v0, f32x4_t v1) {
+            const float x8[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
             Frag<T> fh, fl;
             split_frag<T>(x8, fh, fl);
             s_q[ds * 64 + lane] = fh;
             if constexpr (sizeof(T) == 2) s_q[(NDS + ds) * 64 + lane] = fl;
+        };
+        if (wave < NDS) stage_q(wave, q0, q1);
+        for (int ds = wave + nw; ds < NDS; ds += nw) {
+            const f32x4_t* src = reinterpret_cast<const f32x4_t*>(qrow + ds * 32);
+            stage_q(ds, src[0], src[1]);
         }
-        Frag<T> kA[2][NDS], kB[2][NDS], vA[NDT], vB[NDT];
-        load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, min(first, last_blk), c, g);
-        load_kv<T, NDS, NDT>(kB, vB, kbase, vbase, min(first + nw, last_blk), c, g);
         if (rt == 0) {
-            L = a.cache_len[b];
+            L = Lraw;
             if (L + q > a.S_max) {   // the host checks capacity; never read past this sequence's cache
                 if (threadIdx.x == 0) atomicOr(a.err, 4);
                 return;
@@ -242,21 +266,30 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
         // steady state (unconditional loads): blocks i and i + 1 are loaded
         for (; i + 4 <= cnt; i += 2) {
             attend_block<T, NDS, NDT>(kA, vA, s_q, lane, mrow, first + i * nw, m, L, Tb, q, tree, a.scale, g, rmax, rsum, o);
-            load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, first + (i + 2) * nw, c, g);
+            load_kv<T, NDS, NDT>(kA, vA, kr, vr, first + (i + 2) * nw, c, g);
             attend_block<T, NDS, NDT>(kB, vB, s_q, lane, mrow, first + (i + 1) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
                                       rsum, o);
-            load_kv<T, NDS, NDT>(kB, vB, kbase, vbase, first + (i + 3) * nw, c, g);
+            load_kv<T, NDS, NDT>(kB, vB, kr, vr, first + (i + 3) * nw, c, g);
         }
-        // 0 .. 3 blocks left
-        if (i < cnt)
+        // 0 .. 3 blocks left, blocks i and i + 1 loaded.  Three left is its own
+        // straight-line path, so its one load does not make the compiler wait
+        // for it before block i + 1.
+        const int rem = cnt - i;
+        if (rem == 3) {
             attend_block<T, NDS, NDT>(kA, vA, s_q, lane, mrow, first + i * nw, m, L, Tb, q, tree, a.scale, g, rmax, rsum, o);
-        if (i + 2 < cnt) load_kv<T, NDS, NDT>(kA, vA, kbase, vbase, first + (i + 2) * nw, c, g);
-        if (i + 1 < cnt)
+            load_kv<T, NDS, NDT>(kA, vA, kr, vr, first + (i + 2) * nw, c, g);
             attend_block<T, NDS, NDT>(kB, vB, s_q, lane, mrow, first + (i + 1) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
                                       rsum, o);
-        if (i + 2 < cnt)
             attend_block<T, NDS, NDT>(kA, vA, s_q, lane, mrow, first + (i + 2) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
                                       rsum, o);
+        } else {
+            if (rem >= 1)
+                attend_block<T, NDS, NDT>(kA, vA, s_q, lane, mrow, first + i * nw, m, L, Tb, q, tree, a.scale, g, rmax,
+                                          rsum, o);
+            if (rem == 2)
+                attend_block<T, NDS, NDT>(kB, vB, s_q, lane, mrow, first + (i + 1) * nw, m, L, Tb, q, tree, a.scale, g,
+                                          rmax, rsum, o);
+        }
 
         rsum += __shfl_xor(rsum, 16, 64);
         rsum += __shfl_xor(rsum, 32, 64);
@@ -266,25 +299,29 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
         }
         __syncthreads();
         // rescale this wave's partial to the common maximum and park it in LDS
+        float wmax[kMaxWaves], wsum[kMaxWaves];
+        float gmax = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kMaxWaves; ++w) {
+            wmax[w] = w < nw ? s_max[w][c] : -INFINITY;
+            wsum[w] = w < nw ? s_sum[w][c] : 0.f;
+            gmax = fmaxf(gmax, wmax[w]);
+        }
         {
-            float gmax = -INFINITY;
-            for (int w = 0; w < nw; ++w) gmax = fmaxf(gmax, s_max[w][c]);
             const float alpha = rmax == -INFINITY ? 0.f : expf(rmax - gmax);
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) opart[(wave * NDT + dt) * 64 + lane] = o[dt] * alpha;
         }
+        float den = 0.f;
+#pragma unroll
+        for (int w = 0; w < kMaxWaves; ++w) den += wmax[w] == -INFINITY ? 0.f : expf(wmax[w] - gmax) * wsum[w];
         __syncthreads();
         // sum the partials in wave order; output tiles are spread over the waves
         for (int dt = wave; dt < NDT; dt += nw) {
-            float gmax = -INFINITY;
-            for (int w = 0; w < nw; ++w) gmax = fmaxf(gmax, s_max[w][c]);
-            float den = 0.f;
             f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            for (int w = 0; w < nw; ++w) {
-                const float wm = s_max[w][c];
-                den += wm == -INFINITY ? 0.f : expf(wm - gmax) * s_sum[w][c];
-                acc += opart[(w * NDT + dt) * 64 + lane];
-            }
+#pragma unroll
+            for (int w = 0; w < kMaxWaves; ++w)
+                if (w < nw) acc += opart[(w * NDT + dt) * 64 + lane];
             if (m >= q) continue;
             const int d = 16 * dt + 4 * g;
             if (a.splits > 1) {
@@ -363,7 +400,10 @@ __global__ void __launch_bounds__(64) attn_combine_kernel(AttnArgs a, int rows) 
 
 template <typename T, int DH>
 static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, a);
+    if (a.q > 16)
+        hipLaunchKernelGGL((attn_kernel<T, DH, true>), dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, a);
+    else
+        hipLaunchKernelGGL((attn_kernel<T, DH, false>), dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.splits <= 1) return e;
     const int n = a.B * a.H * a.q * (DH / 4);

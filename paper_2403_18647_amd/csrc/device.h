@@ -36,6 +36,7 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) { return (uint16_t)f32x
 template <typename T> struct Frag;
 
 template <> struct Frag<uint16_t> {
+    using elem = uint16_t;
     u32x4_t v;
     __device__ __forceinline__ static Frag zero() { Frag f; f.v = u32x4_t{0u, 0u, 0u, 0u}; return f; }
     __device__ __forceinline__ static Frag load(const uint16_t* p) { Frag f; f.v = *reinterpret_cast<const u32x4_t*>(p); return f; }
@@ -59,6 +60,7 @@ template <> struct Frag<uint16_t> {
 };
 
 template <> struct Frag<float> {
+    using elem = float;
     f32x4_t lo, hi;
     __device__ __forceinline__ static Frag zero() {
         Frag f; f.lo = f32x4_t{0.f, 0.f, 0.f, 0.f}; f.hi = f.lo; return f;
@@ -80,6 +82,25 @@ template <> struct Frag<float> {
         Frag f; f.lo = f32x4_t{x[0], x[1], x[2], x[3]}; f.hi = f32x4_t{x[4], x[5], x[6], x[7]}; return f;
     }
 };
+
+// Buffer resource over [p, p + bytes): loads through it take a 32-bit lane
+// offset (VGPR) plus a wave-uniform one (SGPR), and lanes whose offset lies
+// past the end read zeros without touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+template <typename T>
+__device__ __forceinline__ Frag<T> buf_frag(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    Frag<T> f;
+    if constexpr (sizeof(T) == 2) {
+        f.v = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+    } else {
+        f.lo = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+        f.hi = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff + 16, soff, 0));
+    }
+    return f;
+}
 
 // acc += A(16 x 32) * B(32 x 16) with the fragment convention above.
 __device__ __forceinline__ void mma(f32x4_t& acc, const Frag<uint16_t>& a, const Frag<uint16_t>& b) {

@@ -127,15 +127,14 @@ __device__ __forceinline__ Frag<T> a_frag(const XT& x, float inv) {
 }
 
 // One batch of U contraction steps: the weight fragments of the NTW tiles
-// (streamed, non-temporal) and the X fragments of every row tile.  Rows past
-// M read row 0 (their output rows are never stored).  TAIL batches may run
-// past the wave's slice: those steps reload the last step with X zeroed.
-// Loads of the steady-state loop are unconditional so that the compiler's
-// wait counts stay exact and two batches really are in flight.
+// (streamed, non-temporal) and the X fragments of every row tile.  TAIL
+// batches may run past the wave's slice: those steps reload the last step
+// with X zeroed.  Loads of the steady-state loop are unconditional so that
+// the compiler's wait counts stay exact and two batches really are in flight.
 template <typename T, typename XT, int MT, int NTW, int U, bool TAIL>
 __device__ __forceinline__ void load_batch(Frag<T> (&w)[U][NTW], XT (&x)[U][MT], const T* const (&wp)[NTW],
-                                           const void* const (&xr)[MT], int s, int nks) {
-    using XE = typename std::conditional<sizeof(XT) == 32, float, T>::type;
+                                           __amdgpu_buffer_rsrc_t xrs, const uint32_t (&xo)[MT], int s, int nks) {
+    constexpr uint32_t step_bytes = 32 * (sizeof(XT) / 8);   // 32 elements of the X type
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int st = TAIL ? min(s + u, nks - 1) : s + u;
@@ -143,7 +142,7 @@ __device__ __forceinline__ void load_batch(Frag<T> (&w)[U][NTW], XT (&x)[U][MT],
         for (int j = 0; j < NTW; ++j) w[u][j] = Frag<T>::load_nt(wp[j] + (size_t)st * 512);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            x[u][mt] = XT::load(reinterpret_cast<const XE*>(xr[mt]) + st * 32);
+            x[u][mt] = buf_frag<typename XT::elem>(xrs, xo[mt] + (uint32_t)st * step_bytes, 0);
             if (TAIL && s + u >= nks) x[u][mt] = XT::zero();
         }
     }
@@ -339,16 +338,20 @@ __global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(Gemm
     // keeps two in flight.
     Frag<T> w0[U][NTW], w1[U][NTW];
     XT x0[U][MT], x1[U][MT];
-    const void* xr[MT];
+    // X rows [0, M) as a buffer resource; lane offsets in bytes (rows past M
+    // point past its end and read zeros without a memory access)
+    constexpr uint32_t xes = sizeof(XT) / 8;   // bytes per X element as stored
+    const uint32_t x_bytes = (uint32_t)M * (uint32_t)a.ldx * xes;
+    const __amdgpu_buffer_rsrc_t xrs = buf_rsrc(XF ? (const void*)a.xf : a.xa, x_bytes);
+    uint32_t xr[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
         const int m = 16 * mt + c;
-        const size_t off = (size_t)(m < M ? m : 0) * a.ldx + ks0 * 32 + 8 * g;
-        xr[mt] = XF ? (const void*)(a.xf + off) : (const void*)(reinterpret_cast<const T*>(a.xa) + off);
+        xr[mt] = m < M ? ((uint32_t)m * a.ldx + ks0 * 32 + 8 * g) * xes : x_bytes;
     }
     if (nks > 0) {
-        load_batch<T, XT, MT, NTW, U, true>(w0, x0, wp, xr, 0, nks);
-        load_batch<T, XT, MT, NTW, U, true>(w1, x1, wp, xr, U, nks);
+        load_batch<T, XT, MT, NTW, U, true>(w0, x0, wp, xrs, xr, 0, nks);
+        load_batch<T, XT, MT, NTW, U, true>(w1, x1, wp, xrs, xr, U, nks);
     }
 
     // row scales 1/rms, needed before the first matrix-core step (rows past
@@ -383,15 +386,15 @@ __global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(Gemm
         int s = 0;
         for (; s + 4 * U <= nks; s += 2 * U) {
             mma_batch<T, XF, XT, MT, NTW, U>(acc, w0, x0, inv);
-            load_batch<T, XT, MT, NTW, U, false>(w0, x0, wp, xr, s + 2 * U, nks);
+            load_batch<T, XT, MT, NTW, U, false>(w0, x0, wp, xrs, xr, s + 2 * U, nks);
             mma_batch<T, XF, XT, MT, NTW, U>(acc, w1, x1, inv);
-            load_batch<T, XT, MT, NTW, U, false>(w1, x1, wp, xr, s + 3 * U, nks);
+            load_batch<T, XT, MT, NTW, U, false>(w1, x1, wp, xrs, xr, s + 3 * U, nks);
         }
         // tail: steps s .. nks-1 (fewer than 4U), the first two batches loaded
         mma_batch<T, XF, XT, MT, NTW, U>(acc, w0, x0, inv);
-        if (s + 2 * U < nks) load_batch<T, XT, MT, NTW, U, true>(w0, x0, wp, xr, s + 2 * U, nks);
+        if (s + 2 * U < nks) load_batch<T, XT, MT, NTW, U, true>(w0, x0, wp, xrs, xr, s + 2 * U, nks);
         if (s + U < nks) mma_batch<T, XF, XT, MT, NTW, U>(acc, w1, x1, inv);
-        if (s + 3 * U < nks) load_batch<T, XT, MT, NTW, U, true>(w1, x1, wp, xr, s + 3 * U, nks);
+        if (s + 3 * U < nks) load_batch<T, XT, MT, NTW, U, true>(w1, x1, wp, xrs, xr, s + 3 * U, nks);
         if (s + 2 * U < nks) mma_batch<T, XF, XT, MT, NTW, U>(acc, w0, x0, inv);
         if (s + 3 * U < nks) mma_batch<T, XF, XT, MT, NTW, U>(acc, w1, x1, inv);
     }
