@@ -96,6 +96,7 @@ struct sdsat_ctx {
     void* kc = nullptr; void* vc = nullptr;
     size_t layer_elems = 0;   // elements per layer of K (and of V)
     double* inv_freq = nullptr;   // rotary inverse frequencies [Dh/2]
+    float* rope = nullptr;        // rotary cos / sin per cache slot [S][Dh/2][2]
     // activations
     float* x = nullptr; float* ssq = nullptr;
     float* xg = nullptr;  // x o (next RMSNorm gain), float, row stride d_pad (zero pad)
@@ -149,6 +150,7 @@ void carve(sdsat_ctx* c, Carver& cv) {
     c->kc = cv.take(c->layer_elems * D.L * e);
     c->vc = cv.take(c->layer_elems * D.L * e);
     c->inv_freq = (double*)cv.take((size_t)(D.Dh / 2) * 8);
+    c->rope = (float*)cv.take((size_t)D.S * (D.Dh / 2) * 8);
     c->x = (float*)cv.take((size_t)D.maxM * D.d * 4);
     c->ssq = (float*)cv.take((size_t)D.maxM * D.n_ssq * 4);
     c->xg = (float*)cv.take((size_t)D.maxM * D.d_pad * 4);
@@ -242,10 +244,10 @@ int fits(sdsat_ctx* c, int B, int q, bool* ok) {
 int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask, const float* qbuf, void* out,
                     int out_f32, int ldo) {
     const Dims& D = c->D;
-    const AttnPlan p = plan_attention(B, D.H, q, D.Dh, max_hint(c, B));
+    const AttnPlan p = plan_attention(B, D.H, q, D.Dh, max_hint(c, B), D.S);
     AttnArgs a{};
     a.qbuf = qbuf; a.kc = layer_k(c, layer); a.vc = layer_v(c, layer);
-    a.cache_len = c->cache_len; a.len_bound = max_hint(c, B); a.mask = mask;
+    a.cache_len = c->cache_len; a.per_split = p.per_split; a.mask = mask;
     a.B = B; a.q = q; a.H = D.H; a.S_max = D.S;
     a.scale = (float)(1.0 / std::sqrt((double)D.Dh));
     a.splits = p.splits; a.part = c->attn_part;
@@ -271,7 +273,7 @@ int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const 
         a.xf = c->xg; a.ldx = D.d_pad; a.ssq = c->ssq; a.n_ssq = D.n_ssq; a.eps = c->cfg.rms_eps;
         a.qbuf = c->qbuf; a.kc = layer_k(c, l); a.vc = layer_v(c, l);
         a.cache_len = c->cache_len; a.q = q; a.H = D.H; a.Dh = D.Dh; a.S_max = D.S; a.mask = mask;
-        a.inv_freq = c->inv_freq;
+        a.rope = c->rope;
         int rc = run_gemm(c, PK_QKV, EP_QKV, M, D.nt_qkv, D.ks_d, 3 * D.d, D.d, c->w_qkv[l], a);
         if (rc) return rc;
         rc = attention_layer(c, l, B, q, mask, (const float*)c->qbuf, c->obuf, 0, D.d_pad);
@@ -401,14 +403,18 @@ int sdsat_init(const sdsat_config* cfg, const void* const* weights, int32_t n_we
     }
     auto init_fail = [&](int code) { std::string m = c->err; delete c; return fail(nullptr, code, m); };
     if (hipGetLastError() != hipSuccess) { c->err = "weight packing launch failed"; return init_fail(SDSAT_EDEVICE); }
-    // rotary inverse frequencies base^(-2i/Dh), in double (the QKV epilogue forms
-    // the angle pos * inv_freq in double and rounds cos / sin to float)
+    // rotary inverse frequencies base^(-2i/Dh) in double, and the table of cos / sin
+    // of pos * inv_freq (formed in double, rounded to float) the QKV epilogue reads
     {
         const int half = D.Dh / 2;
         std::vector<double> inv(half);
         for (int i = 0; i < half; ++i) inv[i] = std::pow((double)cfg->rope_base, -2.0 * i / D.Dh);
         if (hipMemcpyAsync(c->inv_freq, inv.data(), inv.size() * 8, hipMemcpyHostToDevice, c->stream) != hipSuccess) {
             c->err = "rotary table upload failed";
+            return init_fail(SDSAT_EDEVICE);
+        }
+        if (launch_rope_table(c->inv_freq, D.S, half, c->rope, c->stream) != hipSuccess) {
+            c->err = "rotary table launch failed";
             return init_fail(SDSAT_EDEVICE);
         }
         if (hipStreamSynchronize(c->stream) != hipSuccess) {   // the host vector goes out of scope

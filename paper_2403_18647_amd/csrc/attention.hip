@@ -33,27 +33,34 @@ namespace sdsat {
 static constexpr int kMaxWaves = 8;
 static constexpr int kMaxSplits = 8;
 
-// Decode blocks (q <= 16): key splits only pay when the (b, h) pairs leave most
-// compute units idle and each pair has many key blocks; below that the combine
-// kernel costs more than the parallelism gains (measured on MI355X).  Longer
-// blocks (prefill chunks) do q/16 passes over the keys per workgroup and take
-// splits of at least two blocks.  Waves per workgroup: one per 32-key block of
-// the split, at most 8 (LDS holds waves x Dh/16 tiles of 1 KiB).
-AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len) {
+// Decode blocks (q <= 16) partition the keys by absolute 32-key block index
+// only: split sp owns blocks [sp * P, (sp + 1) * P) with P fixed by the cache
+// capacity (enough splits at full capacity to give the GPU about 256
+// workgroups), and within a split block i goes to wave i mod waves.  A query
+// row therefore sees the same keys in the same order of accumulation whatever
+// the block size q and the cache length: blocks it cannot see (later rows of
+// its own block) add exact zeros.  So a token's logits do not depend on how
+// many draft rows share its block, and greedy SDSAT reproduces autoregressive
+// decoding bit for bit.  Longer blocks (prefill chunks) do q/16 passes over
+// the keys per workgroup and take splits of at least two blocks.  Waves per
+// workgroup: one per block of the split, at most 8.
+AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_max) {
     AttnPlan p;
-    const int nblk = (max_len + q + 31) / 32;
+    const int cap = std::max(1, S_max / 32);
+    const int nblk = std::max(1, std::min(cap, (max_len + q + 31) / 32));
     const int pairs = B * H;
-    int splits = 1;
-    if (pairs < 256) {
-        const int want = (256 + pairs - 1) / pairs;
-        if (q > 16) splits = std::min(want, nblk / 2);
-        else if (nblk >= 48) splits = std::min(want, nblk / 16);
-        splits = std::max(1, std::min(splits, kMaxSplits));
+    if (q <= 16) {
+        const int target = std::max(1, std::min(kMaxSplits, (256 + pairs - 1) / pairs));
+        p.per_split = (cap + target - 1) / target;
+        p.splits = (nblk + p.per_split - 1) / p.per_split;
+    } else {
+        int splits = 1;
+        if (pairs < 256) splits = std::max(1, std::min(std::min((256 + pairs - 1) / pairs, nblk / 2), kMaxSplits));
+        p.per_split = (nblk + splits - 1) / splits;
+        p.splits = (nblk + p.per_split - 1) / p.per_split;
     }
-    const int per_split = (nblk + splits - 1) / splits;
-    p.waves = std::max(1, std::min(per_split, kMaxWaves));
-    p.splits = splits;
-    p.grid = pairs * splits;
+    p.waves = std::max(1, std::min(p.per_split, kMaxWaves));
+    p.grid = pairs * p.splits;
     p.lds_bytes = p.waves * (head_dim / 16) * 64 * 16;
     return p;
 }
@@ -172,14 +179,17 @@ template <typename T, int DH, bool MULTI>
 __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     constexpr int NDS = DH / 32;   // 32-wide steps over the head dimension
     constexpr int NDT = DH / 16;   // 16-row output tiles over the head dimension
+    // Per wave DH * 64 bytes of LDS: its Q fragments of the row tile
+    // ([hi / lo][ds][lane], read back in every block), then its partial O
+    // ([dt][lane]) for the merge.
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    f32x4_t* opart = reinterpret_cast<f32x4_t*>(smem_raw);   // [waves][NDT][64]
     __shared__ float s_max[kMaxWaves][16], s_sum[kMaxWaves][16];
-    __shared__ Frag<T> s_q[2 * NDS * 64];                      // Q of the row tile: [hi / lo][ds][lane]
 
     const int nw = blockDim.x >> 6;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63, c = lane & 15, g = lane >> 4;
+    Frag<T>* s_q = reinterpret_cast<Frag<T>*>(smem_raw + (size_t)wave * DH * 64);
+    const f32x4_t* opart = reinterpret_cast<const f32x4_t*>(smem_raw);   // [waves][NDT][64]
     const int bh = blockIdx.x / a.splits, sp = blockIdx.x % a.splits;
     const int b = bh / a.H, h = bh % a.H;
     const int q = a.q;
@@ -191,69 +201,64 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     const float* qb = a.qbuf;
     const bool tree = a.mask != nullptr;
 
-    // Split sp owns blocks [wlo, wlo + per_wg) of the partition the host's
-    // length bound gives (the last split runs on to the true end, so a stale
-    // bound costs time, never keys).  The wave's blocks are first + i * nw;
-    // the first two are requested before the true length is known (indices
-    // clamped into the cache; a block past the length is loaded, not used).
-    const int nb_bound = min((a.len_bound + q + 31) / 32, a.S_max / 32);
-    const int per_wg = max(1, (nb_bound + a.splits - 1) / a.splits);
-    const int wlo = sp * per_wg;
+    // Split sp owns blocks [wlo, wlo + per_split) (the last split runs on to
+    // the true end, so a stale host bound costs time, never keys).  The
+    // wave's blocks are first + i * nw; the first two are requested before the
+    // true length is known (indices clamped into the cache; a block past the
+    // length is loaded, not used).
+    const int wlo = sp * a.per_split;
     const int first = wlo + wave;
     const int last_blk = a.S_max / 32 - 1;
     const int n_rt = MULTI ? (q + 15) / 16 : 1;
+    // The cache length is the first request, as a vector load (a scalar one
+    // would be scheduled after the K/V requests, and the first block waits
+    // for it).
+    int bv = b;
+    asm volatile("" : "+v"(bv));
+    const int Lv = a.cache_len[bv];
     int L = 0, whi = 0;
 
     for (int rt = 0; rt < n_rt; ++rt) {
-        // Issue order: the cache length (first tile), the ancestor mask, this
-        // wave's Q fragments, then its first two K/V blocks; Q is split and
-        // parked in LDS while the keys are in flight.  Query rows past q read
-        // row q-1 (their scores are masked out).  The loads ahead of the block
-        // loop are unconditional or wave-uniform, so the compiler's wait counts
-        // stay exact.
+        // Issue order: the ancestor mask, the wave's Q fragments, its first two
+        // K/V blocks; Q is split and parked in the wave's LDS while the keys
+        // are in flight (no barrier: each wave reads only its own copy).
+        // Query rows past q read row q-1 (their scores are masked out).  The
+        // loads ahead of the block loop are unconditional or wave-uniform, so
+        // the compiler's wait counts stay exact.
         const int m = 16 * rt + c;
         const int mr = min(m, q - 1);
-        if (rt > 0) __syncthreads();   // every wave is done with the previous tile's Q and merge
-        int Lraw = 0;
-        if (rt == 0) Lraw = a.cache_len[b];
+        if (MULTI && rt > 0) __syncthreads();   // every wave is done reading the previous tile's partials
         const uint64_t mrow = tree ? a.mask[(size_t)b * q + mr] : 0ull;
-        // wave w stages Q columns 32w.. (with fewer waves than such column
-        // groups, the rest follow the K/V requests)
-        const float* qrow = qb + (((size_t)b * q + mr) * a.H + h) * DH + 8 * g;
-        f32x4_t q0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, q1 = q0;
-        if (wave < NDS) {
-            const f32x4_t* src = reinterpret_cast<const f32x4_t*>(qrow + wave * 32);
-            q0 = src[0];
-            q1 = src[1];
+        const f32x4_t* qsrc = reinterpret_cast<const f32x4_t*>(qb + (((size_t)b * q + mr) * a.H + h) * DH + 8 * g);
+        f32x4_t qv[NDS][2];
+#pragma unroll
+        for (int ds = 0; ds < NDS; ++ds) {
+            qv[ds][0] = qsrc[ds * 8];
+            qv[ds][1] = qsrc[ds * 8 + 1];
         }
         Frag<T> kA[2][NDS], kB[2][NDS], vA[NDT], vB[NDT];
         load_kv<T, NDS, NDT>(kA, vA, kr, vr, min(first, last_blk), c, g);
         load_kv<T, NDS, NDT>(kB, vB, kr, vr, min(first + nw, last_blk), c, g);
-        // Q columns 32ds.. of the tile's rows as hi / lo; the first group's wait
-        // is for its own loads only (the K/V requests stay in flight)
-        auto stage_q = [&](int ds, f32x4_t v0, f32x4_t v1) {
-            const float x8[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+        __builtin_amdgcn_sched_barrier(0);   // keep the K/V requests ahead of the wait for Q
+#pragma unroll
+        for (int ds = 0; ds < NDS; ++ds) {   // Q columns 32ds.. of the tile's rows as hi / lo
+            const float x8[8] = {qv[ds][0].x, qv[ds][0].y, qv[ds][0].z, qv[ds][0].w,
+                                 qv[ds][1].x, qv[ds][1].y, qv[ds][1].z, qv[ds][1].w};
             Frag<T> fh, fl;
             split_frag<T>(x8, fh, fl);
             s_q[ds * 64 + lane] = fh;
             if constexpr (sizeof(T) == 2) s_q[(NDS + ds) * 64 + lane] = fl;
-        };
-        if (wave < NDS) stage_q(wave, q0, q1);
-        for (int ds = wave + nw; ds < NDS; ds += nw) {
-            const f32x4_t* src = reinterpret_cast<const f32x4_t*>(qrow + ds * 32);
-            stage_q(ds, src[0], src[1]);
         }
         if (rt == 0) {
-            L = Lraw;
+            L = __builtin_amdgcn_readfirstlane(Lv);
             if (L + q > a.S_max) {   // the host checks capacity; never read past this sequence's cache
                 if (threadIdx.x == 0) atomicOr(a.err, 4);
                 return;
             }
             const int nblk = (L + q + 31) / 32;
-            whi = sp == a.splits - 1 ? nblk : min(nblk, wlo + per_wg);
+            whi = sp == a.splits - 1 ? nblk : min(nblk, wlo + a.per_split);
         }
         const int Tb = L + q;
-        __syncthreads();   // the tile's Q fragments are in LDS
 
         float rmax = -INFINITY, rsum = 0.f;
         f32x4_t o[NDT];
@@ -293,35 +298,38 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
 
         rsum += __shfl_xor(rsum, 16, 64);
         rsum += __shfl_xor(rsum, 32, 64);
+        // the wave's partial (to its own maximum) goes to its LDS region, in
+        // place of its Q
+        {
+            f32x4_t* own = reinterpret_cast<f32x4_t*>(s_q);
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) own[dt * 64 + lane] = o[dt];
+        }
         if (g == 0) {
             s_max[wave][c] = rmax;
             s_sum[wave][c] = rsum;
         }
         __syncthreads();
-        // rescale this wave's partial to the common maximum and park it in LDS
-        float wmax[kMaxWaves], wsum[kMaxWaves];
+        // log-sum-exp merge of the waves' partials in wave order; output tiles
+        // are spread over the waves
+        float alpha[kMaxWaves];
         float gmax = -INFINITY;
 #pragma unroll
         for (int w = 0; w < kMaxWaves; ++w) {
-            wmax[w] = w < nw ? s_max[w][c] : -INFINITY;
-            wsum[w] = w < nw ? s_sum[w][c] : 0.f;
-            gmax = fmaxf(gmax, wmax[w]);
-        }
-        {
-            const float alpha = rmax == -INFINITY ? 0.f : expf(rmax - gmax);
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) opart[(wave * NDT + dt) * 64 + lane] = o[dt] * alpha;
+            alpha[w] = w < nw ? s_max[w][c] : -INFINITY;
+            gmax = fmaxf(gmax, alpha[w]);
         }
         float den = 0.f;
 #pragma unroll
-        for (int w = 0; w < kMaxWaves; ++w) den += wmax[w] == -INFINITY ? 0.f : expf(wmax[w] - gmax) * wsum[w];
-        __syncthreads();
-        // sum the partials in wave order; output tiles are spread over the waves
+        for (int w = 0; w < kMaxWaves; ++w) {
+            alpha[w] = alpha[w] == -INFINITY ? 0.f : expf(alpha[w] - gmax);
+            if (w < nw) den += alpha[w] * s_sum[w][c];
+        }
         for (int dt = wave; dt < NDT; dt += nw) {
             f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int w = 0; w < kMaxWaves; ++w)
-                if (w < nw) acc += opart[(w * NDT + dt) * 64 + lane];
+                if (w < nw) acc += opart[(w * NDT + dt) * 64 + lane] * alpha[w];
             if (m >= q) continue;
             const int d = 16 * dt + 4 * g;
             if (a.splits > 1) {
@@ -337,6 +345,9 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
                 float* po = reinterpret_cast<float*>(a.out) + row + d;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) po[r] = acc[r] * inv;
+            } else if constexpr (sizeof(T) == 2) {   // 4 bf16 in one 8-byte store
+                const uint2 pk = {f32x2_to_bf16x2(acc[0] * inv, acc[1] * inv), f32x2_to_bf16x2(acc[2] * inv, acc[3] * inv)};
+                *reinterpret_cast<uint2*>(reinterpret_cast<T*>(a.out) + row + d) = pk;
             } else {
                 T* po = reinterpret_cast<T*>(a.out) + row + d;
 #pragma unroll
@@ -413,7 +424,8 @@ static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s)
 
 hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s) {
     if (a.q < 1 || a.q > 64 || p.waves < 1 || p.waves > kMaxWaves || a.splits < 1 || a.splits > kMaxSplits ||
-        a.splits != p.splits || (a.splits > 1 && !a.part) || p.grid != a.B * a.H * a.splits)
+        a.splits != p.splits || (a.splits > 1 && !a.part) || p.grid != a.B * a.H * a.splits || a.ldo % 4 != 0 ||
+        a.per_split != p.per_split || a.per_split < 1)
         return hipErrorInvalidValue;
     if (dtype == 1) {
         if (head_dim == 128) return launch_dh<uint16_t, 128>(p, a, s);

@@ -165,7 +165,7 @@ __device__ __forceinline__ void mma_batch(f32x4_t (&acc)[NTW][MT], const Frag<T>
 // acc[mt][r] = Y[m = 16mt + 4g + r][column c of the tile]
 template <typename T, int EP, int MT>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, int tile, const f32x4_t (&acc)[MT],
-                                         const float (&ep_in)[MT][4], double inv_freq, int c, int g) {
+                                         const float (&ep_in)[MT][4], int c, int g) {
     const int M = a.M;
     if (EP == EP_STORE) {
         const int n = tile * 16 + c;
@@ -237,13 +237,12 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int tile, const f32x
                 float out = mine;
                 if (sec < 2) {
                     // rotary position: the row's depth in the block (its ancestors
-                    // counted by the tree mask; row index for a chain).  The angle
-                    // pos * base^(-2i/Dh) is formed in double and cos / sin are
-                    // rounded to float, as a float table built in double would hold.
+                    // counted by the tree mask; row index for a chain), at most pos.
+                    // cos / sin come from the table (angle formed in double, rounded
+                    // to float).
                     const int rpos = a.mask ? L + __popcll(a.mask[m]) - 1 : pos;
-                    double sd, cd;
-                    sincos((double)rpos * inv_freq, &sd, &cd);
-                    const float cs = (float)cd, sn = (float)sd;
+                    const float2 csn = *reinterpret_cast<const float2*>(a.rope + ((size_t)rpos * half + pi) * 2);
+                    const float cs = csn.x, sn = csn.y;
                     out = c < 8 ? mine * cs - other * sn : other * sn + mine * cs;
                 }
                 if (sec == 0) {
@@ -296,25 +295,20 @@ __global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(Gemm
             sq[j][t] = (XF && m < M && col < a.n_ssq) ? a.ssq[(size_t)m * a.n_ssq + col] : 0.f;
         }
     // EP_RESID: residual values per tile; EP_QKV: cache_len of each row's
-    // sequence (the same for every tile) and the rotary inverse frequency of
-    // this lane's column pair per tile
+    // sequence (the same for every tile)
     constexpr int NEP = EP == EP_RESID ? NTW : 1;
     float ep_in[NEP][MT][4];
-    double inv_freq[NTW];
 #pragma unroll
     for (int j = 0; j < NEP; ++j)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int r = 0; r < 4; ++r) ep_in[j][mt][r] = 0.f;
-#pragma unroll
-    for (int j = 0; j < NTW; ++j) inv_freq[j] = 0.0;
     if (wave == 0) {
 #pragma unroll
         for (int j = 0; j < NTW; ++j) {
             const int tile = tile0 + j;
             if (tile >= a.n_tiles) break;
-            if (EP == EP_QKV) inv_freq[j] = a.inv_freq[8 * (tile % (a.Dh / 16)) + (c & 7)];
             if (EP != EP_RESID && j > 0) continue;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
@@ -391,6 +385,8 @@ __global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(Gemm
             load_batch<T, XT, MT, NTW, U, false>(w1, x1, wp, xrs, xr, s + 3 * U, nks);
         }
         // tail: steps s .. nks-1 (fewer than 4U), the first two batches loaded
+        // (unconditional refills here, or one straight-line path per remaining
+        // count, measured slower on MI355X)
         mma_batch<T, XF, XT, MT, NTW, U>(acc, w0, x0, inv);
         if (s + 2 * U < nks) load_batch<T, XT, MT, NTW, U, true>(w0, x0, wp, xrs, xr, s + 2 * U, nks);
         if (s + U < nks) mma_batch<T, XF, XT, MT, NTW, U>(acc, w1, x1, inv);
@@ -416,7 +412,7 @@ __global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(Gemm
             for (int w = 1; w < nw; ++w) v += red[(w * MT + mt) * 64 + lane];
             t_acc[mt] = v;
         }
-        epilogue<T, EP, MT>(a, tile0 + j, t_acc, ep_in[j < NEP ? j : 0], inv_freq[j], c, g);
+        epilogue<T, EP, MT>(a, tile0 + j, t_acc, ep_in[j < NEP ? j : 0], c, g);
     }
 }
 

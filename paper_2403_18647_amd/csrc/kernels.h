@@ -65,7 +65,7 @@ struct GemmArgs {
     void* qbuf; void* kc; void* vc;      // EP_QKV: Q float [M][H][Dh]; layer base of K and V caches
     const int* cache_len; int q, H, Dh, S_max;
     const uint64_t* mask;                // [M] ancestor masks or null (chain)
-    const double* inv_freq;              // [Dh/2] rotary inverse frequencies base^(-2i/Dh)
+    const float* rope;                   // [S_max][Dh/2][2] rotary cos, sin of position x base^(-2i/Dh)
     void* uout; int F; int ldu;          // EP_SWIGLU: T [M][ldu]
     int* err;                            // device error flags (bit 4: write past the cache)
 };
@@ -82,7 +82,7 @@ struct AttnArgs {
     const void* kc;          // T K cache of one layer: [B][H][S_max][Dh]
     const void* vc;          // T V cache of one layer: [B][H][S_max/32][Dh][32] (keys permuted, vperm)
     const int* cache_len;
-    int len_bound;           // host's upper bound of cache_len[b] (sets the key partition and the early loads)
+    int per_split;           // 32-key blocks per split (split sp owns blocks [sp * per_split, ...))
     const uint64_t* mask;    // [B*q] or null
     int B, q, H, S_max;
     float scale;
@@ -92,9 +92,10 @@ struct AttnArgs {
     int out_f32, ldo;
     int* err;                // device error flags (bit 4: read past the cache)
 };
-// `splits` workgroups of `waves` waves per (sequence, head)
-struct AttnPlan { int waves, splits, grid, lds_bytes; };
-AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len);
+// `splits` workgroups of `waves` waves per (sequence, head); max_len: the host's
+// upper bound of the cache lengths; S_max: key slots per sequence
+struct AttnPlan { int waves, splits, per_split, grid, lds_bytes; };
+AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_max);
 size_t attention_partial_floats(int B, int H, int q_max, int head_dim);
 hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s);
 
@@ -112,6 +113,8 @@ hipError_t launch_commit_gather(int dtype, void* kc, void* vc, size_t layer_stri
                                 const int* rows, int q, int* err, hipStream_t s);
 hipError_t launch_set_len(int* cache_len, int B, const int* vals_or_null, int value, hipStream_t s);
 hipError_t launch_fill_i32(int* p, size_t n, int value, hipStream_t s);
+// rotary table [S][half][2]: cos and sin of the angle pos * inv_freq[i], formed in double, rounded to float
+hipError_t launch_rope_table(const double* inv_freq, int S, int half, float* rope, hipStream_t s);
 
 // ---------------------------------------------------------------- verify
 hipError_t launch_verify_greedy(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,

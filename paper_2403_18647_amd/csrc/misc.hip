@@ -224,6 +224,23 @@ hipError_t launch_fill_i32(int* p, size_t n, int value, hipStream_t s) {
     return hipGetLastError();
 }
 
+__global__ void rope_table_kernel(const double* inv_freq, int S, int half, float* rope) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (size_t)S * half) return;
+    const int pos = (int)(i / half), p = (int)(i % half);
+    double sd, cd;
+    sincos((double)pos * inv_freq[p], &sd, &cd);
+    rope[2 * i] = (float)cd;
+    rope[2 * i + 1] = (float)sd;
+}
+
+hipError_t launch_rope_table(const double* inv_freq, int S, int half, float* rope, hipStream_t s) {
+    const size_t n = (size_t)S * half;
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, inv_freq, S, half, rope);
+    return hipGetLastError();
+}
+
 // draft step 1 block: [pending_b, a_1..a_k]
 __global__ void build_draft1_kernel(const int* pending, const int* adaptive, int B, int k, int* tokens) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;

@@ -60,6 +60,43 @@ def _first_mismatch_ok(sh, W, prompt, got, ref, bf16, mode="greedy"):
     return len(ref)
 
 
+@pytest.mark.parametrize("dtype,k,prompt_len", [("bf16", 5, 318), ("bf16", 10, 254), ("fp32", 5, 189),
+                                                 ("bf16", 5, 40), ("bf16", 10, 1625)])
+def test_block_rows_bitwise_equal_single_token_steps(dtype, k, prompt_len):
+    """A token's logits do not depend on how many draft rows share its block (Section 2.1,
+    Eq. 1-3 compare a block's predictions with autoregressive ones): row r of a (k+1)-row
+    block equals, bit for bit, the logits of the same token fed alone at the same position
+    after rows 0..r-1 were committed one at a time.  The block spans a 32-key block and a
+    key-split boundary, with several key splits per head.  At the 1625-token prompt a key
+    partition sized from the current length plus the block size (51 vs 52 key blocks in 3
+    splits) would give the block and the single-token steps different split boundaries."""
+    if dtype == "bf16":
+        shape = synth.small_shape(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=688, vocab=1000,
+                                  n_adaptive=10, rope_base=1e6, dtype="bf16")
+    else:
+        shape = synth.small_shape(n_adaptive=10)   # the tiny fp32 decoder: 4 heads of 64
+    wl = synth.Workload("inv", shape, seed=11, batch=1, k=k, prompt_len=prompt_len, max_new=1, gain_std=0.1)
+    q = k + 1
+    ctx = helpers.make_ctx(wl, max_batch=1, max_ctx=prompt_len + 2 * q + 40, max_block=64)
+    prompt = synth.prompts(wl)[0]
+    dev = "cuda"
+    for lo in range(0, len(prompt), 16):
+        t = torch.tensor(prompt[lo:lo + 16], dtype=torch.int32, device=dev)
+        B.sdsat_forward_block(ctx.handle, 1, len(t), t, None, None)
+        B.sdsat_commit_kv(ctx.handle, 1, len(t), torch.tensor([len(t)], dtype=torch.int32, device=dev))
+    toks = np.random.default_rng(3).integers(0, shape.vocab, q).astype(np.int32)
+    blk = torch.empty((q, shape.vocab), dtype=torch.float32, device=dev)
+    B.sdsat_forward_block(ctx.handle, 1, q, torch.from_numpy(toks).to(dev), None, blk)
+    one = torch.empty((1, shape.vocab), dtype=torch.float32, device=dev)
+    for r in range(q):
+        B.sdsat_forward_block(ctx.handle, 1, 1, torch.from_numpy(toks[r:r + 1]).to(dev), None, one)
+        B.sdsat_commit_kv(ctx.handle, 1, 1, torch.tensor([1], dtype=torch.int32, device=dev))
+        torch.cuda.synchronize()
+        diff = (one[0] - blk[r]).abs().max().item()
+        assert torch.equal(one[0], blk[r]), (r, diff)
+    ctx.close()
+
+
 def test_generate_tiny_greedy_matches_ar():
     wl = synth.workload("tiny")
     sh = wl.shape
