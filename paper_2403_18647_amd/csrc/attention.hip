@@ -35,7 +35,7 @@ static constexpr int kMaxSplits = 8;
 
 // Decode blocks (q <= 16) partition the keys by absolute 32-key block index
 // only: split sp owns blocks [sp * P, (sp + 1) * P) with P fixed by the cache
-// capacity (enough splits at full capacity to give the GPU about 256
+// capacity (at full capacity, as many splits as fit one round of 256
 // workgroups), and within a split block i goes to wave i mod waves.  A query
 // row therefore sees the same keys in the same order of accumulation whatever
 // the block size q and the cache length: blocks it cannot see (later rows of
@@ -50,7 +50,8 @@ AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_ma
     const int nblk = std::max(1, std::min(cap, (max_len + q + 31) / 32));
     const int pairs = B * H;
     if (q <= 16) {
-        const int target = std::max(1, std::min(kMaxSplits, (256 + pairs - 1) / pairs));
+        // one round of workgroups (a workgroup of 8 waves holds a compute unit's registers)
+        const int target = std::max(1, std::min(kMaxSplits, 256 / pairs));
         p.per_split = (cap + target - 1) / target;
         p.splits = (nblk + p.per_split - 1) / p.per_split;
     } else {
