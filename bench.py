@@ -43,10 +43,11 @@ def block_bytes(sh, B, q, ctx_len):
 
 
 def gateup_bytes(sh, M):
-    """Algorithmic bytes of one gate/up launch: the [2F, d] bf16 weight tiles (RMSNorm gain folded in),
-    the M bf16 residual rows, their per-16-column sums of squares, and the bf16 SwiGLU output."""
+    """Algorithmic bytes of one gate/up launch: the [2F, d] bf16 weight tiles, the M float rows x o g of
+    its RMSNorm input (gain applied by the producing epilogue), their per-16-column sums of squares,
+    and the bf16 SwiGLU output."""
     d, F = sh.d_model, sh.d_ffn
-    return 2 * F * d * 2 + M * d * 2 + M * (d // 16) * 4 + M * F * 2
+    return 2 * F * d * 2 + M * d * 4 + M * (d // 16) * 4 + M * F * 2
 
 
 def profiled_traffic():

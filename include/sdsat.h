@@ -205,8 +205,11 @@ int sdsat_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const float* d_
  * 1 gate/up GEMM, 2 QKV GEMM, 3 attention, 4 down GEMM, 5 O GEMM, 6 LM head,
  * 7 whole block forward with logits (draft / verify blocks), 8 whole block
  * forward without logits (prefill).  period >= 1: one launch of that kind in
- * every `period` is bracketed by a pair of events (each pair costs a few
- * microseconds of queue time, so a period > 1 keeps timed runs undisturbed).
+ * every `period` is timed.  Kinds 1-6 take their events from the kernel's own
+ * dispatch (start and end of the kernel, or of the attention kernel and its
+ * split combine), the interval a kernel trace reports; kinds 7 and 8 record a
+ * pair of events around the block (each pair costs a few microseconds of
+ * queue time, so a period > 1 keeps timed runs undisturbed).
  * sdsat_kernel_time synchronizes the stream and returns the summed
  * milliseconds and the number of timed launches since the last call. */
 int sdsat_profile_kernel(sdsat_ctx* ctx, int32_t kind, int32_t period);

@@ -179,7 +179,9 @@ void* layer_k(sdsat_ctx* c, int l) { return (char*)c->kc + (size_t)l * c->layer_
 void* layer_v(sdsat_ctx* c, int l) { return (char*)c->vc + (size_t)l * c->layer_elems * c->D.esz; }
 
 // ---------------------------------------------------------------- profiling
-void prof_begin(sdsat_ctx* c, int kind, hipEvent_t* out) {
+// Takes the next event pair of the pool for a sampled launch of `kind` (null
+// when this launch is not sampled).
+void prof_take(sdsat_ctx* c, int kind, hipEvent_t* out) {
     *out = nullptr;
     if (c->prof_kind != kind) return;
     if (c->prof_seen++ % c->prof_period != 0) return;
@@ -193,7 +195,22 @@ void prof_begin(sdsat_ctx* c, int kind, hipEvent_t* out) {
     }
     *out = c->events[c->ev_used];
     c->ev_used += 2;
-    (void)hipEventRecord(*out, c->stream);
+}
+
+void prof_begin(sdsat_ctx* c, int kind, hipEvent_t* out) {
+    prof_take(c, kind, out);
+    if (*out) (void)hipEventRecord(*out, c->stream);
+}
+
+// Event pair for one launch of a profiled kind, taken at the kernel's own start
+// and end (hipExtLaunchKernel) rather than recorded around it.
+void prof_pair(sdsat_ctx* c, int kind, hipEvent_t* e0, hipEvent_t* e1) {
+    *e0 = *e1 = nullptr;
+    hipEvent_t s;
+    prof_take(c, kind, &s);
+    if (!s) return;
+    *e0 = s;
+    *e1 = c->events[c->ev_used - 1];
 }
 
 void prof_end(sdsat_ctx* c, hipEvent_t start) {
@@ -208,10 +225,9 @@ int run_gemm(sdsat_ctx* c, int kind, int ep, int M, int n_tiles, int k_steps, in
              GemmArgs a) {
     const GemmPlan p = plan_gemm(M, n_tiles, k_steps);
     a.M = M; a.N = N; a.K = K; a.n_tiles = n_tiles; a.k_steps = k_steps; a.W = W; a.err = c->err_flag;
-    hipEvent_t ev;
-    prof_begin(c, kind, &ev);
-    HIPCHK(c, launch_gemm(c->D.dtype, ep, p, a, c->stream));
-    prof_end(c, ev);
+    hipEvent_t e0, e1;
+    prof_pair(c, kind, &e0, &e1);
+    HIPCHK(c, launch_gemm(c->D.dtype, ep, p, a, c->stream, e0, e1));
     return SDSAT_OK;
 }
 
@@ -252,10 +268,9 @@ int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask,
     a.scale = (float)(1.0 / std::sqrt((double)D.Dh));
     a.splits = p.splits; a.part = c->attn_part;
     a.out = out; a.out_f32 = out_f32; a.ldo = ldo; a.err = c->err_flag;
-    hipEvent_t ev;
-    prof_begin(c, PK_ATTN, &ev);
-    HIPCHK(c, launch_attention(D.dtype, D.Dh, p, a, c->stream));
-    prof_end(c, ev);
+    hipEvent_t e0, e1;
+    prof_pair(c, PK_ATTN, &e0, &e1);
+    HIPCHK(c, launch_attention(D.dtype, D.Dh, p, a, c->stream, e0, e1));
     return SDSAT_OK;
 }
 

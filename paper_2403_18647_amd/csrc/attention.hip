@@ -411,29 +411,36 @@ __global__ void __launch_bounds__(64) attn_combine_kernel(AttnArgs a, int rows) 
 }
 
 template <typename T, int DH>
-static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s) {
-    if (a.q > 16)
-        hipLaunchKernelGGL((attn_kernel<T, DH, true>), dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, a);
-    else
-        hipLaunchKernelGGL((attn_kernel<T, DH, false>), dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, a);
+static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+    const bool comb = a.splits > 1;
+    auto go = [&](auto kernel) {
+        if (ev0) hipExtLaunchKernelGGL(kernel, dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, ev0,
+                                       comb ? nullptr : ev1, 0, a);
+        else hipLaunchKernelGGL(kernel, dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, a);
+    };
+    if (a.q > 16) go(attn_kernel<T, DH, true>);
+    else go(attn_kernel<T, DH, false>);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || a.splits <= 1) return e;
+    if (e != hipSuccess || !comb) return e;
     const int n = a.B * a.H * a.q * (DH / 4);
-    hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3((n + 63) / 64), dim3(64), 0, s, a, (a.q + 15) / 16 * 16);
+    const int rows = (a.q + 15) / 16 * 16;
+    if (ev0) hipExtLaunchKernelGGL(attn_combine_kernel<T, DH>, dim3((n + 63) / 64), dim3(64), 0, s, nullptr, ev1, 0, a, rows);
+    else hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3((n + 63) / 64), dim3(64), 0, s, a, rows);
     return hipGetLastError();
 }
 
-hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s) {
+hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s,
+                            hipEvent_t ev0, hipEvent_t ev1) {
     if (a.q < 1 || a.q > 64 || p.waves < 1 || p.waves > kMaxWaves || a.splits < 1 || a.splits > kMaxSplits ||
         a.splits != p.splits || (a.splits > 1 && !a.part) || p.grid != a.B * a.H * a.splits || a.ldo % 4 != 0 ||
         a.per_split != p.per_split || a.per_split < 1)
         return hipErrorInvalidValue;
     if (dtype == 1) {
-        if (head_dim == 128) return launch_dh<uint16_t, 128>(p, a, s);
-        if (head_dim == 64) return launch_dh<uint16_t, 64>(p, a, s);
+        if (head_dim == 128) return launch_dh<uint16_t, 128>(p, a, s, ev0, ev1);
+        if (head_dim == 64) return launch_dh<uint16_t, 64>(p, a, s, ev0, ev1);
     } else {
-        if (head_dim == 128) return launch_dh<float, 128>(p, a, s);
-        if (head_dim == 64) return launch_dh<float, 64>(p, a, s);
+        if (head_dim == 128) return launch_dh<float, 128>(p, a, s, ev0, ev1);
+        if (head_dim == 64) return launch_dh<float, 64>(p, a, s, ev0, ev1);
     }
     return hipErrorInvalidValue;
 }

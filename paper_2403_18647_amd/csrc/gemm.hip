@@ -417,17 +417,21 @@ __global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(Gemm
 }
 
 template <typename T, int EP, bool XF>
-static hipError_t launch_mt(const GemmPlan& p, const GemmArgs& a, hipStream_t s) {
+static hipError_t launch_mt(const GemmPlan& p, const GemmArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     const dim3 grid(p.grid), block(64 * p.waves);
     if ((p.ntw > 1 || XF) && p.waves > 8) return hipErrorInvalidValue;
+    auto go = [&](auto kernel) {
+        if (ev0) hipExtLaunchKernelGGL(kernel, grid, block, p.lds_bytes, s, ev0, ev1, 0, a);
+        else hipLaunchKernelGGL(kernel, grid, block, p.lds_bytes, s, a);
+    };
     switch (p.mt * 10 + p.ntw) {
-        case 11: hipLaunchKernelGGL((gemm_kernel<T, EP, 1, 1, XF>), grid, block, p.lds_bytes, s, a); break;
-        case 21: hipLaunchKernelGGL((gemm_kernel<T, EP, 2, 1, XF>), grid, block, p.lds_bytes, s, a); break;
-        case 31: hipLaunchKernelGGL((gemm_kernel<T, EP, 3, 1, XF>), grid, block, p.lds_bytes, s, a); break;
-        case 41: hipLaunchKernelGGL((gemm_kernel<T, EP, 4, 1, XF>), grid, block, p.lds_bytes, s, a); break;
-        case 24: hipLaunchKernelGGL((gemm_kernel<T, EP, 2, 4, XF>), grid, block, p.lds_bytes, s, a); break;
-        case 34: hipLaunchKernelGGL((gemm_kernel<T, EP, 3, 4, XF>), grid, block, p.lds_bytes, s, a); break;
-        case 44: hipLaunchKernelGGL((gemm_kernel<T, EP, 4, 4, XF>), grid, block, p.lds_bytes, s, a); break;
+        case 11: go(gemm_kernel<T, EP, 1, 1, XF>); break;
+        case 21: go(gemm_kernel<T, EP, 2, 1, XF>); break;
+        case 31: go(gemm_kernel<T, EP, 3, 1, XF>); break;
+        case 41: go(gemm_kernel<T, EP, 4, 1, XF>); break;
+        case 24: go(gemm_kernel<T, EP, 2, 4, XF>); break;
+        case 34: go(gemm_kernel<T, EP, 3, 4, XF>); break;
+        case 44: go(gemm_kernel<T, EP, 4, 4, XF>); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -436,21 +440,23 @@ static hipError_t launch_mt(const GemmPlan& p, const GemmArgs& a, hipStream_t s)
 // RMSNorm-input GEMMs (QKV, gate/up, LM head) read float x o g rows; O and
 // down read element-type rows (attention output, SwiGLU product).
 template <typename T>
-static hipError_t launch_t(int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s) {
+static hipError_t launch_t(int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     const bool xf = a.xf != nullptr;
     if (xf && !a.ssq) return hipErrorInvalidValue;
     switch (ep) {
-        case EP_STORE: return xf ? launch_mt<T, EP_STORE, true>(p, a, s) : launch_mt<T, EP_STORE, false>(p, a, s);
-        case EP_QKV: return xf ? launch_mt<T, EP_QKV, true>(p, a, s) : hipErrorInvalidValue;
-        case EP_RESID: return xf ? hipErrorInvalidValue : launch_mt<T, EP_RESID, false>(p, a, s);
-        case EP_SWIGLU: return xf ? launch_mt<T, EP_SWIGLU, true>(p, a, s) : hipErrorInvalidValue;
+        case EP_STORE:
+            return xf ? launch_mt<T, EP_STORE, true>(p, a, s, e0, e1) : launch_mt<T, EP_STORE, false>(p, a, s, e0, e1);
+        case EP_QKV: return xf ? launch_mt<T, EP_QKV, true>(p, a, s, e0, e1) : hipErrorInvalidValue;
+        case EP_RESID: return xf ? hipErrorInvalidValue : launch_mt<T, EP_RESID, false>(p, a, s, e0, e1);
+        case EP_SWIGLU: return xf ? launch_mt<T, EP_SWIGLU, true>(p, a, s, e0, e1) : hipErrorInvalidValue;
         default: return hipErrorInvalidValue;
     }
 }
 
-hipError_t launch_gemm(int dtype, int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s) {
+hipError_t launch_gemm(int dtype, int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s, hipEvent_t ev0,
+                       hipEvent_t ev1) {
     if (a.M < 1 || a.M > 64 || p.waves < 1 || p.waves > 16) return hipErrorInvalidValue;
-    return dtype == 1 ? launch_t<uint16_t>(ep, p, a, s) : launch_t<float>(ep, p, a, s);
+    return dtype == 1 ? launch_t<uint16_t>(ep, p, a, s, ev0, ev1) : launch_t<float>(ep, p, a, s, ev0, ev1);
 }
 
 }  // namespace sdsat

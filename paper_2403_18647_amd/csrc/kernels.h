@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -74,7 +75,10 @@ struct GemmPlan {
     int waves, mt, ntw, grid, lds_bytes;   // ntw: 16-column tiles per workgroup
 };
 GemmPlan plan_gemm(int M, int n_tiles, int k_steps);
-hipError_t launch_gemm(int dtype, int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s);
+// ev0 / ev1 (optional): events taken at the kernel's own start and end (its
+// dispatch packet's timestamps), for timing one launch
+hipError_t launch_gemm(int dtype, int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s,
+                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 // ---------------------------------------------------------------- attention
 struct AttnArgs {
@@ -97,7 +101,9 @@ struct AttnArgs {
 struct AttnPlan { int waves, splits, per_split, grid, lds_bytes; };
 AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_max);
 size_t attention_partial_floats(int B, int H, int q_max, int head_dim);
-hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s);
+// ev0 / ev1 (optional): start of the attention kernel, end of the last kernel of the call
+hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s,
+                            hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 // ---------------------------------------------------------------- misc kernels
 hipError_t launch_embed(int dtype, const void* embed, int n_rows_emb, int d, const int* tokens, int M,
