@@ -258,7 +258,7 @@ def main():
     torch.cuda.synchronize()
     log(f"weights generated and resident ({time.time() - t0:.1f}s)")
     max_ctx = wl.prompt_len + wl.max_new + 2 * q + 32
-    cfg = B.make_config(sh, max_batch=wl.batch, max_ctx=max_ctx, max_block=max(q, 64 // wl.batch))
+    cfg = B.make_config(sh, max_batch=wl.batch, max_ctx=max_ctx, max_block=max(q, min(1024, wl.prompt_len)))
     ctx = B.Context(cfg, weights)
     torch.cuda.synchronize()
     log(f"context ready (workspace {ctx.workspace.numel() / 2**30:.2f} GiB)")

@@ -67,7 +67,11 @@ typedef struct sdsat_config {
     int32_t dtype;       /* SDSAT_DTYPE_FP32 or SDSAT_DTYPE_BF16: weights, KV cache, GEMM inputs */
     int32_t max_batch;   /* B_max */
     int32_t max_ctx;     /* KV slots per sequence (committed + one block) */
-    int32_t max_block;   /* largest q (rows per sequence per block), <= 64 */
+    int32_t max_block;   /* largest q (rows per sequence per block), <= 4096; also the
+                            prefill block of sdsat_generate.  Blocks of more than 64 rows
+                            in total (batch * q) run their linear layers as library GEMMs
+                            (rocBLAS, no atomics) on the caller's weights and take no
+                            ancestor mask; decode blocks need batch * (k + 1) <= 64 */
 } sdsat_config;
 
 /* Statistics of sdsat_generate (Section 3.4 reports tokens/s and accept rate). */

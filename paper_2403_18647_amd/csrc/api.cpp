@@ -2,6 +2,7 @@
 // weight packing, block forward, verification, KV commit and the draft/verify
 // generation loop (Section 2.1).  Declared in include/sdsat.h.
 #include <hip/hip_runtime.h>
+#include <rocblas/rocblas.h>
 
 #include <chrono>
 #include <cmath>
@@ -45,6 +46,9 @@ struct Dims {
     int d_pad, F_pad;  // activation row strides (contraction lengths padded to 32)
 };
 
+constexpr int kMaxBlock = 4096;   // rows per sequence per block
+constexpr int kSkinnyRows = 64;   // blocks of at most this many rows (B*q) run the skinny GEMM kernels
+
 int make_dims(const sdsat_config* c, Dims* D, std::string* why) {
     if (!c) { *why = "config is NULL"; return SDSAT_EINVAL; }
     if (c->n_layers < 1 || c->d_model < 16 || c->n_heads < 1 || c->d_ffn < 8 || c->vocab < 2 ||
@@ -56,13 +60,13 @@ int make_dims(const sdsat_config* c, Dims* D, std::string* why) {
     if (c->n_heads * c->head_dim != c->d_model) { *why = "d_model must equal n_heads * head_dim"; return SDSAT_EINVAL; }
     if (c->d_model % 16) { *why = "d_model must be a multiple of 16"; return SDSAT_EUNSUPPORTED; }
     if (c->dtype != SDSAT_DTYPE_FP32 && c->dtype != SDSAT_DTYPE_BF16) { *why = "dtype must be 0 or 1"; return SDSAT_EINVAL; }
-    if (c->max_block > 64) { *why = "max_block must be <= 64"; return SDSAT_EUNSUPPORTED; }
+    if (c->max_block > kMaxBlock) { *why = "max_block must be <= 4096"; return SDSAT_EUNSUPPORTED; }
     if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) { *why = "rms_eps must be >= 0 and rope_base > 0"; return SDSAT_EINVAL; }
     D->L = c->n_layers; D->d = c->d_model; D->H = c->n_heads; D->Dh = c->head_dim; D->F = c->d_ffn;
     D->V = c->vocab; D->A = c->n_adaptive; D->dtype = c->dtype; D->esz = c->dtype == SDSAT_DTYPE_BF16 ? 2 : 4;
     D->S = (int)align_up((size_t)c->max_ctx, 32);
     D->maxB = c->max_batch; D->maxQ = c->max_block;
-    D->maxM = c->max_batch * c->max_block < 64 ? c->max_batch * c->max_block : 64;
+    D->maxM = c->max_batch * c->max_block;
     D->ks_d = (D->d + 31) / 32; D->ks_f = (D->F + 31) / 32;
     D->nt_qkv = 3 * D->d / 16; D->nt_o = D->d / 16; D->nt_gu = (D->F + 7) / 8; D->nt_down = D->d / 16;
     D->nt_lm = (D->V + 15) / 16;
@@ -89,6 +93,9 @@ struct sdsat_ctx {
     const void* embed = nullptr;
     std::vector<const float*> attn_norm, ffn_norm;
     const float* final_norm = nullptr;
+    // the caller's row-major weights (embed, {attn_norm, wq, wk, wv, wo, ffn_norm, w_gate, w_up, w_down} x L,
+    // final_norm, lm_head): the library GEMMs of large blocks read them
+    std::vector<const void*> w_src;
     // packed weights
     std::vector<void*> w_qkv, w_o, w_gu, w_down;
     void* w_lm = nullptr;
@@ -108,6 +115,9 @@ struct sdsat_ctx {
     int *tok1 = nullptr, *out1 = nullptr, *out2 = nullptr, *n_accept = nullptr, *pending = nullptr;
     int *active = nullptr, *n_commit = nullptr, *pos0 = nullptr, *adaptive = nullptr, *ptok = nullptr;
     float* logits = nullptr;
+    // large blocks (more than kSkinnyRows rows): normalised rows (element type) and float GEMM outputs
+    void* hbuf = nullptr; float* c_qkv = nullptr; float* c_gu = nullptr; float* c_y = nullptr;
+    rocblas_handle blas = nullptr;
     int* h_pin = nullptr;   // pinned host staging
     size_t h_pin_ints = 0;
     // upper bounds of cache_len, tracked on the host for launch planning
@@ -118,6 +128,12 @@ struct sdsat_ctx {
     int64_t prof_seen = 0;
     std::vector<hipEvent_t> events;
     size_t ev_used = 0;
+
+    ~sdsat_ctx() {
+        for (hipEvent_t e : events) (void)hipEventDestroy(e);
+        if (h_pin) (void)hipHostFree(h_pin);
+        if (blas) (void)rocblas_destroy_handle(blas);
+    }
 };
 
 namespace {
@@ -173,6 +189,12 @@ void carve(sdsat_ctx* c, Carver& cv) {
     c->pos0 = (int*)cv.take((size_t)D.maxB * 4);
     c->adaptive = (int*)cv.take(64 * 4);
     c->logits = (float*)cv.take(bq * D.V * 4);
+    if (D.maxM > kSkinnyRows) {
+        c->hbuf = cv.take((size_t)D.maxM * D.d_pad * e);
+        c->c_qkv = (float*)cv.take((size_t)D.maxM * 3 * D.d * 4);
+        c->c_gu = (float*)cv.take((size_t)D.maxM * 2 * D.F * 4);
+        c->c_y = (float*)cv.take((size_t)D.maxM * D.d * 4);
+    }
 }
 
 void* layer_k(sdsat_ctx* c, int l) { return (char*)c->kc + (size_t)l * c->layer_elems * c->D.esz; }
@@ -274,9 +296,69 @@ int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask,
     return SDSAT_OK;
 }
 
+// C[M][N] (row stride ldc, float) = A[M][K] (row stride lda) . W[N][K]^T, A and W in the model's element
+// type, W the caller's row-major [out, in] weight: a plain library GEMM (column-major C^T = W^T' . A^T').
+int lib_gemm(sdsat_ctx* c, int M, int N, int K, const void* A, int lda, const void* W, float* C, int ldc) {
+    const rocblas_datatype t = c->D.dtype == SDSAT_DTYPE_BF16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
+    const float alpha = 1.f, beta = 0.f;
+    const rocblas_status st = rocblas_gemm_ex(c->blas, rocblas_operation_transpose, rocblas_operation_none, N, M, K,
+                                              &alpha, W, t, K, A, t, lda, &beta, C, rocblas_datatype_f32_r, ldc, C,
+                                              rocblas_datatype_f32_r, ldc, rocblas_datatype_f32_r,
+                                              rocblas_gemm_algo_standard, 0, 0);
+    if (st != rocblas_status_success)
+        return fail(c, SDSAT_EDEVICE, std::string("rocblas_gemm_ex: ") + rocblas_status_to_string(st));
+    return SDSAT_OK;
+}
+
+// Block forward of a large block (B*q > kSkinnyRows rows, chain mask): linear layers as library GEMMs on
+// the caller's weights, the rest in row-wise kernels that round where the skinny path rounds.
+int large_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, float* logits) {
+    const Dims& D = c->D;
+    const int M = B * q;
+    const float eps = c->cfg.rms_eps;
+    hipEvent_t evb;
+    prof_begin(c, logits ? PK_BLOCK : PK_PREFILL, &evb);
+    HIPCHK(c, launch_embed(D.dtype, c->embed, D.V + D.A, D.d, tokens, M, c->x, c->xg, c->attn_norm[0], D.d_pad,
+                           c->ssq, D.n_ssq, c->err_flag, c->stream));
+    for (int l = 0; l < D.L; ++l) {
+        const void* const* w = c->w_src.data() + 1 + 9 * l;   // attn_norm, wq, wk, wv, wo, ffn_norm, wg, wu, wd
+        HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, eps, M, c->hbuf, D.d_pad, c->stream));
+        for (int j = 0; j < 3; ++j) {
+            int rc = lib_gemm(c, M, D.d, D.d, c->hbuf, D.d_pad, w[1 + j], c->c_qkv + j * D.d, 3 * D.d);
+            if (rc) return rc;
+        }
+        HIPCHK(c, launch_qkv_rope(D.dtype, c->c_qkv, 3 * D.d, M, q, D.H, D.Dh, c->cache_len, D.S, c->rope,
+                                  (float*)c->qbuf, layer_k(c, l), layer_v(c, l), c->err_flag, c->stream));
+        int rc = attention_layer(c, l, B, q, nullptr, (const float*)c->qbuf, c->obuf, 0, D.d_pad);
+        if (rc) return rc;
+        rc = lib_gemm(c, M, D.d, D.d, c->obuf, D.d_pad, w[4], c->c_y, D.d);
+        if (rc) return rc;
+        HIPCHK(c, launch_resid_rows(c->c_y, D.d, M, D.d, c->x, D.d, c->xg, D.d_pad, c->ffn_norm[l], c->ssq, D.n_ssq,
+                                    c->stream));
+        HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, eps, M, c->hbuf, D.d_pad, c->stream));
+        for (int j = 0; j < 2; ++j) {
+            rc = lib_gemm(c, M, D.F, D.d, c->hbuf, D.d_pad, w[6 + j], c->c_gu + j * D.F, 2 * D.F);
+            if (rc) return rc;
+        }
+        HIPCHK(c, launch_swiglu_rows(D.dtype, c->c_gu, c->c_gu + D.F, 2 * D.F, M, D.F, c->ubuf, D.F_pad, c->stream));
+        rc = lib_gemm(c, M, D.d, D.F, c->ubuf, D.F_pad, w[8], c->c_y, D.d);
+        if (rc) return rc;
+        HIPCHK(c, launch_resid_rows(c->c_y, D.d, M, D.d, c->x, D.d, c->xg, D.d_pad,
+                                    l + 1 < D.L ? c->attn_norm[l + 1] : c->final_norm, c->ssq, D.n_ssq, c->stream));
+    }
+    if (logits) {
+        HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, eps, M, c->hbuf, D.d_pad, c->stream));
+        int rc = lib_gemm(c, M, D.V, D.d, c->hbuf, D.d_pad, c->w_src[2 + 9 * D.L], logits, D.V);
+        if (rc) return rc;
+    }
+    prof_end(c, evb);
+    return SDSAT_OK;
+}
+
 int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const uint64_t* mask, float* logits) {
     const Dims& D = c->D;
     const int M = B * q;
+    if (M > kSkinnyRows) return large_block_impl(c, B, q, tokens, logits);
     hipEvent_t evb;
     prof_begin(c, logits ? PK_BLOCK : PK_PREFILL, &evb);
     HIPCHK(c, launch_embed(D.dtype, c->embed, D.V + D.A, D.d, tokens, M, c->x, c->xg, c->attn_norm[0], D.d_pad,
@@ -387,6 +469,7 @@ int sdsat_init(const sdsat_config* cfg, const void* const* weights, int32_t n_we
     (void)hipGetDevice(&c->device);
 
     c->embed = weights[0];
+    c->w_src.assign(weights, weights + n_weights);
     c->attn_norm.resize(D.L); c->ffn_norm.resize(D.L);
     for (int l = 0; l < D.L; ++l) {
         const void* const* w = weights + 1 + 9 * l;
@@ -461,6 +544,14 @@ int sdsat_init(const sdsat_config* cfg, const void* const* weights, int32_t n_we
         c->err = "pinned host allocation failed";
         return init_fail(SDSAT_ENOMEM);
     }
+    if (D.maxM > kSkinnyRows) {   // large blocks: deterministic library GEMMs (no atomics) on the context's stream
+        if (rocblas_create_handle(&c->blas) != rocblas_status_success ||
+            rocblas_set_stream(c->blas, c->stream) != rocblas_status_success ||
+            rocblas_set_atomics_mode(c->blas, rocblas_atomics_not_allowed) != rocblas_status_success) {
+            c->err = "rocBLAS handle creation failed";
+            return init_fail(SDSAT_EDEVICE);
+        }
+    }
     *out = c;
     return SDSAT_OK;
 }
@@ -496,7 +587,8 @@ int sdsat_forward_block(sdsat_ctx* c, int32_t batch, int32_t q, const int32_t* d
     int rc = check_block_args(c, batch, q);
     if (rc) return rc;
     if (!d_tokens) return fail(c, SDSAT_EINVAL, "d_tokens is NULL");
-    if (batch * q > 64) return fail(c, SDSAT_ECAPACITY, "batch * q must be <= 64");
+    if (batch * q > kSkinnyRows && d_ancestor_mask)
+        return fail(c, SDSAT_EUNSUPPORTED, "ancestor masks need batch * q <= 64");
     bool ok = false;
     rc = fits(c, batch, q, &ok);
     if (rc) return rc;
@@ -573,8 +665,8 @@ int sdsat_generate(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_
     const auto t0 = clk::now();
     int rc = sdsat_reset(c, batch);
     if (rc) return rc;
-    // prefill: prompt tokens 0..P-2 in blocks of up to qc rows per sequence
-    const int qc = std::max(1, std::min(D.maxQ, 64 / batch));
+    // prefill: prompt tokens 0..P-2 in blocks of up to max_block rows per sequence
+    const int qc = D.maxQ;
     for (int lo = 0; lo < P - 1; lo += qc) {
         const int n = std::min(qc, P - 1 - lo);
         for (int b = 0; b < batch; ++b)
@@ -761,8 +853,6 @@ int sdsat_kernel_time(sdsat_ctx* c, double* total_ms, int64_t* launches) {
 int sdsat_destroy(sdsat_ctx* c) {
     if (!c) return SDSAT_OK;
     (void)hipStreamSynchronize(c->stream);
-    for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
-    if (c->h_pin) (void)hipHostFree(c->h_pin);
     delete c;
     return SDSAT_OK;
 }

@@ -431,7 +431,7 @@ static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s,
 
 hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s,
                             hipEvent_t ev0, hipEvent_t ev1) {
-    if (a.q < 1 || a.q > 64 || p.waves < 1 || p.waves > kMaxWaves || a.splits < 1 || a.splits > kMaxSplits ||
+    if (a.q < 1 || a.q > 4096 || (a.mask && a.q > 64) || p.waves < 1 || p.waves > kMaxWaves || a.splits < 1 || a.splits > kMaxSplits ||
         a.splits != p.splits || (a.splits > 1 && !a.part) || p.grid != a.B * a.H * a.splits || a.ldo % 4 != 0 ||
         a.per_split != p.per_split || a.per_split < 1)
         return hipErrorInvalidValue;

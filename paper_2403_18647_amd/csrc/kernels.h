@@ -122,6 +122,21 @@ hipError_t launch_fill_i32(int* p, size_t n, int value, hipStream_t s);
 // rotary table [S][half][2]: cos and sin of the angle pos * inv_freq[i], formed in double, rounded to float
 hipError_t launch_rope_table(const double* inv_freq, int S, int half, float* rope, hipStream_t s);
 
+// ---------------------------------------------------------------- large blocks (prefill)
+// Row-wise steps around the library GEMMs of blocks of more than 64 rows.
+// h = elem(xg / rms) with rms from the row's per-16-column sums of squares
+hipError_t launch_rms_rows(int dtype, const float* xg, int ldxg, const float* ssq, int n_ssq, int K, float eps, int M,
+                           void* h, int ldh, hipStream_t s);
+// c[m] = Q | K | V (float, row stride ldc): RoPE, Q to qbuf [M][H][Dh], K / V into the cache at cache_len[b] + row
+hipError_t launch_qkv_rope(int dtype, const float* c, int ldc, int M, int q, int H, int Dh, const int* cache_len,
+                           int S_max, const float* rope, float* qbuf, void* kc, void* vc, int* err, hipStream_t s);
+// x += y; xg = x o gnext; ssq = per-16-column sums of squares of x
+hipError_t launch_resid_rows(const float* y, int ldy, int M, int N, float* x, int ldx, float* xg, int ldxg,
+                             const float* gnext, float* ssq, int n_tiles, hipStream_t s);
+// u = elem(silu(g) * up)
+hipError_t launch_swiglu_rows(int dtype, const float* g, const float* up, int ldg, int M, int F, void* u, int ldu,
+                              hipStream_t s);
+
 // ---------------------------------------------------------------- verify
 hipError_t launch_verify_greedy(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,
                                 int* tokens_out, int* n_accept, int* counter, hipStream_t s);

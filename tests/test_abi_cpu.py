@@ -48,7 +48,7 @@ def test_query_sizes_host_only():
     assert big > weights
 
 
-@pytest.mark.parametrize("field,value,code", [("head_dim", 96, B.ERRORS and -5), ("max_block", 65, -5),
+@pytest.mark.parametrize("field,value,code", [("head_dim", 96, B.ERRORS and -5), ("max_block", 4097, -5),
                                               ("d_model", 250, -1), ("dtype", 7, -1), ("n_layers", 0, -1)])
 def test_query_sizes_rejects_bad_configs(field, value, code):
     cfg = B.make_config(synth.TINY, max_batch=1, max_ctx=128, max_block=6)

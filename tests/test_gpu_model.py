@@ -97,6 +97,55 @@ def test_block_rows_bitwise_equal_single_token_steps(dtype, k, prompt_len):
     ctx.close()
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_large_block_matches_oracle(dtype):
+    """A block of more than 64 rows (the prompt-prefill path: library GEMMs on the caller's weights
+    around row-wise kernels that round where the decode kernels round) matches the oracle's block
+    forward: its logits, and the K/V it leaves in the cache, read back by the next (decode-size) block.
+    Batch 2 x 70 rows after a 40-token prefix prefilled in 16-row blocks."""
+    if dtype == "bf16":
+        shape = synth.small_shape(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=688, vocab=1000,
+                                  n_adaptive=5, rope_base=1e6, dtype="bf16")
+        tol = 3e-2
+    else:
+        shape = synth.small_shape()   # the tiny fp32 decoder
+        tol = 1e-4
+    Bn, P, q, q2 = 2, 40, 70, 6
+    wl = synth.Workload("large", shape, seed=13, batch=Bn, k=q2 - 1, prompt_len=P, max_new=1, gain_std=0.1)
+    W = helpers.oracle_weights(wl)
+    bf16 = dtype == "bf16"
+    prompts = synth.prompts(wl)
+    rng = np.random.default_rng(5)
+    toks = rng.integers(0, shape.vocab, (Bn, q)).astype(np.int32)
+    toks2 = rng.integers(0, shape.vocab, (Bn, q2)).astype(np.int32)
+    ctx = helpers.make_ctx(wl, max_batch=Bn, max_ctx=P + q + q2 + 16, max_block=q)
+    dev = "cuda"
+    B.sdsat_reset(ctx.handle, Bn)
+    for lo in range(0, P, 16):
+        t = torch.from_numpy(np.ascontiguousarray(prompts[:, lo:lo + 16]).astype(np.int32)).to(dev)
+        n = t.shape[1]
+        B.sdsat_forward_block(ctx.handle, Bn, n, t, None, None)
+        B.sdsat_commit_kv(ctx.handle, Bn, n, torch.full((Bn,), n, dtype=torch.int32, device=dev))
+    lg = torch.empty((Bn * q, shape.vocab), dtype=torch.float32, device=dev)
+    B.sdsat_forward_block(ctx.handle, Bn, q, torch.from_numpy(toks).to(dev), None, lg)
+    B.sdsat_commit_kv(ctx.handle, Bn, q, torch.full((Bn,), q, dtype=torch.int32, device=dev))
+    lg2 = torch.empty((Bn * q2, shape.vocab), dtype=torch.float32, device=dev)
+    B.sdsat_forward_block(ctx.handle, Bn, q2, torch.from_numpy(toks2).to(dev), None, lg2)
+    torch.cuda.synchronize()
+    lg, lg2 = lg.cpu().numpy().reshape(Bn, q, -1), lg2.cpu().numpy().reshape(Bn, q2, -1)
+    worst = 0.0
+    for b in range(Bn):
+        cache = M.prefill(shape, W, prompts[b], bf16=bf16)
+        ref, kv = M.forward_block(shape, W, cache, toks[b], np.arange(P, P + q), bf16=bf16)
+        cache.commit(kv, range(q))
+        ref2, _ = M.forward_block(shape, W, cache, toks2[b], np.arange(P + q, P + q + q2), bf16=bf16)
+        e1, e2 = float(np.abs(lg[b] - ref).max()), float(np.abs(lg2[b] - ref2).max())
+        worst = max(worst, e1, e2)
+        assert e1 <= tol and e2 <= tol, (b, e1, e2)
+    print(f"large block {dtype}: max |logit diff| = {worst:.3g}")
+    ctx.close()
+
+
 def test_generate_tiny_greedy_matches_ar():
     wl = synth.workload("tiny")
     sh = wl.shape
