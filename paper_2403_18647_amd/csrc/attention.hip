@@ -6,16 +6,19 @@
 //   the block rows r may see (0..r, or the rows set in its ancestor mask).
 // The block's own K/V rows were written into slots L_b.. by the QKV epilogue.
 //
-// Workgroups per (b, h): one, or a few key splits when the (b, h) pairs alone
-// cannot fill the GPU.  Waves take the workgroup's 32-key blocks round-robin.
+// Workgroups per (b, h, 16-row tile of the block): one per key split (the
+// splits are fixed 32-key block ranges, see plan_attention); a combine
+// kernel merges the splits' partials.  Waves take the workgroup's 32-key
+// blocks round-robin.
 // Q arrives in float and the probabilities are formed in float; on bf16
 // models each enters the matrix cores as a pair of bf16 fragments (value and
 // rounding remainder, about 16 significant bits), so neither is rounded to
 // bf16 on its way: the scores and the weighted sum of V keep float accuracy
 // (K and V are bf16 as stored).
-// Query rows are handled 16 at a time (one matrix-core tile); a block of more
-// rows (a prefill chunk) loops over its row tiles and re-reads the keys, which
-// then come from L2.  Per block a wave computes the 32 x 16 score tile
+// Query rows are handled 16 at a time (one matrix-core tile); the row tiles
+// of a longer block (a prefill chunk) are separate workgroups that read the
+// same keys (the later readers from L2), each only up to its last row.  Per
+// block a wave computes the 32 x 16 score tile
 // S^T = K Q^T on the matrix cores (A = K rows straight from the cache, B = Q^T
 // from registers), runs an online softmax per query row (query rows live in
 // lanes, keys in registers and lane groups), and accumulates O^T = V^T P^T
@@ -33,35 +36,29 @@ namespace sdsat {
 static constexpr int kMaxWaves = 8;
 static constexpr int kMaxSplits = 8;
 
-// Decode blocks (q <= 16) partition the keys by absolute 32-key block index
-// only: split sp owns blocks [sp * P, (sp + 1) * P) with P fixed by the cache
-// capacity (at full capacity, as many splits as fit one round of 256
-// workgroups), and within a split block i goes to wave i mod waves.  A query
-// row therefore sees the same keys in the same order of accumulation whatever
-// the block size q and the cache length: blocks it cannot see (later rows of
-// its own block) add exact zeros.  So a token's logits do not depend on how
-// many draft rows share its block, and greedy SDSAT reproduces autoregressive
-// decoding bit for bit.  Longer blocks (prefill chunks) do q/16 passes over
-// the keys per workgroup and take splits of at least two blocks.  Waves per
-// workgroup: one per block of the split, at most 8.
+// Keys are partitioned by absolute 32-key block index only: split sp owns
+// blocks [sp * P, (sp + 1) * P) with P fixed by the cache capacity (at full
+// capacity, as many splits as fit one round of 256 workgroups per row tile),
+// and within a split block i goes to wave i mod waves.  Each 16-row tile of
+// the block has its own workgroups and reads only the key blocks its last row
+// can see.  A query row therefore sees the same keys in the same order of
+// accumulation whatever the block size q and the cache length: blocks it
+// cannot see (later rows of its own block) add exact zeros.  So a token's
+// logits do not depend on how many draft rows share its block, and greedy
+// SDSAT reproduces autoregressive decoding bit for bit.  Waves per workgroup:
+// one per block of the split, at most 8.
 AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_max) {
     AttnPlan p;
     const int cap = std::max(1, S_max / 32);
     const int nblk = std::max(1, std::min(cap, (max_len + q + 31) / 32));
     const int pairs = B * H;
-    if (q <= 16) {
-        // one round of workgroups (a workgroup of 8 waves holds a compute unit's registers)
-        const int target = std::max(1, std::min(kMaxSplits, 256 / pairs));
-        p.per_split = (cap + target - 1) / target;
-        p.splits = (nblk + p.per_split - 1) / p.per_split;
-    } else {
-        int splits = 1;
-        if (pairs < 256) splits = std::max(1, std::min(std::min((256 + pairs - 1) / pairs, nblk / 2), kMaxSplits));
-        p.per_split = (nblk + splits - 1) / splits;
-        p.splits = (nblk + p.per_split - 1) / p.per_split;
-    }
+    // one round of workgroups per row tile (a workgroup of 8 waves holds a compute unit's registers)
+    const int target = std::max(1, std::min(kMaxSplits, 256 / pairs));
+    p.per_split = (cap + target - 1) / target;
+    p.splits = (nblk + p.per_split - 1) / p.per_split;
+    p.row_tiles = (q + 15) / 16;
     p.waves = std::max(1, std::min(p.per_split, kMaxWaves));
-    p.grid = pairs * p.splits;
+    p.grid = pairs * p.row_tiles * p.splits;
     p.lds_bytes = p.waves * (head_dim / 16) * 64 * 16;
     return p;
 }
@@ -174,9 +171,8 @@ __device__ __forceinline__ void attend_block(const Frag<T> (&kf)[2][NDS], const 
     }
 }
 
-// MULTI: more than 16 query rows (a loop over row tiles); decode blocks take
-// the single-tile instance, which keeps nothing live across tiles.
-template <typename T, int DH, bool MULTI>
+// One workgroup per (sequence, head, 16-row tile, key split).
+template <typename T, int DH>
 __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     constexpr int NDS = DH / 32;   // 32-wide steps over the head dimension
     constexpr int NDT = DH / 16;   // 16-row output tiles over the head dimension
@@ -191,9 +187,11 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     const int lane = threadIdx.x & 63, c = lane & 15, g = lane >> 4;
     Frag<T>* s_q = reinterpret_cast<Frag<T>*>(smem_raw + (size_t)wave * DH * 64);
     const f32x4_t* opart = reinterpret_cast<const f32x4_t*>(smem_raw);   // [waves][NDT][64]
-    const int bh = blockIdx.x / a.splits, sp = blockIdx.x % a.splits;
-    const int b = bh / a.H, h = bh % a.H;
     const int q = a.q;
+    const int n_rt = (q + 15) / 16;
+    const int sp = blockIdx.x % a.splits, rt = (blockIdx.x / a.splits) % n_rt;
+    const int bh = blockIdx.x / (a.splits * n_rt);
+    const int b = bh / a.H, h = bh % a.H;
     const uint32_t slice_bytes = (uint32_t)a.S_max * DH * sizeof(T);
     const __amdgpu_buffer_rsrc_t kr =
         buf_rsrc(reinterpret_cast<const T*>(a.kc) + ((size_t)b * a.H + h) * a.S_max * DH, slice_bytes);
@@ -210,16 +208,13 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     const int wlo = sp * a.per_split;
     const int first = wlo + wave;
     const int last_blk = a.S_max / 32 - 1;
-    const int n_rt = MULTI ? (q + 15) / 16 : 1;
     // The cache length is the first request, as a vector load (a scalar one
     // would be scheduled after the K/V requests, and the first block waits
     // for it).
     int bv = b;
     asm volatile("" : "+v"(bv));
     const int Lv = a.cache_len[bv];
-    int L = 0, whi = 0;
-
-    for (int rt = 0; rt < n_rt; ++rt) {
+    {
         // Issue order: the ancestor mask, the wave's Q fragments, its first two
         // K/V blocks; Q is split and parked in the wave's LDS while the keys
         // are in flight (no barrier: each wave reads only its own copy).
@@ -228,7 +223,6 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
         // the compiler's wait counts stay exact.
         const int m = 16 * rt + c;
         const int mr = min(m, q - 1);
-        if (MULTI && rt > 0) __syncthreads();   // every wave is done reading the previous tile's partials
         const uint64_t mrow = tree ? a.mask[(size_t)b * q + mr] : 0ull;
         const f32x4_t* qsrc = reinterpret_cast<const f32x4_t*>(qb + (((size_t)b * q + mr) * a.H + h) * DH + 8 * g);
         f32x4_t qv[NDS][2];
@@ -250,15 +244,14 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
             s_q[ds * 64 + lane] = fh;
             if constexpr (sizeof(T) == 2) s_q[(NDS + ds) * 64 + lane] = fl;
         }
-        if (rt == 0) {
-            L = __builtin_amdgcn_readfirstlane(Lv);
-            if (L + q > a.S_max) {   // the host checks capacity; never read past this sequence's cache
-                if (threadIdx.x == 0) atomicOr(a.err, 4);
-                return;
-            }
-            const int nblk = (L + q + 31) / 32;
-            whi = sp == a.splits - 1 ? nblk : min(nblk, wlo + a.per_split);
+        const int L = __builtin_amdgcn_readfirstlane(Lv);
+        if (L + q > a.S_max) {   // the host checks capacity; never read past this sequence's cache
+            if (threadIdx.x == 0) atomicOr(a.err, 4);
+            return;
         }
+        // key blocks the tile's last row can see (keys up to L + that row)
+        const int nblk = (L + min(16 * rt + 15, q - 1) + 32) / 32;
+        const int whi = sp == a.splits - 1 ? nblk : min(nblk, wlo + a.per_split);
         const int Tb = L + q;
 
         float rmax = -INFINITY, rsum = 0.f;
@@ -413,13 +406,11 @@ __global__ void __launch_bounds__(64) attn_combine_kernel(AttnArgs a, int rows) 
 template <typename T, int DH>
 static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     const bool comb = a.splits > 1;
-    auto go = [&](auto kernel) {
-        if (ev0) hipExtLaunchKernelGGL(kernel, dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, ev0,
-                                       comb ? nullptr : ev1, 0, a);
-        else hipLaunchKernelGGL(kernel, dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, a);
-    };
-    if (a.q > 16) go(attn_kernel<T, DH, true>);
-    else go(attn_kernel<T, DH, false>);
+    if (ev0)
+        hipExtLaunchKernelGGL(attn_kernel<T, DH>, dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, ev0,
+                              comb ? nullptr : ev1, 0, a);
+    else
+        hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !comb) return e;
     const int n = a.B * a.H * a.q * (DH / 4);
@@ -432,7 +423,8 @@ static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s,
 hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s,
                             hipEvent_t ev0, hipEvent_t ev1) {
     if (a.q < 1 || a.q > 4096 || (a.mask && a.q > 64) || p.waves < 1 || p.waves > kMaxWaves || a.splits < 1 || a.splits > kMaxSplits ||
-        a.splits != p.splits || (a.splits > 1 && !a.part) || p.grid != a.B * a.H * a.splits || a.ldo % 4 != 0 ||
+        a.splits != p.splits || (a.splits > 1 && !a.part) || p.row_tiles != (a.q + 15) / 16 ||
+        p.grid != a.B * a.H * a.splits * p.row_tiles || a.ldo % 4 != 0 ||
         a.per_split != p.per_split || a.per_split < 1)
         return hipErrorInvalidValue;
     if (dtype == 1) {

@@ -96,9 +96,9 @@ struct AttnArgs {
     int out_f32, ldo;
     int* err;                // device error flags (bit 4: read past the cache)
 };
-// `splits` workgroups of `waves` waves per (sequence, head); max_len: the host's
+// `splits` workgroups of `waves` waves per (sequence, head, 16-row tile); max_len: the host's
 // upper bound of the cache lengths; S_max: key slots per sequence
-struct AttnPlan { int waves, splits, per_split, grid, lds_bytes; };
+struct AttnPlan { int waves, splits, per_split, row_tiles, grid, lds_bytes; };
 AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_max);
 size_t attention_partial_floats(int B, int H, int q_max, int head_dim);
 // ev0 / ev1 (optional): start of the attention kernel, end of the last kernel of the call
