@@ -175,6 +175,20 @@ int sdsat_generate(sdsat_ctx* ctx, int32_t batch, const int32_t* h_prompts, int3
                    float temperature, float top_p, int32_t top_k, uint64_t seed,
                    int32_t* h_out, sdsat_stats* h_stats);
 
+/* sdsat_generate with the drafts of every draft step 2 taken from a known
+ * continuation instead of draft step 1's adaptive rows: d_j of sequence b
+ * = h_ref[b][n + j] (n = tokens sequence b has emitted so far, j = 1..k; ids
+ * past ref_len read as 0).  With h_ref = the autoregressive output of the
+ * same prompts (ref_len >= max_new + k + 1), verification (Eq. 3) accepts
+ * every draft, so each loop emits k + 2 tokens: the loop at full acceptance,
+ * for measurement on weights whose adaptive rows do not predict the target.
+ * h_ref: [batch, ref_len] int32 (host).  Other arguments and the output as
+ * sdsat_generate.  Synchronous. */
+int sdsat_generate_forced(sdsat_ctx* ctx, int32_t batch, const int32_t* h_prompts, int32_t P,
+                          int32_t max_new, int32_t k, const int32_t* h_adaptive_ids, int32_t mode,
+                          float temperature, float top_p, int32_t top_k, uint64_t seed,
+                          const int32_t* h_ref, int32_t ref_len, int32_t* h_out, sdsat_stats* h_stats);
+
 /* ---- op-level entry points (kernel tests and micro-benchmarks) ---- */
 
 /* Write K and V rows (float32, [batch, n, H, Dh]) of `layer` into cache slots

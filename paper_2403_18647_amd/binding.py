@@ -52,6 +52,9 @@ _SIGNATURES = {
     "sdsat_commit_kv": ([_VP, _I32, _I32, _VP, _VP], _I32),
     "sdsat_generate": ([_VP, _I32, ctypes.POINTER(_I32), _I32, _I32, _I32, ctypes.POINTER(_I32), _I32, _F32, _F32,
                         _I32, _U64, ctypes.POINTER(_I32), ctypes.POINTER(sdsat_stats)], _I32),
+    "sdsat_generate_forced": ([_VP, _I32, ctypes.POINTER(_I32), _I32, _I32, _I32, ctypes.POINTER(_I32), _I32, _F32,
+                               _F32, _I32, _U64, ctypes.POINTER(_I32), _I32, ctypes.POINTER(_I32),
+                               ctypes.POINTER(sdsat_stats)], _I32),
     "sdsat_kv_write": ([_VP, _I32, _I32, _I32, _VP, _VP, _VP], _I32),
     "sdsat_attention": ([_VP, _I32, _I32, _I32, _VP, _VP, _VP], _I32),
     "sdsat_linear_packed_bytes": ([_I32, _I32, _I32], _SZ),
@@ -164,16 +167,25 @@ def sdsat_commit_kv(ctx, batch, q, n_commit, rows=None):
 
 
 def sdsat_generate(ctx, prompts, max_new, k, adaptive_ids, mode=MODE_GREEDY, temperature=0.0, top_p=1.0,
-                   top_k=0, seed=0):
-    """prompts: host int32 [batch, P].  Returns (tokens int32 [batch, max_new], stats dict)."""
+                   top_k=0, seed=0, ref=None):
+    """prompts: host int32 [batch, P].  Returns (tokens int32 [batch, max_new], stats dict).  With ref
+    (host int32 [batch, ref_len]) calls sdsat_generate_forced: draft step 2 takes its drafts from ref."""
     p = np.ascontiguousarray(prompts, np.int32)
     batch, P = p.shape
     ad = np.ascontiguousarray(adaptive_ids if k else np.zeros(1), np.int32)
     out = np.zeros((batch, max_new), np.int32)
     st = sdsat_stats()
     ip = ctypes.POINTER(ctypes.c_int32)
-    _check(lib().sdsat_generate(ctx, batch, p.ctypes.data_as(ip), P, max_new, k, ad.ctypes.data_as(ip), mode,
-                                temperature, top_p, top_k, seed, out.ctypes.data_as(ip), ctypes.byref(st)), ctx)
+    if ref is None:
+        _check(lib().sdsat_generate(ctx, batch, p.ctypes.data_as(ip), P, max_new, k, ad.ctypes.data_as(ip), mode,
+                                    temperature, top_p, top_k, seed, out.ctypes.data_as(ip), ctypes.byref(st)), ctx)
+    else:
+        r = np.ascontiguousarray(ref, np.int32)
+        if r.ndim != 2 or r.shape[0] != batch:
+            raise ValueError("ref must be [batch, ref_len]")
+        _check(lib().sdsat_generate_forced(ctx, batch, p.ctypes.data_as(ip), P, max_new, k, ad.ctypes.data_as(ip),
+                                           mode, temperature, top_p, top_k, seed, r.ctypes.data_as(ip), r.shape[1],
+                                           out.ctypes.data_as(ip), ctypes.byref(st)), ctx)
     stats = {"loops": st.loops, "blocks": st.blocks, "prefill_blocks": st.prefill_blocks, "tokens": st.tokens,
              "accepted": st.accepted, "accept_hist": list(st.accept_hist)[: k + 1],
              "prefill_ms": st.prefill_ms, "decode_ms": st.decode_ms}

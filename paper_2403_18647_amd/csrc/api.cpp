@@ -637,9 +637,15 @@ int sdsat_commit_kv(sdsat_ctx* c, int32_t batch, int32_t q, const int32_t* d_n_c
     return SDSAT_OK;
 }
 
-int sdsat_generate(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t P, int32_t max_new, int32_t k,
-                   const int32_t* h_adaptive_ids, int32_t mode, float temperature, float top_p, int32_t top_k,
-                   uint64_t seed, int32_t* h_out, sdsat_stats* h_stats) {
+}  // extern "C"
+
+namespace {
+
+// The generation loop of sdsat_generate; with h_ref, draft step 2 takes its drafts d_1..d_k of
+// sequence b from h_ref[b][n+1..n+k] (n = tokens emitted so far) instead of draft step 1's rows.
+int generate_impl(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t P, int32_t max_new, int32_t k,
+                  const int32_t* h_adaptive_ids, int32_t mode, float temperature, float top_p, int32_t top_k,
+                  uint64_t seed, const int32_t* h_ref, int32_t ref_len, int32_t* h_out, sdsat_stats* h_stats) {
     if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
     const Dims& D = c->D;
     if (batch < 1 || batch > D.maxB) return fail(c, SDSAT_ECAPACITY, "batch exceeds max_batch");
@@ -714,6 +720,16 @@ int sdsat_generate(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_
         }
         HIPCHK(c, launch_commit(c->cache_len, batch, c->active, D.S, c->err_flag, c->stream));   // keep row 0 (active: 1)
         for (int b = 0; b < batch; ++b) c->len_hint[b] += h_act[b];
+        if (h_ref && k > 0) {   // drafts from the reference continuation (pinned staging after h_err)
+            int* dr = h_err + 1;
+            for (int b = 0; b < batch; ++b)
+                for (int j = 0; j < k; ++j) {
+                    const long i = (long)produced[b] + 1 + j;
+                    dr[b * k + j] = i < ref_len ? h_ref[(size_t)b * ref_len + i] : 0;
+                }
+            HIPCHK(c, hipMemcpy2DAsync(c->out1 + 1, (size_t)q * 4, dr, (size_t)k * 4, (size_t)k * 4, batch,
+                                       hipMemcpyHostToDevice, c->stream));
+        }
         // draft step 2 (Eq. 2): [t1, d_1..d_k] = out1
         rc = forward_block_impl(c, batch, q, c->out1, nullptr, c->logits);
         if (rc) return rc;
@@ -757,6 +773,29 @@ int sdsat_generate(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_
     st.decode_ms = std::chrono::duration<double, std::milli>(t2 - t1).count();
     if (h_stats) *h_stats = st;
     return SDSAT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sdsat_generate(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t P, int32_t max_new, int32_t k,
+                   const int32_t* h_adaptive_ids, int32_t mode, float temperature, float top_p, int32_t top_k,
+                   uint64_t seed, int32_t* h_out, sdsat_stats* h_stats) {
+    return generate_impl(c, batch, h_prompts, P, max_new, k, h_adaptive_ids, mode, temperature, top_p, top_k, seed,
+                         nullptr, 0, h_out, h_stats);
+}
+
+int sdsat_generate_forced(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t P, int32_t max_new,
+                          int32_t k, const int32_t* h_adaptive_ids, int32_t mode, float temperature, float top_p,
+                          int32_t top_k, uint64_t seed, const int32_t* h_ref, int32_t ref_len, int32_t* h_out,
+                          sdsat_stats* h_stats) {
+    if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
+    if (!h_ref || ref_len < 1) return fail(c, SDSAT_EINVAL, "h_ref is NULL or ref_len < 1");
+    for (long i = 0; i < (long)batch * ref_len; ++i)
+        if (h_ref[i] < 0 || h_ref[i] >= c->D.V + c->D.A) return fail(c, SDSAT_EINVAL, "reference id out of range");
+    return generate_impl(c, batch, h_prompts, P, max_new, k, h_adaptive_ids, mode, temperature, top_p, top_k, seed,
+                         h_ref, ref_len, h_out, h_stats);
 }
 
 int sdsat_kv_write(sdsat_ctx* c, int32_t layer, int32_t batch, int32_t n, const float* d_k, const float* d_v,

@@ -120,3 +120,22 @@ def test_7b_batch4_nucleus_sdsat_emits_ar_nucleus_tokens():
         assert [int(t) for t in sd[b]] == [int(t) for t in ar[b]], b
     assert st["blocks"] == 2 * st["loops"]
     ctx.close()
+
+
+def test_7b_forced_drafts_from_ar_output_accept_every_draft():
+    """Whole 7B model: the greedy AR continuation fed as drafts is accepted in full every loop
+    (m = k = 5, 7 tokens per loop), and the emitted tokens are the AR tokens."""
+    wl = synth.workload("7b", max_new=42)
+    sh = wl.shape
+    q = wl.k + 1
+    weights = synth.device_weights(wl, "cuda")
+    cfg = B.make_config(sh, max_batch=1, max_ctx=wl.prompt_len + wl.max_new + 3 * q + 32, max_block=512)
+    ctx = B.Context(cfg, weights)
+    prompts = synth.prompts(wl)
+    ad = synth.adaptive_ids(sh, wl.k)
+    ref, _ = B.sdsat_generate(ctx.handle, prompts, wl.max_new + wl.k + 1, 0, ad)
+    out, st = B.sdsat_generate(ctx.handle, prompts, wl.max_new, wl.k, ad, ref=ref)
+    assert [int(t) for t in out[0]] == [int(t) for t in ref[0, :wl.max_new]]
+    assert st["accept_hist"][wl.k] == st["loops"] == wl.max_new // (wl.k + 2)
+    print(f"7b forced drafts: {st['loops']} loops, accept hist {st['accept_hist']}")
+    ctx.close()

@@ -146,6 +146,28 @@ def test_large_block_matches_oracle(dtype):
     ctx.close()
 
 
+@pytest.mark.parametrize("name,k", [("tiny", 5), ("small_bf16", 10)])
+def test_forced_drafts_from_ar_output_accept_every_draft(name, k):
+    """Section 2.1, Eq. 3: drafts equal to the target's own continuation are all accepted.  Feeding the
+    greedy AR output as the drafts of every draft step 2 gives m = k in every loop (k + 2 tokens per
+    loop) and exactly the AR tokens -- this needs a token's logits to be the same whether it is decoded
+    alone or inside a (k+1)-row block, which the GPU guarantees bit for bit."""
+    wl = synth.workload("tiny", max_new=40) if name == "tiny" else helpers.small_bf16(
+        max_new=40, shape=synth.small_shape(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=688,
+                                            vocab=1000, n_adaptive=10, rope_base=1e6, dtype="bf16"))
+    sh = wl.shape
+    q = k + 1
+    ctx = helpers.make_ctx(wl, max_batch=1, max_ctx=wl.prompt_len + wl.max_new + 3 * q + 16, max_block=q)
+    prompts = synth.prompts(wl)
+    ad = synth.adaptive_ids(sh, k)
+    ref, _ = B.sdsat_generate(ctx.handle, prompts, wl.max_new + k + 1, 0, ad)
+    out, st = B.sdsat_generate(ctx.handle, prompts, wl.max_new, k, ad, ref=ref)
+    assert [int(t) for t in out[0]] == [int(t) for t in ref[0, :wl.max_new]]
+    assert st["accept_hist"][k] == st["loops"] and st["accepted"] == k * st["loops"]
+    assert st["loops"] == -(-wl.max_new // (k + 2))
+    ctx.close()
+
+
 def test_generate_tiny_greedy_matches_ar():
     wl = synth.workload("tiny")
     sh = wl.shape
