@@ -120,6 +120,34 @@ def cpu_baseline(wl, m_bar, n_layers_sample=2, n_blocks=3):
     }
 
 
+def ksweep(B, synth, ctx, wl, prompts, new_tokens=64, k_max=13):
+    """Block-forward and loop time against k (Section 3.4: the loop time stays almost flat as k grows),
+    greedy, identical adaptive ids (any k).  Per k: HIP events around every block forward of a
+    generation of `new_tokens`, and the same generation with the autoregressive continuation injected
+    as drafts (full acceptance, synthetic)."""
+    import torch
+    sh = wl.shape
+    rows = []
+    for k in range(0, k_max + 1):
+        ad = synth.adaptive_ids(sh, k, identical=True) if k else []
+        B.sdsat_generate(ctx.handle, prompts, new_tokens, k, ad)   # warm-up at this block size
+        B.sdsat_profile_kernel(ctx.handle, "block")
+        _, st = B.sdsat_generate(ctx.handle, prompts, new_tokens, k, ad)
+        blk_ms, n_blk = B.sdsat_kernel_time(ctx.handle)
+        B.sdsat_profile_kernel(ctx.handle, "off")
+        ref, _ = B.sdsat_generate(ctx.handle, prompts, new_tokens + k + 1, 0, ad)
+        torch.cuda.synchronize()
+        out_f, st_f = B.sdsat_generate(ctx.handle, prompts, new_tokens, k, ad, ref=ref)
+        rows.append({"k": k, "q": k + 1, "block_ms": round(blk_ms / max(1, n_blk), 4),
+                     "loop_ms": round(st_f["decode_ms"] / max(1, st_f["loops"]), 4),
+                     "tokens_per_loop_full_accept": k + 2 if k else 2,
+                     "decode_tokens_per_s_full_accept": round(new_tokens * wl.batch / (st_f["decode_ms"] / 1e3), 2),
+                     "tokens_equal_ar": bool((out_f == ref[:, :new_tokens]).all())})
+    return {"metric": "k sweep: block forward and loop time vs k", "unit": "ms", "workload": wl.name,
+            "data": "synthetic (random-init weights; identical adaptive ids; full acceptance injected)",
+            "new_tokens": new_tokens, "rows": rows}
+
+
 def micro(B, synth):
     """Kernel micro-benchmarks: device-event times on the library stream, weights rotated past the
     256 MB memory-side cache where they are streamed."""
@@ -223,6 +251,7 @@ def main():
                          "[8, 11, 32016] logits, the 11 x 4096 x 11008 skinny GEMM")
     ap.add_argument("--no-ar-baseline", action="store_true")
     ap.add_argument("--no-forced", action="store_true", help="skip the full-acceptance (injected drafts) run")
+    ap.add_argument("--ksweep", action="store_true", help="block and loop time for k = 0..13 (prints its own line)")
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (a plain copy kernel of known "
                          "size, for scaling hardware traffic counters)")
@@ -266,6 +295,9 @@ def main():
     prompts = synth.prompts(wl)
     ad = synth.adaptive_ids(sh, wl.k)
     mode = B.MODE_NUCLEUS if wl.mode == "nucleus" else B.MODE_GREEDY
+    if args.ksweep:
+        print(json.dumps(ksweep(B, synth, ctx, wl, prompts)), flush=True)
+        return
 
     def step():
         return B.sdsat_generate(ctx.handle, prompts, wl.max_new, wl.k, ad, mode=mode,
