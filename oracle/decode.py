@@ -160,6 +160,138 @@ def generate_sdsat(shape, weights, prompt, k, max_new, adaptive, mode="greedy",
     return out[:max_new], ms
 
 
+# ---------------------------------------------------------------- draft tree (Section 2.1.2)
+#
+# Draft step 1 offers, at each adaptive row j, several possible draft tokens.
+# Draft step 2 arranges them as a tree run in one block with tree attention,
+# and verification keeps the longest branch the target confirms.  The paper
+# leaves the tree shape to a manual design; the reading here is a chain plus
+# siblings of width w: depth j holds the w most probable tokens of adaptive
+# row j (ties to the lower id); the first forms the main chain, the other
+# w - 1 are leaves under the chain node one level up.  w = 1 is the chain.
+
+
+def top_candidates(row: np.ndarray, w: int) -> list[int]:
+    """The w largest values of a logit row, ties to the lower id."""
+    r = np.asarray(row, np.float32).astype(np.float64)
+    order = np.lexsort((np.arange(r.shape[0]), -r))
+    return [int(i) for i in order[:w]]
+
+
+def draft_tree(t1: int, cand: list[list[int]]):
+    """Draft step 2's block for the candidates cand[j-1] of depths j = 1..k.
+
+    Rows: 0 the root t1; 1..k the chain (depth j, parent j-1); then, depth by
+    depth, each depth's other candidates (parent: the chain node one level
+    up).  Returns (tokens, parent, depth) lists over the rows.
+    """
+    tokens, parent, depth = [int(t1)], [-1], [0]
+    k = len(cand)
+    for j in range(1, k + 1):
+        tokens.append(int(cand[j - 1][0]))
+        parent.append(j - 1)
+        depth.append(j)
+    for j in range(1, k + 1):
+        for t in cand[j - 1][1:]:
+            tokens.append(int(t))
+            parent.append(j - 1)
+            depth.append(j)
+    return tokens, parent, depth
+
+
+def tree_visibility(parent) -> np.ndarray:
+    """[q, q] boolean: row r may attend to block row a iff a is r or one of its ancestors."""
+    q = len(parent)
+    vis = np.zeros((q, q), bool)
+    for r in range(q):
+        a = r
+        while a >= 0:
+            vis[r, a] = True
+            a = parent[a]
+    return vis
+
+
+def verify_tree(targets, tokens, parent):
+    """Longest confirmed branch (the verification of Section 2.1.2, in the
+    form of Eq. 3).  From the root, the target's token at the current node
+    (targets[node]) is emitted; if a child of the node carries that token (the
+    lowest such row) the walk descends into it, otherwise it stops.  Returns
+    (path rows from the root, emitted tokens); m = len(path) - 1 drafts were
+    accepted and len(path) tokens emitted."""
+    children: dict[int, list[int]] = {}
+    for r in range(1, len(parent)):
+        children.setdefault(parent[r], []).append(r)
+    path, emitted, node = [0], [], 0
+    while True:
+        t = int(targets[node])
+        emitted.append(t)
+        nxt = next((r for r in children.get(node, []) if int(tokens[r]) == t), None)
+        if nxt is None:
+            return path, emitted
+        path.append(nxt)
+        node = nxt
+
+
+def generate_sdsat_tree(shape, weights, prompt, k, width, max_new, adaptive, mode="nucleus",
+                        temperature=1.0, top_p=1.0, top_k=0, seed=0, b=0, bf16=False, per_row=False,
+                        force_cand=None, trace=None):
+    """SDSAT with a draft tree of the given width (Section 2.1.2).  Returns (tokens, per-loop m).
+
+    ``force_cand(n, k, width)``, if given, replaces draft step 1's candidates
+    (a list of k lists of width tokens) for a loop whose first token is output
+    number n (to place known continuations at chosen tree nodes)."""
+    prompt = np.asarray(prompt, np.int64)
+    adaptive = [int(a) for a in adaptive[:k]]
+    cache = M.prefill(shape, weights, prompt[:-1], bf16=bf16, per_row=per_row)
+    pending = int(prompt[-1])
+    out: list[int] = []
+    ms: list[int] = []
+    greedy = mode == "greedy" or temperature <= 0.0
+    while len(out) < max_new:
+        # draft step 1: [pending, a_1..a_k]; t1 from row 0, candidates from the adaptive rows
+        L = cache.length
+        logits, kv = _block(shape, weights, cache, [pending] + adaptive, bf16, per_row, trace)
+        lg = np.asarray(logits, np.float32)
+        if greedy:
+            t1 = S.argmax_lowest(lg[0])
+        else:
+            t1, mg = S.sample(lg[0], temperature, top_p, top_k, S.uniform(seed, b, L + 1))
+            if trace is not None:
+                trace.margins.append(mg)
+        cand = [top_candidates(lg[j], width) for j in range(1, k + 1)]
+        cache.commit(kv, [0])
+        out.append(int(t1))
+        if force_cand is not None:
+            cand = [[int(t) for t in c] for c in force_cand(len(out), k, width)]
+        # draft step 2: the tree, rows at positions L + depth, each seeing its ancestors
+        tokens, parent, depth = draft_tree(t1, cand)
+        L = cache.length
+        vis = tree_visibility(parent)
+        logits, kv = M.forward_block(shape, weights, cache, tokens, L + np.asarray(depth), visible=vis,
+                                     bf16=bf16, per_row=per_row)
+        if trace is not None:
+            trace.blocks.append({"tokens": np.asarray(tokens, np.int64), "cache_len": L, "parent": list(parent),
+                                 "logits": logits.astype(np.float32) if bf16 else logits})
+        lg = np.asarray(logits, np.float32)
+        targets = []
+        for r in range(len(tokens)):
+            if greedy:
+                targets.append(S.argmax_lowest(lg[r]))
+            else:
+                t, mg = S.sample(lg[r], temperature, top_p, top_k, S.uniform(seed, b, L + 1 + depth[r]))
+                targets.append(t)
+                if trace is not None:
+                    trace.margins.append(mg)
+        path, emitted = verify_tree(targets, tokens, parent)
+        cache.commit(kv, path)
+        out.extend(emitted)
+        pending = emitted[-1]
+        ms.append(len(path) - 1)
+    if trace is not None:
+        trace.loop_m = ms
+    return out[:max_new], ms
+
+
 def generate_ar(shape, weights, prompt, max_new, mode="greedy", temperature=1.0, top_p=1.0,
                 top_k=0, seed=0, b=0, bf16=False, per_row=False, trace=None):
     """Plain autoregressive decoding, one token per block forward."""

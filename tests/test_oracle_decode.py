@@ -261,3 +261,102 @@ def test_nucleus_sdsat_preserves_top_p_joint_distribution():
         dof += 1
     # generous bound: chi2 < dof + 5 sqrt(2 dof)
     assert chi2 < dof + 5 * math.sqrt(2 * dof), (chi2, dof)
+
+
+# ---------------------------------------------------------------- draft tree (Section 2.1.2)
+def test_draft_tree_layout_and_visibility():
+    """Rows: root, the chain of first candidates, then each depth's other candidates under the chain
+    node one level up; each row sees exactly itself and its ancestors (siblings never see each other)."""
+    tokens, parent, depth = D.draft_tree(7, [[1, 2, 3], [4, 5, 6]])
+    assert tokens == [7, 1, 4, 2, 3, 5, 6]
+    assert parent == [-1, 0, 1, 0, 0, 1, 1]
+    assert depth == [0, 1, 2, 1, 1, 2, 2]
+    vis = D.tree_visibility(parent)
+    for r in range(len(parent)):
+        anc, a = set(), r
+        while a >= 0:
+            anc.add(a)
+            a = parent[a]
+        assert set(np.nonzero(vis[r])[0].tolist()) == anc
+    assert not vis[3, 4] and not vis[4, 3] and not vis[5, 2]
+
+
+def test_verify_tree_worked_cases():
+    """Longest confirmed branch, worked by hand: rows 0:7 (root), 1:1, 2:4 (chain), 3:2 (depth-1 leaf),
+    4:5 (depth-2 leaf).  targets[r] is the target's token after row r."""
+    tokens, parent, _ = D.draft_tree(7, [[1, 2], [4, 5]])
+    assert D.verify_tree([1, 4, 9, 0, 0], tokens, parent) == ([0, 1, 2], [1, 4, 9])   # chain twice
+    assert D.verify_tree([1, 5, 0, 0, 8], tokens, parent) == ([0, 1, 4], [1, 5, 8])   # depth-2 leaf
+    assert D.verify_tree([2, 0, 0, 6, 0], tokens, parent) == ([0, 3], [2, 6])         # depth-1 leaf
+    assert D.verify_tree([3, 0, 0, 0, 0], tokens, parent) == ([0], [3])               # nothing
+
+
+def test_top_candidates_order_and_ties():
+    row = np.array([0.5, 2.0, 2.0, -1.0, 1.0], np.float32)
+    assert D.top_candidates(row, 3) == [1, 2, 4]
+    assert D.top_candidates(row, 1) == [S.argmax_lowest(row)]
+
+
+@pytest.mark.parametrize("mode", ["greedy", "nucleus"])
+def test_tree_of_width_one_is_the_chain(mode):
+    wl, w = _model(weight_std=0.08)
+    sh = wl.shape
+    pr = synth.prompts(wl)[0]
+    ad = synth.adaptive_ids(sh, 4)
+    kw = dict(mode=mode, temperature=0.8, top_p=0.95, top_k=0, seed=5, per_row=True)
+    out_t, ms_t = D.generate_sdsat_tree(sh, w, pr, 4, 1, 25, ad, **kw)
+    out_c, ms_c = D.generate_sdsat(sh, w, pr, 4, 25, ad, **kw)
+    assert out_t == out_c and ms_t == ms_c
+
+
+@pytest.mark.parametrize("width,k", [(2, 3), (3, 4)])
+@pytest.mark.parametrize("T,p,top_k", [(0.8, 0.95, 0), (0.2, 0.95, 10)])
+def test_tree_nucleus_equals_ar_nucleus_tokenwise(width, k, T, p, top_k):
+    """Every token the tree loop emits is the target's keyed sample at its position, so the output is
+    the AR nucleus sequence whatever the tree."""
+    wl, w = _model(weight_std=0.08)
+    sh = wl.shape
+    pr = synth.prompts(wl)[0]
+    for b in range(2):
+        tr = D.Trace()
+        out, _ = D.generate_sdsat_tree(sh, w, pr, k, width, 24, synth.adaptive_ids(sh, k), temperature=T,
+                                       top_p=p, top_k=top_k, seed=17, b=b, per_row=True, trace=tr)
+        ref = D.generate_ar(sh, w, pr, 24, mode="nucleus", temperature=T, top_p=p, top_k=top_k, seed=17, b=b,
+                            per_row=True)
+        assert out == ref
+        assert min(tr.margins) > 1e-12
+
+
+def test_tree_greedy_equals_ar_greedy():
+    wl, w = _model()
+    sh = wl.shape
+    pr = synth.prompts(wl)[0]
+    out, _ = D.generate_sdsat_tree(sh, w, pr, 4, 3, 30, synth.adaptive_ids(sh, 4), mode="greedy", per_row=True)
+    assert out == D.generate_ar(sh, w, pr, 30, per_row=True)
+
+
+@pytest.mark.parametrize("where", ["depth1_leaf", "depth2_leaf", "chain"])
+def test_tree_accepts_known_continuation_at_any_node(where):
+    """Candidates forced so that the true continuation sits on the chain or on a leaf: the walk accepts
+    it (m as predicted), commits the branch's rows (a leaf is not block row m), and later loops still
+    emit the greedy AR tokens, which fails if a committed row's K/V is the wrong one."""
+    wl, w = _model()
+    sh = wl.shape
+    pr = synth.prompts(wl)[0]
+    k, width, n_new = 3, 2, 24
+    ref = D.generate_ar(sh, w, pr, n_new + k + 2, per_row=True)
+    wrong = lambda t: (t + 1) % sh.vocab
+
+    def cand(n, kk, ww):
+        # output number n is the loop's t1 (ref[n-1]); depth j's true token is ref[n - 1 + j]
+        true = [ref[n - 1 + j] for j in range(1, kk + 1)]
+        if where == "chain":
+            return [[t, wrong(t)] for t in true]
+        if where == "depth1_leaf":
+            return [[wrong(true[0]), true[0]]] + [[true[j], wrong(true[j])] for j in range(1, kk)]
+        return [[true[0], wrong(true[0])], [wrong(true[1]), true[1]]] + [[t, wrong(t)] for t in true[2:]]
+
+    out, ms = D.generate_sdsat_tree(sh, w, pr, k, width, n_new, synth.adaptive_ids(sh, k), mode="greedy",
+                                    per_row=True, force_cand=cand)
+    assert out == ref[:n_new]
+    assert set(ms) == {{"chain": k, "depth1_leaf": 1, "depth2_leaf": 2}[where]}
