@@ -175,6 +175,23 @@ int sdsat_generate(sdsat_ctx* ctx, int32_t batch, const int32_t* h_prompts, int3
                    float temperature, float top_p, int32_t top_k, uint64_t seed,
                    int32_t* h_out, sdsat_stats* h_stats);
 
+/* sdsat_generate with draft step 2 run over a draft tree (Section 2.1.2):
+ * depth j = 1..k holds the `width` most probable tokens of draft step 1's
+ * adaptive row j (ties to the lower id); the first of each depth forms the
+ * main chain, the others are leaves under the chain node one level up.  The
+ * tree's 1 + k*width rows run as one block with ancestor masks (each row at
+ * position cache_len + depth, seeing its ancestors); the target's token at
+ * every node (greedy arg-max, or the nucleus sample keyed by the position it
+ * is for) is computed, the longest branch whose tokens the targets confirm
+ * is accepted (m of its nodes), its rows are gathered into the cache and
+ * m + 1 tokens are emitted after t1.  width = 1 is sdsat_generate.  Needs
+ * width in 1..8, 1 + k*width <= max_block and batch * (1 + k*width) <= 64.
+ * Other arguments and the output as sdsat_generate.  Synchronous. */
+int sdsat_generate_tree(sdsat_ctx* ctx, int32_t batch, const int32_t* h_prompts, int32_t P,
+                        int32_t max_new, int32_t k, int32_t width, const int32_t* h_adaptive_ids,
+                        int32_t mode, float temperature, float top_p, int32_t top_k, uint64_t seed,
+                        int32_t* h_out, sdsat_stats* h_stats);
+
 /* sdsat_generate with the drafts of every draft step 2 taken from a known
  * continuation instead of draft step 1's adaptive rows: d_j of sequence b
  * = h_ref[b][n + j] (n = tokens sequence b has emitted so far, j = 1..k; ids

@@ -98,6 +98,7 @@ class Trace:
     blocks: list = field(default_factory=list)
     loop_m: list = field(default_factory=list)
     margins: list = field(default_factory=list)
+    paths: list = field(default_factory=list)     # draft tree: the accepted branch's block rows per loop
 
 
 def _block(shape, weights, cache, tokens, bf16, per_row, trace):
@@ -283,6 +284,8 @@ def generate_sdsat_tree(shape, weights, prompt, k, width, max_new, adaptive, mod
                 if trace is not None:
                     trace.margins.append(mg)
         path, emitted = verify_tree(targets, tokens, parent)
+        if trace is not None:
+            trace.paths.append(list(path))
         cache.commit(kv, path)
         out.extend(emitted)
         pending = emitted[-1]

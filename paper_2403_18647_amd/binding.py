@@ -52,6 +52,8 @@ _SIGNATURES = {
     "sdsat_commit_kv": ([_VP, _I32, _I32, _VP, _VP], _I32),
     "sdsat_generate": ([_VP, _I32, ctypes.POINTER(_I32), _I32, _I32, _I32, ctypes.POINTER(_I32), _I32, _F32, _F32,
                         _I32, _U64, ctypes.POINTER(_I32), ctypes.POINTER(sdsat_stats)], _I32),
+    "sdsat_generate_tree": ([_VP, _I32, ctypes.POINTER(_I32), _I32, _I32, _I32, _I32, ctypes.POINTER(_I32), _I32,
+                             _F32, _F32, _I32, _U64, ctypes.POINTER(_I32), ctypes.POINTER(sdsat_stats)], _I32),
     "sdsat_generate_forced": ([_VP, _I32, ctypes.POINTER(_I32), _I32, _I32, _I32, ctypes.POINTER(_I32), _I32, _F32,
                                _F32, _I32, _U64, ctypes.POINTER(_I32), _I32, ctypes.POINTER(_I32),
                                ctypes.POINTER(sdsat_stats)], _I32),
@@ -167,16 +169,23 @@ def sdsat_commit_kv(ctx, batch, q, n_commit, rows=None):
 
 
 def sdsat_generate(ctx, prompts, max_new, k, adaptive_ids, mode=MODE_GREEDY, temperature=0.0, top_p=1.0,
-                   top_k=0, seed=0, ref=None):
+                   top_k=0, seed=0, ref=None, width=1):
     """prompts: host int32 [batch, P].  Returns (tokens int32 [batch, max_new], stats dict).  With ref
-    (host int32 [batch, ref_len]) calls sdsat_generate_forced: draft step 2 takes its drafts from ref."""
+    (host int32 [batch, ref_len]) calls sdsat_generate_forced: draft step 2 takes its drafts from ref.
+    With width > 1 calls sdsat_generate_tree (draft tree of that width)."""
     p = np.ascontiguousarray(prompts, np.int32)
     batch, P = p.shape
     ad = np.ascontiguousarray(adaptive_ids if k else np.zeros(1), np.int32)
     out = np.zeros((batch, max_new), np.int32)
     st = sdsat_stats()
     ip = ctypes.POINTER(ctypes.c_int32)
-    if ref is None:
+    if width > 1:
+        if ref is not None:
+            raise ValueError("ref and width > 1 cannot be combined")
+        _check(lib().sdsat_generate_tree(ctx, batch, p.ctypes.data_as(ip), P, max_new, k, width,
+                                         ad.ctypes.data_as(ip), mode, temperature, top_p, top_k, seed,
+                                         out.ctypes.data_as(ip), ctypes.byref(st)), ctx)
+    elif ref is None:
         _check(lib().sdsat_generate(ctx, batch, p.ctypes.data_as(ip), P, max_new, k, ad.ctypes.data_as(ip), mode,
                                     temperature, top_p, top_k, seed, out.ctypes.data_as(ip), ctypes.byref(st)), ctx)
     else:

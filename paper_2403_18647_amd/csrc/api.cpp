@@ -114,6 +114,9 @@ struct sdsat_ctx {
     // generation buffers
     int *tok1 = nullptr, *out1 = nullptr, *out2 = nullptr, *n_accept = nullptr, *pending = nullptr;
     int *active = nullptr, *n_commit = nullptr, *pos0 = nullptr, *adaptive = nullptr, *ptok = nullptr;
+    // draft tree (draft step 2 of the tree loop): tokens, ancestor masks, depths, targets, branch rows
+    int *tree_tok = nullptr, *tree_depth = nullptr, *tree_target = nullptr, *tree_rows = nullptr;
+    uint64_t* tree_mask = nullptr;
     float* logits = nullptr;
     // large blocks (more than kSkinnyRows rows): normalised rows (element type) and float GEMM outputs
     void* hbuf = nullptr; float* c_qkv = nullptr; float* c_gu = nullptr; float* c_y = nullptr;
@@ -188,6 +191,11 @@ void carve(sdsat_ctx* c, Carver& cv) {
     c->n_commit = (int*)cv.take((size_t)D.maxB * 4);
     c->pos0 = (int*)cv.take((size_t)D.maxB * 4);
     c->adaptive = (int*)cv.take(64 * 4);
+    c->tree_tok = (int*)cv.take(bq * 4);
+    c->tree_depth = (int*)cv.take(bq * 4);
+    c->tree_target = (int*)cv.take(bq * 4);
+    c->tree_rows = (int*)cv.take(bq * 4);
+    c->tree_mask = (uint64_t*)cv.take(bq * 8);
     c->logits = (float*)cv.take(bq * D.V * 4);
     if (D.maxM > kSkinnyRows) {
         c->hbuf = cv.take((size_t)D.maxM * D.d_pad * e);
@@ -644,23 +652,27 @@ namespace {
 // The generation loop of sdsat_generate; with h_ref, draft step 2 takes its drafts d_1..d_k of
 // sequence b from h_ref[b][n+1..n+k] (n = tokens emitted so far) instead of draft step 1's rows.
 int generate_impl(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t P, int32_t max_new, int32_t k,
-                  const int32_t* h_adaptive_ids, int32_t mode, float temperature, float top_p, int32_t top_k,
-                  uint64_t seed, const int32_t* h_ref, int32_t ref_len, int32_t* h_out, sdsat_stats* h_stats) {
+                  int32_t width, const int32_t* h_adaptive_ids, int32_t mode, float temperature, float top_p,
+                  int32_t top_k, uint64_t seed, const int32_t* h_ref, int32_t ref_len, int32_t* h_out,
+                  sdsat_stats* h_stats) {
     if (!c) return fail(nullptr, SDSAT_EINVAL, "ctx is NULL");
     const Dims& D = c->D;
     if (batch < 1 || batch > D.maxB) return fail(c, SDSAT_ECAPACITY, "batch exceeds max_batch");
     if (!h_prompts || !h_out || P < 1 || max_new < 0 || k < 0) return fail(c, SDSAT_EINVAL, "bad prompts/out/P/k");
     if (k > 0 && !h_adaptive_ids) return fail(c, SDSAT_EINVAL, "h_adaptive_ids is NULL");
     const int q = k + 1;
-    if (q > D.maxQ) return fail(c, SDSAT_ECAPACITY, "k + 1 exceeds max_block");
-    if (batch * q > 64) return fail(c, SDSAT_ECAPACITY, "batch * (k + 1) must be <= 64");
+    if (width < 1 || width > kMaxTreeWidth) return fail(c, SDSAT_EINVAL, "tree width must be 1..8");
+    const bool tree = width > 1 && k > 0;
+    const int q2 = tree ? 1 + k * width : q;   // rows of draft step 2 (the tree block)
+    if (q2 > D.maxQ) return fail(c, SDSAT_ECAPACITY, "k + 1 (tree: 1 + k * width) exceeds max_block");
+    if (batch * q2 > 64) return fail(c, SDSAT_ECAPACITY, "batch * (k + 1) (tree: 1 + k * width) must be <= 64");
     if (mode != SDSAT_MODE_GREEDY && mode != SDSAT_MODE_NUCLEUS) return fail(c, SDSAT_EINVAL, "bad mode");
     const bool nucleus = mode == SDSAT_MODE_NUCLEUS && temperature > 0.f;
     if (nucleus && D.V > 32768) return fail(c, SDSAT_EUNSUPPORTED, "nucleus verification needs vocab <= 32768");
     for (int j = 0; j < k; ++j)
         if (h_adaptive_ids[j] < 0 || h_adaptive_ids[j] >= D.V + D.A)
             return fail(c, SDSAT_EINVAL, "adaptive id out of range");
-    if ((long)P - 1 + (long)max_new + q + 1 > D.S) return fail(c, SDSAT_ECAPACITY, "prompt + max_new exceeds max_ctx");
+    if ((long)P - 1 + (long)max_new + q2 + 1 > D.S) return fail(c, SDSAT_ECAPACITY, "prompt + max_new exceeds max_ctx");
     for (long i = 0; i < (long)batch * P; ++i)
         if (h_prompts[i] < 0 || h_prompts[i] >= D.V + D.A) return fail(c, SDSAT_EINVAL, "prompt id out of range");
 
@@ -698,8 +710,8 @@ int generate_impl(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t
     std::vector<int> produced(batch, 0);
     int* h_act = c->h_pin;                       // [batch]
     int* h_o1 = c->h_pin + 64;                   // [batch*q]
-    int* h_o2 = h_o1 + (size_t)batch * q;        // [batch*q]
-    int* h_m = h_o2 + (size_t)batch * q;         // [batch]
+    int* h_o2 = h_o1 + (size_t)batch * q;        // [batch*q2]
+    int* h_m = h_o2 + (size_t)batch * q2;        // [batch]
     int* h_err = h_m + batch;
     for (;;) {
         bool any = false;
@@ -730,22 +742,46 @@ int generate_impl(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t
             HIPCHK(c, hipMemcpy2DAsync(c->out1 + 1, (size_t)q * 4, dr, (size_t)k * 4, (size_t)k * 4, batch,
                                        hipMemcpyHostToDevice, c->stream));
         }
-        // draft step 2 (Eq. 2): [t1, d_1..d_k] = out1
-        rc = forward_block_impl(c, batch, q, c->out1, nullptr, c->logits);
-        if (rc) return rc;
-        if (nucleus) {
-            HIPCHK(c, launch_pos0(c->cache_len, batch, 1, c->pos0, c->stream));
-            HIPCHK(c, launch_verify_nucleus(c->logits, batch, q, D.V, c->out1 + 1, q, temperature, top_p, top_k,
-                                            seed, c->pos0, c->out2, c->n_accept, c->verify_cnt, c->stream));
+        if (tree) {
+            // draft step 2 over the tree (Section 2.1.2): candidates of draft step 1's adaptive rows, rows at
+            // position L + depth seeing their ancestors; the target's token at every node; the longest
+            // confirmed branch; its rows gathered to slots L.. and committed, pending = the last token
+            HIPCHK(c, launch_tree_build(c->logits, batch, q, D.V, c->out1, k, width, q2, c->tree_tok, c->tree_mask,
+                                        c->tree_depth, c->stream));
+            rc = forward_block_impl(c, batch, q2, c->tree_tok, c->tree_mask, c->logits);
+            if (rc) return rc;
+            if (nucleus) {
+                HIPCHK(c, launch_pos0(c->cache_len, batch, 1, c->pos0, c->stream));
+                HIPCHK(c, launch_verify_nucleus(c->logits, batch, q2, D.V, nullptr, 0, temperature, top_p, top_k,
+                                                seed, c->pos0, c->tree_target, nullptr, c->verify_cnt, c->stream,
+                                                c->tree_depth));
+            } else {
+                HIPCHK(c, launch_verify_greedy(c->logits, batch, q2, D.V, nullptr, 0, c->tree_target, nullptr,
+                                               c->verify_cnt, c->stream));
+            }
+            HIPCHK(c, launch_tree_walk(batch, q2, k, width, c->tree_tok, c->tree_target, c->active, c->out2,
+                                       c->n_accept, c->tree_rows, c->pending, c->n_commit, c->stream));
+            HIPCHK(c, launch_commit_gather(D.dtype, c->kc, c->vc, c->layer_elems, D.L, batch, D.H, D.Dh, D.S,
+                                           c->cache_len, c->n_commit, c->tree_rows, q2, c->err_flag, c->stream));
+            HIPCHK(c, launch_commit(c->cache_len, batch, c->n_commit, D.S, c->err_flag, c->stream));
         } else {
-            HIPCHK(c, launch_verify_greedy(c->logits, batch, q, D.V, c->out1 + 1, q, c->out2, c->n_accept,
-                                           c->verify_cnt, c->stream));
+            // draft step 2 (Eq. 2): [t1, d_1..d_k] = out1
+            rc = forward_block_impl(c, batch, q, c->out1, nullptr, c->logits);
+            if (rc) return rc;
+            if (nucleus) {
+                HIPCHK(c, launch_pos0(c->cache_len, batch, 1, c->pos0, c->stream));
+                HIPCHK(c, launch_verify_nucleus(c->logits, batch, q, D.V, c->out1 + 1, q, temperature, top_p, top_k,
+                                                seed, c->pos0, c->out2, c->n_accept, c->verify_cnt, c->stream));
+            } else {
+                HIPCHK(c, launch_verify_greedy(c->logits, batch, q, D.V, c->out1 + 1, q, c->out2, c->n_accept,
+                                               c->verify_cnt, c->stream));
+            }
+            // verification (Eq. 3): commit rows 0..m, pending = o_m
+            HIPCHK(c, launch_loop_commit(c->cache_len, batch, q, c->active, c->n_accept, c->out2, c->pending,
+                                         c->n_commit, c->stream));
         }
-        // verification (Eq. 3): commit rows 0..m, pending = o_m
-        HIPCHK(c, launch_loop_commit(c->cache_len, batch, q, c->active, c->n_accept, c->out2, c->pending,
-                                     c->n_commit, c->stream));
         HIPCHK(c, hipMemcpyAsync(h_o1, c->out1, (size_t)batch * q * 4, hipMemcpyDeviceToHost, c->stream));
-        HIPCHK(c, hipMemcpyAsync(h_o2, c->out2, (size_t)batch * q * 4, hipMemcpyDeviceToHost, c->stream));
+        HIPCHK(c, hipMemcpyAsync(h_o2, c->out2, (size_t)batch * q2 * 4, hipMemcpyDeviceToHost, c->stream));
         HIPCHK(c, hipMemcpyAsync(h_m, c->n_accept, (size_t)batch * 4, hipMemcpyDeviceToHost, c->stream));
         HIPCHK(c, hipMemcpyAsync(h_err, c->err_flag, 4, hipMemcpyDeviceToHost, c->stream));
         HIPCHK(c, hipStreamSynchronize(c->stream));
@@ -764,7 +800,7 @@ int generate_impl(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t
             st.tokens += m + 2;
             int* row = h_out + (size_t)b * max_new;
             if (produced[b] < max_new) row[produced[b]++] = h_o1[b * q];
-            for (int j = 0; j <= m && produced[b] < max_new; ++j) row[produced[b]++] = h_o2[b * q + j];
+            for (int j = 0; j <= m && produced[b] < max_new; ++j) row[produced[b]++] = h_o2[b * q2 + j];
             c->len_hint[b] += m + 1;
         }
     }
@@ -782,8 +818,15 @@ extern "C" {
 int sdsat_generate(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t P, int32_t max_new, int32_t k,
                    const int32_t* h_adaptive_ids, int32_t mode, float temperature, float top_p, int32_t top_k,
                    uint64_t seed, int32_t* h_out, sdsat_stats* h_stats) {
-    return generate_impl(c, batch, h_prompts, P, max_new, k, h_adaptive_ids, mode, temperature, top_p, top_k, seed,
-                         nullptr, 0, h_out, h_stats);
+    return generate_impl(c, batch, h_prompts, P, max_new, k, 1, h_adaptive_ids, mode, temperature, top_p, top_k,
+                         seed, nullptr, 0, h_out, h_stats);
+}
+
+int sdsat_generate_tree(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t P, int32_t max_new,
+                        int32_t k, int32_t width, const int32_t* h_adaptive_ids, int32_t mode, float temperature,
+                        float top_p, int32_t top_k, uint64_t seed, int32_t* h_out, sdsat_stats* h_stats) {
+    return generate_impl(c, batch, h_prompts, P, max_new, k, width, h_adaptive_ids, mode, temperature, top_p, top_k,
+                         seed, nullptr, 0, h_out, h_stats);
 }
 
 int sdsat_generate_forced(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t P, int32_t max_new,
@@ -794,8 +837,8 @@ int sdsat_generate_forced(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts,
     if (!h_ref || ref_len < 1) return fail(c, SDSAT_EINVAL, "h_ref is NULL or ref_len < 1");
     for (long i = 0; i < (long)batch * ref_len; ++i)
         if (h_ref[i] < 0 || h_ref[i] >= c->D.V + c->D.A) return fail(c, SDSAT_EINVAL, "reference id out of range");
-    return generate_impl(c, batch, h_prompts, P, max_new, k, h_adaptive_ids, mode, temperature, top_p, top_k, seed,
-                         h_ref, ref_len, h_out, h_stats);
+    return generate_impl(c, batch, h_prompts, P, max_new, k, 1, h_adaptive_ids, mode, temperature, top_p, top_k,
+                         seed, h_ref, ref_len, h_out, h_stats);
 }
 
 int sdsat_kv_write(sdsat_ctx* c, int32_t layer, int32_t batch, int32_t n, const float* d_k, const float* d_v,

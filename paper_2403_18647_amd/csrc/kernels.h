@@ -140,9 +140,19 @@ hipError_t launch_swiglu_rows(int dtype, const float* g, const float* up, int ld
 // ---------------------------------------------------------------- verify
 hipError_t launch_verify_greedy(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,
                                 int* tokens_out, int* n_accept, int* counter, hipStream_t s);
+// row_depth (optional, a draft tree; drafts must be NULL): every row is sampled with the uniform of
+// position pos0[b] + row_depth[b*q + row]
 hipError_t launch_verify_nucleus(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,
                                  float temperature, float top_p, int top_k, uint64_t seed, const int* pos0,
-                                 int* tokens_out, int* n_accept, int* counter, hipStream_t s);
+                                 int* tokens_out, int* n_accept, int* counter, hipStream_t s,
+                                 const int* row_depth = nullptr);
+
+// draft tree of width w over draft step 1's rows (k adaptive rows): q2 = 1 + k*w block rows
+constexpr int kMaxTreeWidth = 8;
+hipError_t launch_tree_build(const float* logits1, int B, int q1, int V, const int* out1, int k, int w, int q2,
+                             int* tok2, uint64_t* mask2, int* depth2, hipStream_t s);
+hipError_t launch_tree_walk(int B, int q2, int k, int w, const int* tok2, const int* targets, const int* active,
+                            int* emitted, int* n_accept, int* rows, int* pending, int* n_commit, hipStream_t s);
 
 // ---------------------------------------------------------------- decode-loop helpers
 hipError_t launch_build_draft1(const int* pending, const int* adaptive, int B, int k, int* tokens, hipStream_t s);

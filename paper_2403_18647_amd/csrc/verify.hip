@@ -382,29 +382,159 @@ __device__ int sample_row(const float* row, int V, double T, double p, int top_k
 __global__ void __launch_bounds__(kNT) verify_nucleus_kernel(const float* logits, int q, int V, const int* drafts,
                                                              int drafts_ld, float temperature, float top_p,
                                                              int top_k, uint64_t seed, const int* pos0,
-                                                             int* tokens_out, int* n_accept, int* counter) {
+                                                             const int* row_depth, int* tokens_out, int* n_accept,
+                                                             int* counter) {
     __shared__ float s_val[kWaves];
     __shared__ int s_idx[kWaves];
     const int row = blockIdx.x, b = row / q, j = row % q;
     const float* lg = logits + (size_t)row * V;
-    const bool sample = temperature > 0.f && (drafts != nullptr || j == 0);
+    // row_depth (a draft tree): every row is sampled, keyed by the position of its node's next token
+    const bool sample = temperature > 0.f && (drafts != nullptr || row_depth != nullptr || j == 0);
     int t;
     if (sample) {
-        const double u = keyed_uniform(seed, b, pos0[b] + j);
+        const double u = keyed_uniform(seed, b, pos0[b] + (row_depth ? row_depth[row] : j));
         t = sample_row(lg, V, (double)temperature, (double)top_p, top_k, u);
     } else {
         t = block_argmax<kNT>(lg, V, s_val, s_idx);
     }
     if (threadIdx.x == 0) tokens_out[row] = t;
-    finish_sequence(b, q, drafts, drafts_ld, tokens_out, n_accept, counter);
+    if (drafts || n_accept) finish_sequence(b, q, drafts, drafts_ld, tokens_out, n_accept, counter);
 }
 
 hipError_t launch_verify_nucleus(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,
                                  float temperature, float top_p, int top_k, uint64_t seed, const int* pos0,
-                                 int* tokens_out, int* n_accept, int* counter, hipStream_t s) {
-    if (V > kNT * kCPT) return hipErrorInvalidValue;
+                                 int* tokens_out, int* n_accept, int* counter, hipStream_t s, const int* row_depth) {
+    if (V > kNT * kCPT || (row_depth && drafts)) return hipErrorInvalidValue;
     hipLaunchKernelGGL(verify_nucleus_kernel, dim3(B * q), dim3(kNT), 0, s, logits, q, V, drafts, drafts_ld,
-                       temperature, top_p, top_k, seed, pos0, tokens_out, n_accept, counter);
+                       temperature, top_p, top_k, seed, pos0, row_depth, tokens_out, n_accept, counter);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- draft tree (Section 2.1.2)
+// Tree of width w over draft step 1's adaptive rows: depth j holds the w
+// largest logits of row j (ties to the lower id).  Block rows: 0 the root t1,
+// 1..k the chain of each depth's first candidate (parent: the row above),
+// then depth by depth the other candidates, leaves under the chain node one
+// level up (row k + 1 + (j - 1)(w - 1) + i - 1 for candidate i of depth j).
+
+// arg-max of a row over the ids not in excl[0..n_excl) (ties to the lower id)
+template <int NT>
+__device__ int block_argmax_excl(const float* row, int V, const int* excl, int n_excl, float* s_val, int* s_idx) {
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int i = threadIdx.x; i < V; i += NT) {
+        bool skip = false;
+        for (int e = 0; e < n_excl; ++e) skip |= excl[e] == i;
+        if (skip) continue;
+        const float v = row[i];
+        if (better(v, i, bv, bi)) { bv = v; bi = i; }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float ov = __shfl_xor(bv, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (lane == 0) { s_val[wave] = bv; s_idx[wave] = bi; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < NT / 64; ++w)
+            if (better(s_val[w], s_idx[w], bv, bi)) { bv = s_val[w]; bi = s_idx[w]; }
+        s_idx[0] = bi == 0x7fffffff ? 0 : bi;
+    }
+    __syncthreads();
+    const int r = s_idx[0];
+    __syncthreads();
+    return r;
+}
+
+// One workgroup per (sequence, depth j): the depth's candidates, their block
+// rows' tokens, ancestor masks (bit r: block row r is visible) and depths;
+// depth 1 also writes the root.
+__global__ void __launch_bounds__(kNT) tree_build_kernel(const float* logits1, int q1, int V, const int* out1, int k,
+                                                         int w, int q2, int* tok2, uint64_t* mask2, int* depth2) {
+    __shared__ float s_val[kWaves];
+    __shared__ int s_idx[kWaves];
+    __shared__ int s_ch[kMaxTreeWidth];
+    const int b = blockIdx.x, j = blockIdx.y + 1;
+    const float* row = logits1 + ((size_t)b * q1 + j) * V;
+    for (int p = 0; p < w; ++p) {
+        const int t = block_argmax_excl<kNT>(row, V, s_ch, p, s_val, s_idx);
+        if (threadIdx.x == 0) s_ch[p] = t;
+        __syncthreads();
+    }
+    if (threadIdx.x != 0) return;
+    int* tk = tok2 + (size_t)b * q2;
+    uint64_t* mk = mask2 + (size_t)b * q2;
+    int* dp = depth2 + (size_t)b * q2;
+    const uint64_t up = (1ull << j) - 1;   // the root and chain rows 1..j-1
+    tk[j] = s_ch[0];
+    mk[j] = up | (1ull << j);
+    dp[j] = j;
+    for (int i = 1; i < w; ++i) {
+        const int r = k + 1 + (j - 1) * (w - 1) + (i - 1);
+        tk[r] = s_ch[i];
+        mk[r] = up | (1ull << r);
+        dp[r] = j;
+    }
+    if (j == 1) {
+        tk[0] = out1[(size_t)b * q1];
+        mk[0] = 1ull;
+        dp[0] = 0;
+    }
+}
+
+// Longest confirmed branch, one thread per sequence: from the root, emit the
+// target's token at the node (targets[node]) and descend into the child that
+// carries it (chain child first, then the leaves in row order), else stop.
+// Writes the emitted tokens, m, the branch's block rows (for the gathered
+// commit), the next pending token and the rows to commit (0 when inactive).
+__global__ void tree_walk_kernel(int B, int q2, int k, int w, const int* tok2, const int* targets, const int* active,
+                                 int* emitted, int* n_accept, int* rows, int* pending, int* n_commit) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    const int* tk = tok2 + (size_t)b * q2;
+    const int* tg = targets + (size_t)b * q2;
+    int node = 0, m = 0;
+    rows[(size_t)b * q2] = 0;
+    for (;;) {
+        const int t = tg[node];
+        emitted[(size_t)b * q2 + m] = t;
+        int nxt = -1;
+        if (node < k) {   // a chain node (the root is depth 0); leaves have no children
+            if (tk[node + 1] == t) {
+                nxt = node + 1;
+            } else {
+                for (int i = 0; i < w - 1; ++i) {
+                    const int r = k + 1 + node * (w - 1) + i;
+                    if (tk[r] == t) { nxt = r; break; }
+                }
+            }
+        }
+        if (nxt < 0) break;
+        ++m;
+        rows[(size_t)b * q2 + m] = nxt;
+        node = nxt;
+    }
+    n_accept[b] = m;
+    const bool act = active[b] != 0;
+    if (act) pending[b] = tg[node];
+    n_commit[b] = act ? m + 1 : 0;
+}
+
+hipError_t launch_tree_build(const float* logits1, int B, int q1, int V, const int* out1, int k, int w, int q2,
+                             int* tok2, uint64_t* mask2, int* depth2, hipStream_t s) {
+    if (k < 1 || w < 1 || w > kMaxTreeWidth || q2 != 1 + k * w || q2 > 64) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(tree_build_kernel, dim3(B, k), dim3(kNT), 0, s, logits1, q1, V, out1, k, w, q2, tok2, mask2,
+                       depth2);
+    return hipGetLastError();
+}
+
+hipError_t launch_tree_walk(int B, int q2, int k, int w, const int* tok2, const int* targets, const int* active,
+                            int* emitted, int* n_accept, int* rows, int* pending, int* n_commit, hipStream_t s) {
+    hipLaunchKernelGGL(tree_walk_kernel, dim3((B + 63) / 64), dim3(64), 0, s, B, q2, k, w, tok2, targets, active,
+                       emitted, n_accept, rows, pending, n_commit);
     return hipGetLastError();
 }
 

@@ -219,6 +219,62 @@ def test_generate_nucleus_matches_ar_nucleus(T, p, top_k):
     ctx.close()
 
 
+def _small_vocab_tree():
+    """A decoder with a 16-token vocabulary and large weights: draft step 1's top candidates often hold
+    the target's next tokens, so both the chain and the leaves of a draft tree get accepted."""
+    sh = synth.small_shape(n_layers=2, d_model=128, n_heads=2, head_dim=64, d_ffn=256, vocab=16, n_adaptive=5,
+                           rope_base=1e4, dtype="fp32")
+    return synth.Workload("tree", sh, seed=23, batch=2, k=4, prompt_len=12, max_new=40, weight_std=0.3)
+
+
+@pytest.mark.parametrize("mode,width", [("greedy", 3), ("nucleus", 2), ("nucleus", 4)])
+def test_tree_generate_matches_oracle_tree_and_ar(mode, width):
+    """Section 2.1.2 draft tree: the GPU tree loop emits the oracle tree loop's tokens (nucleus: up to the
+    first draw within 2e-6 of a decision boundary), which are the AR tokens, and drafts get accepted."""
+    wl = _small_vocab_tree()
+    sh, k = wl.shape, wl.k
+    q2 = 1 + k * width
+    ctx = helpers.make_ctx(wl, max_batch=2, max_ctx=wl.prompt_len + wl.max_new + 2 * q2 + 16, max_block=q2)
+    prompts = synth.prompts(wl)
+    ad = synth.adaptive_ids(sh, k)
+    nucleus = mode == "nucleus"
+    T, p, seed = (0.9 if nucleus else 0.0), 0.9, 31
+    kw = dict(mode=B.MODE_NUCLEUS if nucleus else B.MODE_GREEDY, temperature=T, top_p=p, top_k=0, seed=seed)
+    out, st = B.sdsat_generate(ctx.handle, prompts, wl.max_new, k, ad, width=width, **kw)
+    ar, _ = B.sdsat_generate(ctx.handle, prompts, wl.max_new, 0, ad, **kw)
+    W = helpers.oracle_weights(wl)
+    accepted_leaf = False
+    for b in range(2):
+        tr = D.Trace()
+        ref, ms = D.generate_sdsat_tree(sh, W, prompts[b], k, width, wl.max_new, ad, mode=mode, temperature=T,
+                                        top_p=p, seed=seed, b=b, trace=tr)
+        n = next((i for i, mg in enumerate(tr.margins) if mg < 2e-6), len(ref))
+        assert n >= 10
+        got = [int(t) for t in out[b]]
+        assert got[:n] == ref[:n], b
+        assert got[:n] == [int(t) for t in ar[b]][:n], b
+        pos = 0
+        for path in tr.paths:   # a branch ending in a leaf, accepted inside the compared tokens
+            pos += 1 + len(path)
+            accepted_leaf |= any(r > k for r in path) and pos <= n
+    assert accepted_leaf
+    assert st["accepted"] > 0 and st["blocks"] == 2 * st["loops"]
+    ctx.close()
+
+
+def test_tree_of_width_one_is_the_chain_on_gpu():
+    wl = _small_vocab_tree()
+    sh, k = wl.shape, wl.k
+    ctx = helpers.make_ctx(wl, max_batch=2, max_ctx=wl.prompt_len + wl.max_new + 32, max_block=k + 1)
+    prompts = synth.prompts(wl)
+    ad = synth.adaptive_ids(sh, k)
+    kw = dict(mode=B.MODE_NUCLEUS, temperature=0.9, top_p=0.9, top_k=0, seed=3)
+    a, sa = B.sdsat_generate(ctx.handle, prompts, wl.max_new, k, ad, **kw)
+    c, sc = B.sdsat_generate(ctx.handle, prompts, wl.max_new, k, ad, width=1, **kw)
+    assert np.array_equal(a, c) and sa["accept_hist"] == sc["accept_hist"]
+    ctx.close()
+
+
 def test_out_of_range_token_reports_edata():
     wl = synth.workload("tiny")
     ctx = helpers.make_ctx(wl, max_batch=1, max_ctx=64, max_block=6)
