@@ -252,6 +252,7 @@ def main():
     ap.add_argument("--no-ar-baseline", action="store_true")
     ap.add_argument("--no-forced", action="store_true", help="skip the full-acceptance (injected drafts) run")
     ap.add_argument("--ksweep", action="store_true", help="block and loop time for k = 0..13 (prints its own line)")
+    ap.add_argument("--tree", type=int, default=1, help="draft tree width of draft step 2 (1: the chain)")
     ap.add_argument("--calibrate-copy-mb", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (a plain copy kernel of known "
                          "size, for scaling hardware traffic counters)")
@@ -302,7 +303,7 @@ def main():
     def step():
         return B.sdsat_generate(ctx.handle, prompts, wl.max_new, wl.k, ad, mode=mode,
                                 temperature=wl.temperature if mode else 0.0, top_p=wl.top_p, top_k=wl.top_k,
-                                seed=wl.seed)
+                                seed=wl.seed, width=args.tree)
 
     for i in range(args.warmup):
         out, st = step()
@@ -358,7 +359,7 @@ def main():
     # full acceptance, measured (synthetic): every draft step 2 takes its drafts from the autoregressive
     # continuation of the same prompts, which verification accepts in full (m = k, k + 2 tokens per loop)
     forced = None
-    if not args.no_forced and wl.k > 0:
+    if not args.no_forced and wl.k > 0 and args.tree == 1:
         kw = dict(mode=mode, temperature=wl.temperature if mode else 0.0, top_p=wl.top_p, top_k=wl.top_k,
                   seed=wl.seed)
         ref, _ = B.sdsat_generate(ctx.handle, prompts, wl.max_new + wl.k + 1, 0, ad, **kw)
@@ -397,7 +398,8 @@ def main():
         "data": "synthetic (random-init weights N(0,0.02) seed %d, uniform random prompt ids)" % wl.seed,
         "config": {"workload": f"{wl.name}: CodeLlama-7B-shaped decoder (32 layers, d 4096, 32 heads x 128, "
                                f"FFN 11008, vocab 32016+5), bf16, batch {wl.batch}, prompt {wl.prompt_len}, "
-                               f"{wl.max_new} new tokens, greedy SDSAT k={wl.k}",
+                               f"{wl.max_new} new tokens, {wl.mode} SDSAT k={wl.k}"
+                               + (f", draft tree width {args.tree}" if args.tree > 1 else ""),
                    "global_batch": wl.batch, "seq_len": wl.prompt_len + wl.max_new, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": "gate/up GEMM + SwiGLU (M=%d)" % M_rows,
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -139,3 +139,23 @@ def test_7b_forced_drafts_from_ar_output_accept_every_draft():
     assert st["accept_hist"][wl.k] == st["loops"] == wl.max_new // (wl.k + 2)
     print(f"7b forced drafts: {st['loops']} loops, accept hist {st['accept_hist']}")
     ctx.close()
+
+
+def test_7b_tree_nucleus_emits_ar_nucleus_tokens():
+    """Whole 7B model, draft tree of width 2 (11 tree rows with ancestor masks): the tree loop emits the
+    AR nucleus tokens (position-keyed uniforms)."""
+    wl = synth.workload("7b", max_new=24)
+    sh = wl.shape
+    width = 2
+    q2 = 1 + wl.k * width
+    weights = synth.device_weights(wl, "cuda")
+    cfg = B.make_config(sh, max_batch=1, max_ctx=wl.prompt_len + wl.max_new + 2 * q2 + 32, max_block=512)
+    ctx = B.Context(cfg, weights)
+    prompts = synth.prompts(wl)
+    ad = synth.adaptive_ids(sh, wl.k)
+    kw = dict(mode=B.MODE_NUCLEUS, temperature=0.8, top_p=0.95, top_k=0, seed=9)
+    tr, st = B.sdsat_generate(ctx.handle, prompts, wl.max_new, wl.k, ad, width=width, **kw)
+    ar, _ = B.sdsat_generate(ctx.handle, prompts, wl.max_new, 0, ad, **kw)
+    assert [int(t) for t in tr[0]] == [int(t) for t in ar[0]]
+    assert st["blocks"] == 2 * st["loops"]
+    ctx.close()
