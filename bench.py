@@ -31,6 +31,10 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def model_name(sh):
+    return {4096: "CodeLlama-7B", 5120: "CodeLlama-13B"}.get(sh.d_model, "small")
+
+
 def block_bytes(sh, B, q, ctx_len):
     """Algorithmic HBM bytes of one block forward: every weight once, the KV
     cache read, the block's K/V written, the embedding rows and the logits."""
@@ -396,9 +400,12 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if sh.dtype == "bf16" else "fp32",
         "data": "synthetic (random-init weights N(0,0.02) seed %d, uniform random prompt ids)" % wl.seed,
-        "config": {"workload": f"{wl.name}: CodeLlama-7B-shaped decoder (32 layers, d 4096, 32 heads x 128, "
-                               f"FFN 11008, vocab 32016+5), bf16, batch {wl.batch}, prompt {wl.prompt_len}, "
-                               f"{wl.max_new} new tokens, {wl.mode} SDSAT k={wl.k}"
+        "config": {"workload": f"{wl.name}: {model_name(sh)}-shaped decoder ({sh.n_layers} layers, d {sh.d_model}, "
+                               f"{sh.n_heads} heads x {sh.head_dim}, FFN {sh.d_ffn}, vocab {sh.vocab}+{sh.n_adaptive}), "
+                               f"{sh.dtype}, batch {wl.batch}, prompt {wl.prompt_len}, {wl.max_new} new tokens, "
+                               f"{wl.mode} SDSAT k={wl.k}"
+                               + (f" (T {wl.temperature}, top-p {wl.top_p}, top-k {wl.top_k or 'off'})"
+                                  if wl.mode == "nucleus" else "")
                                + (f", draft tree width {args.tree}" if args.tree > 1 else ""),
                    "global_batch": wl.batch, "seq_len": wl.prompt_len + wl.max_new, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": "gate/up GEMM + SwiGLU (M=%d)" % M_rows,

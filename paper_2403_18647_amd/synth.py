@@ -76,6 +76,12 @@ WORKLOADS = {
     # 7B shape, batch 4, nucleus top-p 0.95 T 0.8, k=5, prompts 1024, 256 new each
     "7b_bs4_nucleus": Workload("7b_bs4_nucleus", LLAMA7B, seed=3, batch=4, k=5, prompt_len=1024,
                                max_new=256, mode="nucleus", temperature=0.8, top_p=0.95),
+    # 7B shape, batch 1, the nucleus settings of the paper's speed comparison (Section 3.4.2, Table 4):
+    # top-k 10, top-p 0.95, temperature 0.2 or 1, k=5, prompt 512, 256 new tokens
+    "7b_topk10_T0.2": Workload("7b_topk10_T0.2", LLAMA7B, seed=5, batch=1, k=5, prompt_len=512, max_new=256,
+                               mode="nucleus", temperature=0.2, top_p=0.95, top_k=10),
+    "7b_topk10_T1": Workload("7b_topk10_T1", LLAMA7B, seed=6, batch=1, k=5, prompt_len=512, max_new=256,
+                             mode="nucleus", temperature=1.0, top_p=0.95, top_k=10),
 }
 
 

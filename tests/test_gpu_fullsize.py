@@ -159,3 +159,27 @@ def test_7b_tree_nucleus_emits_ar_nucleus_tokens():
     assert [int(t) for t in tr[0]] == [int(t) for t in ar[0]]
     assert st["blocks"] == 2 * st["loops"]
     ctx.close()
+
+
+@pytest.mark.parametrize("name", ["7b_topk10_T0.2", "7b_topk10_T1"])
+def test_7b_topk10_nucleus_chain_and_tree_emit_ar_tokens(name):
+    """Whole 7B model at the paper's nucleus settings (top-k 10, top-p 0.95, T 0.2 or 1): the chain loop
+    and a width-2 draft tree both emit the autoregressive nucleus tokens (position-keyed uniforms)."""
+    wl = synth.workload(name, max_new=24)
+    sh = wl.shape
+    q2 = 1 + wl.k * 2
+    print(f"{name}: T={wl.temperature} top_p={wl.top_p} top_k={wl.top_k}", flush=True)
+    weights = synth.device_weights(wl, "cuda")
+    cfg = B.make_config(sh, max_batch=1, max_ctx=wl.prompt_len + wl.max_new + 2 * q2 + 32, max_block=512)
+    ctx = B.Context(cfg, weights)
+    prompts = synth.prompts(wl)
+    ad = synth.adaptive_ids(sh, wl.k)
+    kw = dict(mode=B.MODE_NUCLEUS, temperature=wl.temperature, top_p=wl.top_p, top_k=wl.top_k, seed=wl.seed)
+    ar, _ = B.sdsat_generate(ctx.handle, prompts, wl.max_new, 0, ad, **kw)
+    ch, st = B.sdsat_generate(ctx.handle, prompts, wl.max_new, wl.k, ad, **kw)
+    tr, st2 = B.sdsat_generate(ctx.handle, prompts, wl.max_new, wl.k, ad, width=2, **kw)
+    ar = [int(t) for t in ar[0]]
+    assert [int(t) for t in ch[0]] == ar
+    assert [int(t) for t in tr[0]] == ar
+    assert st["blocks"] == 2 * st["loops"] and st2["blocks"] == 2 * st2["loops"]
+    ctx.close()

@@ -197,7 +197,7 @@ def test_generate_bf16_batch_ragged_greedy():
     ctx.close()
 
 
-@pytest.mark.parametrize("T,p,top_k", [(0.8, 0.95, 0), (1.0, 0.9, 10)])
+@pytest.mark.parametrize("T,p,top_k", [(0.8, 0.95, 0), (1.0, 0.9, 10), (0.2, 0.95, 10), (1.0, 0.95, 10)])
 def test_generate_nucleus_matches_ar_nucleus(T, p, top_k):
     wl = synth.workload("tiny", max_new=40, weight_std=0.08, batch=2)
     sh = wl.shape
@@ -227,8 +227,9 @@ def _small_vocab_tree():
     return synth.Workload("tree", sh, seed=23, batch=2, k=4, prompt_len=12, max_new=40, weight_std=0.3)
 
 
-@pytest.mark.parametrize("mode,width", [("greedy", 3), ("nucleus", 2), ("nucleus", 4)])
-def test_tree_generate_matches_oracle_tree_and_ar(mode, width):
+@pytest.mark.parametrize("mode,width,T,top_k", [("greedy", 3, 0.0, 0), ("nucleus", 2, 0.9, 0), ("nucleus", 4, 0.9, 0),
+                                                ("nucleus", 2, 0.2, 10), ("nucleus", 3, 1.0, 10)])
+def test_tree_generate_matches_oracle_tree_and_ar(mode, width, T, top_k):
     """Section 2.1.2 draft tree: the GPU tree loop emits the oracle tree loop's tokens (nucleus: up to the
     first draw within 2e-6 of a decision boundary), which are the AR tokens, and drafts get accepted."""
     wl = _small_vocab_tree()
@@ -238,8 +239,8 @@ def test_tree_generate_matches_oracle_tree_and_ar(mode, width):
     prompts = synth.prompts(wl)
     ad = synth.adaptive_ids(sh, k)
     nucleus = mode == "nucleus"
-    T, p, seed = (0.9 if nucleus else 0.0), 0.9, 31
-    kw = dict(mode=B.MODE_NUCLEUS if nucleus else B.MODE_GREEDY, temperature=T, top_p=p, top_k=0, seed=seed)
+    p, seed = (0.95 if top_k else 0.9), 31
+    kw = dict(mode=B.MODE_NUCLEUS if nucleus else B.MODE_GREEDY, temperature=T, top_p=p, top_k=top_k, seed=seed)
     out, st = B.sdsat_generate(ctx.handle, prompts, wl.max_new, k, ad, width=width, **kw)
     ar, _ = B.sdsat_generate(ctx.handle, prompts, wl.max_new, 0, ad, **kw)
     W = helpers.oracle_weights(wl)
@@ -247,7 +248,7 @@ def test_tree_generate_matches_oracle_tree_and_ar(mode, width):
     for b in range(2):
         tr = D.Trace()
         ref, ms = D.generate_sdsat_tree(sh, W, prompts[b], k, width, wl.max_new, ad, mode=mode, temperature=T,
-                                        top_p=p, seed=seed, b=b, trace=tr)
+                                        top_p=p, top_k=top_k, seed=seed, b=b, trace=tr)
         n = next((i for i, mg in enumerate(tr.margins) if mg < 2e-6), len(ref))
         assert n >= 10
         got = [int(t) for t in out[b]]
