@@ -10,10 +10,12 @@
 // lower ids) and the top-p threshold are found by radix descent over the
 // order-preserving 32-bit keys of the float logits (4 bits per pass, 8
 // passes): the threshold is the largest key K with S(K) = sum of e^(z - zmax)
-// over kept ids with key >= K at least p * E.  The token is the smallest id of
-// the nucleus whose ascending-id cumulative mass exceeds u * S(K*), with the
-// cumulative sums formed by a block-wide prefix scan in id order.  All sums
-// use a fixed reduction order, so results are reproducible run to run.
+// over kept ids with key >= K at least p * E.  Each pass sums its 16 digits
+// through per-thread columns in LDS (one writer per word) and a fixed-order
+// reduction.  The token is the smallest id of the nucleus whose ascending-id
+// cumulative mass exceeds u * S(K*), with the cumulative sums formed by a
+// block-wide prefix scan in id order.  All sums use a fixed reduction order,
+// so results are reproducible run to run.
 #include "device.h"
 #include "kernels.h"
 
@@ -113,14 +115,31 @@ hipError_t launch_verify_greedy(const float* logits, int B, int q, int V, const 
 }
 
 // ---------------------------------------------------------------- nucleus
-static constexpr int kNT = 1024;    // threads per row
-static constexpr int kCPT = 32;     // ids per thread (contiguous): V <= 32768
+// 1024 threads x 32 contiguous ids (V <= 32768); each thread keeps its ids' keys and float64
+// weights in registers and a bit mask (one bit per id) of the kept and nucleus ids
+static constexpr int kNT = 1024;
+static constexpr int kCPT = 32;
+using Bits = uint32_t;
+static_assert(kCPT <= 32, "one mask bit per id");
 static constexpr int kWaves = kNT / 64;
+static constexpr int kBins = 16;    // radix digits of 4 bits
+static_assert(kBins % kWaves == 0, "digit totals: each wave sums kBins / kWaves digits");
+static constexpr int kArgNT = 1024; // threads of the arg-max-only tree kernel
+
+__device__ __forceinline__ double readlane_d(double v, int lane) {
+    const int2 p = __builtin_bit_cast(int2, v);
+    return __builtin_bit_cast(double, make_int2(__builtin_amdgcn_readlane(p.x, lane),
+                                                __builtin_amdgcn_readlane(p.y, lane)));
+}
 
 __device__ __forceinline__ uint32_t order_key(float f) {
     uint32_t u = __float_as_uint(f);
     if (u == 0x80000000u) u = 0u;   // -0 and +0 compare equal
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float key_value(uint32_t k) {
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
 
 // SplitMix64 (Steele, Lea, Flood 2014): output number n of the generator started at `state`
@@ -253,115 +272,137 @@ __device__ float block_max_f(float v, float* s_buf) {
     return s;
 }
 
-__device__ int sample_row(const float* row, int V, double T, double p, int top_k, double u) {
-    __shared__ double s_d[kWaves * 16];
+// Radix descent over the order-preserving keys, 4 bits per pass from the top.
+// Every thread keeps private per-digit sums of its own ids in LDS (column t of
+// hist[digit][thread]), so no atomics are needed and the totals of each digit
+// are formed in a fixed order: wave w sums digit w, lane l over threads l,
+// l + 64, ... in turn, then a butterfly.  Returns the largest key K whose
+// weight sum over kept ids with key >= K reaches `goal` (the lowest key of the
+// final range if rounding leaves every sum short of it) and, in *mass, that
+// sum.  w_of(i) gives id id0 + i's weight (0 for ids outside the kept set).
+template <typename WeightFn>
+__device__ __forceinline__ uint32_t radix_threshold(const uint32_t (&keys)[kCPT], Bits kept, WeightFn w_of, double goal,
+                                    double* hist, double* s_tot, double* mass) {
+    const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+    uint32_t prefix = 0;
+    double above = 0.0, at = 0.0;
+#pragma unroll 1
+    for (int shift = 28; shift >= 0; shift -= 4) {
+        const uint32_t hi = shift == 28 ? 0u : 0xFFFFFFFFu << (shift + 4);
+#pragma unroll
+        for (int v = 0; v < kBins; ++v) hist[v * kNT + t] = 0.0;
+#pragma unroll
+        for (int i = 0; i < kCPT; ++i) {
+            if (!((kept >> i) & 1u)) continue;
+            const uint32_t key = keys[i];
+            if ((key & hi) != (prefix & hi)) continue;
+            // no-return LDS add on the thread's own column: no round trip, and the adds to one
+            // word land in program order (one writer), so the sums repeat bit for bit
+            __hip_atomic_fetch_add(&hist[((key >> shift) & 15u) * kNT + t], w_of(i), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int h = 0; h < kBins / kWaves; ++h) {
+            const int bin = wave + h * kWaves;
+            double sum = 0.0;
+#pragma unroll
+            for (int j = 0; j < kNT / 64; ++j) sum += hist[bin * kNT + j * 64 + lane];
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) sum += dshfl_xor(sum, o);
+            if (lane == 0) s_tot[bin] = sum;
+        }
+        __syncthreads();
+        // every wave walks the 16 digit totals from the top (lane v holds digit v's) and takes the
+        // same decision
+        const double mine = s_tot[lane & (kBins - 1)];
+        double acc = above, before = above;
+        int best = 0;
+        for (int v = kBins - 1; v >= 0; --v) {
+            before = acc;
+            acc += readlane_d(mine, v);
+            if (acc >= goal) { best = v; break; }
+        }
+        prefix |= (uint32_t)best << shift;
+        above = before;
+        at = acc;
+    }
+    *mass = at;
+    return prefix;
+}
+
+__device__ __forceinline__ int sample_row(const float* row, int V, double T, double p, int top_k, double u) {
+    __shared__ double s_hist[kBins * kNT];   // 128 KiB: per-thread digit columns
+    __shared__ double s_tot[kBins];          // digit totals (read by every thread after the last pass)
+    __shared__ double s_d[kWaves];
     __shared__ int s_i[kWaves];
     __shared__ float s_f[kWaves];
     const int id0 = threadIdx.x * kCPT;
-    float lv[kCPT];
+    // ids id0 .. id0+31 as order-preserving keys (the float is recovered from the key where needed)
+    uint32_t keys[kCPT];
 #pragma unroll
     for (int i = 0; i < kCPT; i += 4) {
         if (id0 + i + 3 < V && (V & 3) == 0) {
             const float4 v = *reinterpret_cast<const float4*>(row + id0 + i);
-            lv[i] = v.x; lv[i + 1] = v.y; lv[i + 2] = v.z; lv[i + 3] = v.w;
+            keys[i] = order_key(v.x); keys[i + 1] = order_key(v.y);
+            keys[i + 2] = order_key(v.z); keys[i + 3] = order_key(v.w);
         } else {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) lv[i + j] = id0 + i + j < V ? row[id0 + i + j] : -INFINITY;
+            for (int j = 0; j < 4; ++j) keys[i + j] = order_key(id0 + i + j < V ? row[id0 + i + j] : -INFINITY);
         }
     }
-    uint32_t kept = 0;   // bit i: id0+i is kept by top-k
+    Bits kept = 0;   // bit i: id0+i is kept by top-k
 #pragma unroll
     for (int i = 0; i < kCPT; ++i) if (id0 + i < V) kept |= 1u << i;
 
     if (top_k > 0 && top_k < V) {
-        // largest key Kk with count(key >= Kk) >= top_k
-        uint32_t prefix = 0;
-        for (int shift = 28; shift >= 0; shift -= 4) {
-            int cnt[16];
-#pragma unroll
-            for (int v = 0; v < 16; ++v) cnt[v] = 0;
-#pragma unroll
-            for (int i = 0; i < kCPT; ++i) {
-                if (!((kept >> i) & 1u)) continue;
-                const uint32_t key = order_key(lv[i]);
-#pragma unroll
-                for (int v = 0; v < 16; ++v) cnt[v] += key >= (prefix | ((uint32_t)v << shift)) ? 1 : 0;
-            }
-            int best = 0;
-            for (int v = 0; v < 16; ++v) {
-                const int tot = block_sum_i(cnt[v], s_i);
-                if (tot >= top_k) best = v;
-            }
-            prefix |= (uint32_t)best << shift;
-        }
-        const uint32_t Kk = prefix;
+        // largest key Kk with count(key >= Kk) >= top_k (counts are exact in double)
+        double cnt;
+        const uint32_t Kk = radix_threshold(keys, kept, [&](int) { return 1.0; }, (double)top_k, s_hist, s_tot, &cnt);
         int gt = 0, eq = 0;
 #pragma unroll
         for (int i = 0; i < kCPT; ++i) {
             if (!((kept >> i) & 1u)) continue;
-            const uint32_t key = order_key(lv[i]);
-            gt += key > Kk;
-            eq += key == Kk;
+            gt += keys[i] > Kk;
+            eq += keys[i] == Kk;
         }
         const int need = top_k - block_sum_i(gt, s_i);
         int rank = block_exscan_i(eq, s_i);
-        uint32_t nk = 0;
+        Bits nk = 0;
 #pragma unroll
         for (int i = 0; i < kCPT; ++i) {
             if (!((kept >> i) & 1u)) continue;
-            const uint32_t key = order_key(lv[i]);
-            if (key > Kk) nk |= 1u << i;
-            else if (key == Kk) { if (rank < need) nk |= 1u << i; ++rank; }
+            if (keys[i] > Kk) nk |= 1u << i;
+            else if (keys[i] == Kk) { if (rank < need) nk |= 1u << i; ++rank; }
         }
         kept = nk;
     }
 
-    float lmax = -INFINITY;
+    uint32_t kmax = 0;
 #pragma unroll
-    for (int i = 0; i < kCPT; ++i) if ((kept >> i) & 1u) lmax = fmaxf(lmax, lv[i]);
-    lmax = block_max_f(lmax, s_f);
+    for (int i = 0; i < kCPT; ++i) if ((kept >> i) & 1u) kmax = max(kmax, keys[i]);
+    const float lmax = block_max_f(key_value(kmax), s_f);
     const double zmax = (double)lmax / T;
     double e[kCPT];
     double tot[1] = {0.0};
 #pragma unroll
     for (int i = 0; i < kCPT; ++i) {
-        e[i] = ((kept >> i) & 1u) ? exp((double)lv[i] / T - zmax) : 0.0;
+        e[i] = ((kept >> i) & 1u) ? exp((double)key_value(keys[i]) / T - zmax) : 0.0;
         tot[0] += e[i];
     }
     block_sum_d<1>(tot, s_d);
     const double pE = (p < 1.0 ? p : 1.0) * tot[0];
 
-    // top-p threshold key
-    uint32_t prefix = 0;
-    double mass = tot[0];
-    for (int shift = 28; shift >= 0; shift -= 4) {
-        double S[16];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) S[v] = 0.0;
-#pragma unroll
-        for (int i = 0; i < kCPT; ++i) {
-            if (!((kept >> i) & 1u)) continue;
-            const uint32_t key = order_key(lv[i]);
-#pragma unroll
-            for (int v = 0; v < 16; ++v)
-                if (key >= (prefix | ((uint32_t)v << shift))) S[v] += e[i];
-        }
-        block_sum_d<16>(S, s_d);
-        int best = 0;
-        double bm = S[0];
-#pragma unroll
-        for (int v = 1; v < 16; ++v) if (S[v] >= pE) { best = v; bm = S[v]; }
-        prefix |= (uint32_t)best << shift;
-        mass = bm;
-    }
-    const uint32_t Kstar = prefix;
+    // top-p threshold key and the mass of the nucleus
+    double mass;
+    const uint32_t Kstar = radix_threshold(keys, kept, [&](int i) { return e[i]; }, pE, s_hist, s_tot, &mass);
 
     // inverse CDF over the nucleus in ascending id order
     double loc = 0.0;
-    uint32_t inN = 0;
+    Bits inN = 0;
 #pragma unroll
     for (int i = 0; i < kCPT; ++i)
-        if (((kept >> i) & 1u) && order_key(lv[i]) >= Kstar) { inN |= 1u << i; loc += e[i]; }
+        if (((kept >> i) & 1u) && keys[i] >= Kstar) { inN |= 1u << i; loc += e[i]; }
     const double pre = block_exscan_d(loc, s_d);
     const double target = u * mass;
     int cand = 0x7fffffff;
@@ -452,15 +493,15 @@ __device__ int block_argmax_excl(const float* row, int V, const int* excl, int n
 // One workgroup per (sequence, depth j): the depth's candidates, their block
 // rows' tokens, ancestor masks (bit r: block row r is visible) and depths;
 // depth 1 also writes the root.
-__global__ void __launch_bounds__(kNT) tree_build_kernel(const float* logits1, int q1, int V, const int* out1, int k,
+__global__ void __launch_bounds__(kArgNT) tree_build_kernel(const float* logits1, int q1, int V, const int* out1, int k,
                                                          int w, int q2, int* tok2, uint64_t* mask2, int* depth2) {
-    __shared__ float s_val[kWaves];
-    __shared__ int s_idx[kWaves];
+    __shared__ float s_val[kArgNT / 64];
+    __shared__ int s_idx[kArgNT / 64];
     __shared__ int s_ch[kMaxTreeWidth];
     const int b = blockIdx.x, j = blockIdx.y + 1;
     const float* row = logits1 + ((size_t)b * q1 + j) * V;
     for (int p = 0; p < w; ++p) {
-        const int t = block_argmax_excl<kNT>(row, V, s_ch, p, s_val, s_idx);
+        const int t = block_argmax_excl<kArgNT>(row, V, s_ch, p, s_val, s_idx);
         if (threadIdx.x == 0) s_ch[p] = t;
         __syncthreads();
     }
@@ -526,7 +567,7 @@ __global__ void tree_walk_kernel(int B, int q2, int k, int w, const int* tok2, c
 hipError_t launch_tree_build(const float* logits1, int B, int q1, int V, const int* out1, int k, int w, int q2,
                              int* tok2, uint64_t* mask2, int* depth2, hipStream_t s) {
     if (k < 1 || w < 1 || w > kMaxTreeWidth || q2 != 1 + k * w || q2 > 64) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(tree_build_kernel, dim3(B, k), dim3(kNT), 0, s, logits1, q1, V, out1, k, w, q2, tok2, mask2,
+    hipLaunchKernelGGL(tree_build_kernel, dim3(B, k), dim3(kArgNT), 0, s, logits1, q1, V, out1, k, w, q2, tok2, mask2,
                        depth2);
     return hipGetLastError();
 }
