@@ -71,6 +71,30 @@ def profiled_traffic():
         return None
 
 
+def stream_read_peak(B, torch, region_gib=1, regions=4, iters=12):
+    """Achievable HBM read rate on this device: the library's read-only stream kernel over rotating
+    1 GiB regions (4 GiB in all, far beyond the 256 MB memory-side cache), events around each launch,
+    median launch."""
+    n = region_gib << 30
+    buf = torch.empty(regions * n, dtype=torch.uint8, device="cuda:0")
+    st = torch.cuda.current_stream()
+    for i in range(2):
+        B.sdsat_stream_read(buf[i * n:(i + 1) * n])
+    torch.cuda.synchronize()
+    times = []
+    for i in range(iters):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        B.sdsat_stream_read(buf[(i % regions) * n:(i % regions + 1) * n])
+        e1.record(st)
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    del buf
+    torch.cuda.synchronize()
+    ms = sorted(times)[len(times) // 2]
+    return n / (ms / 1e3) / 1e9
+
+
 def cpu_baseline(wl, m_bar, n_layers_sample=2, n_blocks=3):
     """The float64 oracle on the host cores, on a bounded sample of the workload:
     the 7B model truncated to its first `n_layers_sample` layers (same tensors as
@@ -339,8 +363,9 @@ def main():
     # block-forward bandwidth: HIP events around every decode block (draft and verify) of one more step
     B.sdsat_profile_kernel(ctx.handle, "block")
     _, st2 = step()
-    blk_ms, blk_n = B.sdsat_kernel_time(ctx.handle)
+    blk_samples = B.sdsat_kernel_samples(ctx.handle)
     B.sdsat_profile_kernel(ctx.handle, "off")
+    blk_ms, blk_n = sum(blk_samples), len(blk_samples)
     per_block_ms = blk_ms / max(1, blk_n)
     avg_ctx = wl.prompt_len - 1 + wl.max_new / 2.0      # mean committed length over the decode
     bblk = block_bytes(sh, wl.batch, q, avg_ctx)
@@ -381,6 +406,9 @@ def main():
                   "speedup_vs_ar": round(f_tps / ar["tokens_per_s"], 4) if ar else None,
                   "note": "synthetic: drafts injected from the autoregressive output (sdsat_generate_forced); "
                           "measures the loop at full acceptance on random weights"}
+
+    stream_gbs = stream_read_peak(B, torch)
+    log(f"stream read: {stream_gbs:.0f} GB/s")
 
     M_rows = wl.batch * q
     gu_avg_s = gu_ms / max(1, gu_n) / 1e3
@@ -426,11 +454,18 @@ def main():
         "ar_baseline": ar,
         "full_accept": forced,
         "block_forward": {"avg_ms": round(per_block_ms, 4), "blocks": blk_n,
+                          "p50_ms": round(float(np.percentile(blk_samples, 50)), 4) if blk_samples else None,
+                          "p90_ms": round(float(np.percentile(blk_samples, 90)), 4) if blk_samples else None,
                           "algorithmic_bytes": int(bblk), "achieved_GBs": round(blk_gbs, 1),
                           "frac_of_peak": round(blk_gbs / HBM_PEAK_GBS, 4),
+                          "frac_of_stream_read": round(blk_gbs / stream_gbs, 4),
                           "note": "HIP events around each draft/verify block forward (embed..LM head) of one "
                                   "extra step; bytes at the mean decode context"},
+        "stream_read": {"GBs": round(stream_gbs, 1), "frac_of_peak": round(stream_gbs / HBM_PEAK_GBS, 4),
+                        "note": "achievable HBM read rate: sdsat_stream_read (16 KiB per workgroup, 16-byte "
+                                "nontemporal loads) over rotating 1 GiB regions, median of 12 launches"},
     }
+    result["roofline"]["frac_of_stream_read"] = round(achieved / stream_gbs, 4)
     if not args.no_cpu_baseline:
         log("cpu baseline: timing the oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(wl, m_bar)

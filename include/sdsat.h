@@ -250,6 +250,21 @@ int sdsat_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const float* d_
 int sdsat_profile_kernel(sdsat_ctx* ctx, int32_t kind, int32_t period);
 int sdsat_kernel_time(sdsat_ctx* ctx, double* total_ms, int64_t* launches);
 
+/* As sdsat_kernel_time, but returns each timed launch's milliseconds: the
+ * first min(cap, *launches) of them, in launch order, into the caller's host
+ * array h_ms (cap >= 0; h_ms may be NULL when cap is 0).  *launches = the
+ * number of timed launches since the last call; the samples are consumed. */
+int sdsat_kernel_samples(sdsat_ctx* ctx, float* h_ms, int64_t cap, int64_t* launches);
+
+/* Measurement helper, outside the decoding method: streams `bytes` (a
+ * multiple of 16; EINVAL otherwise) from the device buffer d_src through the
+ * read pattern that measured fastest on MI355X (16 KiB contiguous per
+ * workgroup, 16-byte nontemporal loads) and writes nothing, on hip_stream
+ * (NULL = the default stream).  Time it with events on that stream to get
+ * the achievable HBM read rate that the block forward's bandwidth can be set
+ * against.  The buffer stays the caller's; no context is needed. */
+int sdsat_stream_read(const void* d_src, size_t bytes, void* hip_stream);
+
 /* Release the context (not the caller's buffers).  NULL is accepted. */
 int sdsat_destroy(sdsat_ctx* ctx);
 

@@ -65,6 +65,8 @@ _SIGNATURES = {
     "sdsat_linear": ([_I32, _I32, _I32, _I32, _VP, _VP, _VP, _VP, _VP], _I32),
     "sdsat_profile_kernel": ([_VP, _I32, _I32], _I32),
     "sdsat_kernel_time": ([_VP, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64)], _I32),
+    "sdsat_kernel_samples": ([_VP, ctypes.POINTER(ctypes.c_float), _I64, ctypes.POINTER(_I64)], _I32),
+    "sdsat_stream_read": ([_VP, _SZ, _VP], _I32),
     "sdsat_destroy": ([_VP], _I32),
     "sdsat_last_error": ([_VP], ctypes.c_char_p),
 }
@@ -234,6 +236,20 @@ def sdsat_kernel_time(ctx):
     n = ctypes.c_int64(0)
     _check(lib().sdsat_kernel_time(ctx, ctypes.byref(ms), ctypes.byref(n)), ctx)
     return ms.value, n.value
+
+
+def sdsat_kernel_samples(ctx, cap=1 << 16):
+    """Milliseconds of each timed launch since the last call (a list, launch order)."""
+    buf = (ctypes.c_float * cap)()
+    n = ctypes.c_int64(0)
+    _check(lib().sdsat_kernel_samples(ctx, buf, cap, ctypes.byref(n)), ctx)
+    return [buf[i] for i in range(min(cap, n.value))]
+
+
+def sdsat_stream_read(src, nbytes=None, stream=None):
+    """Stream nbytes (default: all) of the device tensor src with the library's read-only kernel."""
+    nbytes = src.numel() * src.element_size() if nbytes is None else nbytes
+    _check(lib().sdsat_stream_read(_ptr(src), nbytes, _stream(stream)))
 
 
 def sdsat_destroy(ctx):

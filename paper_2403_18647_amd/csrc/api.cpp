@@ -932,6 +932,28 @@ int sdsat_kernel_time(sdsat_ctx* c, double* total_ms, int64_t* launches) {
     return SDSAT_OK;
 }
 
+int sdsat_kernel_samples(sdsat_ctx* c, float* h_ms, int64_t cap, int64_t* launches) {
+    if (!c || !launches || (cap > 0 && !h_ms) || cap < 0) return fail(c, SDSAT_EINVAL, "bad argument");
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    int64_t n = 0;
+    for (size_t i = 0; i + 1 < c->ev_used; i += 2, ++n) {
+        float ms = 0.f;
+        HIPCHK(c, hipEventElapsedTime(&ms, c->events[i], c->events[i + 1]));
+        if (n < cap) h_ms[n] = ms;
+    }
+    *launches = n;
+    c->ev_used = 0;
+    return SDSAT_OK;
+}
+
+int sdsat_stream_read(const void* d_src, size_t bytes, void* hip_stream) {
+    if (!d_src && bytes) return fail(nullptr, SDSAT_EINVAL, "d_src is NULL");
+    if (bytes % 16) return fail(nullptr, SDSAT_EINVAL, "bytes must be a multiple of 16");
+    const hipError_t e = launch_stream_read(d_src, bytes, static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return fail(nullptr, SDSAT_EDEVICE, std::string("stream read: ") + hipGetErrorString(e));
+    return SDSAT_OK;
+}
+
 int sdsat_destroy(sdsat_ctx* c) {
     if (!c) return SDSAT_OK;
     (void)hipStreamSynchronize(c->stream);

@@ -119,6 +119,8 @@ hipError_t launch_commit_gather(int dtype, void* kc, void* vc, size_t layer_stri
                                 const int* rows, int q, int* err, hipStream_t s);
 hipError_t launch_set_len(int* cache_len, int B, const int* vals_or_null, int value, hipStream_t s);
 hipError_t launch_fill_i32(int* p, size_t n, int value, hipStream_t s);
+// reads `bytes` (a multiple of 16) from src and writes nothing: the device's achievable read rate
+hipError_t launch_stream_read(const void* src, size_t bytes, hipStream_t s);
 // rotary table [S][half][2]: cos and sin of the angle pos * inv_freq[i], formed in double, rounded to float
 hipError_t launch_rope_table(const double* inv_freq, int S, int half, float* rope, hipStream_t s);
 

@@ -234,6 +234,32 @@ __global__ void rope_table_kernel(const double* inv_freq, int S, int half, float
     rope[2 * i + 1] = (float)sd;
 }
 
+// Read-only stream for measuring the device's achievable HBM read rate: workgroup g reads bytes
+// [16 KiB g, 16 KiB (g + 1)), its four waves interleaved 1 KiB at a time with all four of a wave's
+// 16-byte nontemporal loads in flight (many small workgroups measured fastest on MI355X).
+__global__ void __launch_bounds__(256) stream_read_kernel(const u32x4_t* __restrict__ src, size_t n16) {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const size_t base = (size_t)blockIdx.x * 1024 + lane;
+    u32x4_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const size_t i = base + (size_t)(wave + 4 * u) * 64;
+        v[u] = i < n16 ? __builtin_nontemporal_load(src + i) : u32x4_t{0, 0, 0, 0};
+    }
+    uint32_t acc = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc ^= v[u].x ^ v[u].w;
+    asm volatile("" ::"v"(acc));   // keeps the loads; nothing is written
+}
+
+hipError_t launch_stream_read(const void* src, size_t bytes, hipStream_t s) {
+    const size_t n16 = bytes / 16;
+    if (n16 == 0) return hipSuccess;
+    hipLaunchKernelGGL(stream_read_kernel, dim3((unsigned)((n16 + 1023) / 1024)), dim3(256), 0, s,
+                       static_cast<const u32x4_t*>(src), n16);
+    return hipGetLastError();
+}
+
 hipError_t launch_rope_table(const double* inv_freq, int S, int half, float* rope, hipStream_t s) {
     const size_t n = (size_t)S * half;
     if (n == 0) return hipSuccess;

@@ -71,3 +71,12 @@ def test_null_context_is_rejected_without_touching_the_gpu():
     assert L.sdsat_forward_block(None, 1, 1, None, None, None) == -1
     assert L.sdsat_destroy(None) == 0
     assert b"ctx" in L.sdsat_last_error(None)
+
+
+def test_measurement_helpers_reject_bad_arguments_on_the_host():
+    L = B.lib()
+    n = ctypes.c_int64(0)
+    assert L.sdsat_kernel_samples(None, None, 0, ctypes.byref(n)) == -1
+    assert L.sdsat_stream_read(None, 16, None) == -1            # NULL source with bytes to read
+    assert L.sdsat_stream_read(ctypes.c_void_p(4096), 24, None) == -1   # not a multiple of 16
+    assert b"multiple of 16" in L.sdsat_last_error(None)

@@ -260,3 +260,28 @@ def test_attention_many_heads_single_workgroup_per_head():
                               n_adaptive=2, rope_base=1e6, dtype="bf16")
     wl = synth.Workload("heads32", shape, seed=5, batch=8, k=5, prompt_len=1, max_new=1)
     _attn_case(wl, [300, 0, 31, 64, 129, 5, 250, 77], 6)
+
+
+def test_stream_read_and_kernel_samples():
+    print("stream read (ragged length) and per-launch samples", flush=True)
+    # three whole 16 KiB workgroups plus 48 bytes; the kernel only reads
+    buf = torch.arange(3 * 4096 + 12, dtype=torch.int32, device="cuda")
+    before = buf.clone()
+    B.sdsat_stream_read(buf)
+    B.sdsat_stream_read(buf, 0)
+    torch.cuda.synchronize()
+    assert torch.equal(buf, before)
+    ctx = _tiny_ctx(1, 2, 1024)
+    tok = torch.tensor([3, 7], dtype=torch.int32, device="cuda")
+    lg = torch.empty((2, 1024), dtype=torch.float32, device="cuda")
+    B.sdsat_reset(ctx.handle, 1)
+    B.sdsat_profile_kernel(ctx.handle, "block")
+    for _ in range(3):
+        B.sdsat_forward_block(ctx.handle, 1, 2, tok, None, lg)
+    s = B.sdsat_kernel_samples(ctx.handle)
+    assert len(s) == 3 and all(x > 0 for x in s)
+    B.sdsat_forward_block(ctx.handle, 1, 2, tok, None, lg)
+    ms, n = B.sdsat_kernel_time(ctx.handle)
+    assert n == 1 and ms > 0
+    B.sdsat_profile_kernel(ctx.handle, "off")
+    ctx.close()
