@@ -163,9 +163,10 @@ __device__ __forceinline__ void mma_batch(f32x4_t (&acc)[NTW][MT], const Frag<T>
 
 // Fused epilogue of one reduced tile (run by wave 0).
 // acc[mt][r] = Y[m = 16mt + 4g + r][column c of the tile]
+// gn: EP_RESID's next-RMSNorm gain at this lane's column (requested in the prologue)
 template <typename T, int EP, int MT>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, int tile, const f32x4_t (&acc)[MT],
-                                         const float (&ep_in)[MT][4], int c, int g) {
+                                         const float (&ep_in)[MT][4], float gn, int c, int g) {
     const int M = a.M;
     if (EP == EP_STORE) {
         const int n = tile * 16 + c;
@@ -178,7 +179,6 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int tile, const f32x
             }
     } else if (EP == EP_RESID) {
         const int n = tile * 16 + c;
-        const float gn = n < a.N ? a.gnext[n] : 0.f;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -239,7 +239,8 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int tile, const f32x
                     // rotary position: the row's depth in the block (its ancestors
                     // counted by the tree mask; row index for a chain), at most pos.
                     // cos / sin come from the table (angle formed in double, rounded
-                    // to float).
+                    // to float).  Requesting them in the prologue, once the cache
+                    // lengths are in, measured slower.
                     const int rpos = a.mask ? L + __popcll(a.mask[m]) - 1 : pos;
                     const float2 csn = *reinterpret_cast<const float2*>(a.rope + ((size_t)rpos * half + pi) * 2);
                     const float cs = csn.x, sn = csn.y;
@@ -284,7 +285,7 @@ __global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(Gemm
 
     // RMSNorm partial sums (wave w reduces rows w, w+nw, ...; the first two
     // are requested here, ahead of the weight stream) and wave 0's epilogue
-    // inputs (residual values, cache lengths, rotary inverse frequencies).
+    // inputs (residual values and the next RMSNorm's gains, cache lengths).
     constexpr int NSQ = 4;   // ssq partials per lane and row (n_ssq <= 256)
     float sq[2][NSQ];
 #pragma unroll
@@ -298,12 +299,15 @@ __global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(Gemm
     // sequence (the same for every tile)
     constexpr int NEP = EP == EP_RESID ? NTW : 1;
     float ep_in[NEP][MT][4];
+    float gnv[NEP];                 // EP_RESID: the next RMSNorm's gain at each tile's column
 #pragma unroll
-    for (int j = 0; j < NEP; ++j)
+    for (int j = 0; j < NEP; ++j) {
+        gnv[j] = 0.f;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int r = 0; r < 4; ++r) ep_in[j][mt][r] = 0.f;
+    }
     if (wave == 0) {
 #pragma unroll
         for (int j = 0; j < NTW; ++j) {
@@ -319,6 +323,7 @@ __global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(Gemm
                         ep_in[j < NEP ? j : 0][mt][r] = a.resid[(size_t)m * a.ldy + tile * 16 + c];
                     if (EP == EP_QKV && m < M) ep_in[0][mt][r] = __int_as_float(a.cache_len[m / a.q]);
                 }
+            if (EP == EP_RESID && tile * 16 + c < a.N) gnv[j < NEP ? j : 0] = a.gnext[tile * 16 + c];
         }
     }
 
@@ -412,7 +417,7 @@ __global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(Gemm
             for (int w = 1; w < nw; ++w) v += red[(w * MT + mt) * 64 + lane];
             t_acc[mt] = v;
         }
-        epilogue<T, EP, MT>(a, tile0 + j, t_acc, ep_in[j < NEP ? j : 0], c, g);
+        epilogue<T, EP, MT>(a, tile0 + j, t_acc, ep_in[j < NEP ? j : 0], gnv[j < NEP ? j : 0], c, g);
     }
 }
 
