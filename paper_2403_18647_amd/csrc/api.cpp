@@ -48,6 +48,7 @@ struct Dims {
 
 constexpr int kMaxBlock = 4096;   // rows per sequence per block
 constexpr int kSkinnyRows = 64;   // blocks of at most this many rows (B*q) run the skinny GEMM kernels
+constexpr int kPreRoundRows = 16; // past one 16-row tile, normalised GEMM inputs are rounded once (rms_rows)
 
 int make_dims(const sdsat_config* c, Dims* D, std::string* why) {
     if (!c) { *why = "config is NULL"; return SDSAT_EINVAL; }
@@ -197,8 +198,8 @@ void carve(sdsat_ctx* c, Carver& cv) {
     c->tree_rows = (int*)cv.take(bq * 4);
     c->tree_mask = (uint64_t*)cv.take(bq * 8);
     c->logits = (float*)cv.take(bq * D.V * 4);
+    c->hbuf = cv.take((size_t)D.maxM * D.d_pad * e);
     if (D.maxM > kSkinnyRows) {
-        c->hbuf = cv.take((size_t)D.maxM * D.d_pad * e);
         c->c_qkv = (float*)cv.take((size_t)D.maxM * 3 * D.d * 4);
         c->c_gu = (float*)cv.take((size_t)D.maxM * 2 * D.F * 4);
         c->c_y = (float*)cv.take((size_t)D.maxM * D.d * 4);
@@ -367,6 +368,23 @@ int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const 
     const Dims& D = c->D;
     const int M = B * q;
     if (M > kSkinnyRows) return large_block_impl(c, B, q, tokens, logits);
+    // The GEMMs behind an RMSNorm read X either as the float rows x o g, scaled
+    // and rounded at the matrix-core input, or (more than 16 rows) as those rows
+    // rounded once by rms_rows: every workgroup re-reads X, and past one row
+    // tile the float rows cost as much traffic as the weights.  Both give the
+    // same element-type values (same partial-sum order, same rounding).
+    const bool pre = M > kPreRoundRows;
+    auto norm_input = [&](GemmArgs& g) -> int {
+        g.ldx = D.d_pad;
+        if (!pre) {
+            g.xf = c->xg; g.ssq = c->ssq; g.n_ssq = D.n_ssq; g.eps = c->cfg.rms_eps;
+            return SDSAT_OK;
+        }
+        HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, c->cfg.rms_eps, M, c->hbuf, D.d_pad,
+                                  c->stream));
+        g.xa = c->hbuf;
+        return SDSAT_OK;
+    };
     hipEvent_t evb;
     prof_begin(c, logits ? PK_BLOCK : PK_PREFILL, &evb);
     HIPCHK(c, launch_embed(D.dtype, c->embed, D.V + D.A, D.d, tokens, M, c->x, c->xg, c->attn_norm[0], D.d_pad,
@@ -375,11 +393,12 @@ int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const 
         // attention sub-block: RMSNorm -> QKV (+RoPE, KV write) -> attention -> O (+residual);
         // xg holds x o (the gain of the RMSNorm the next GEMM applies)
         GemmArgs a{};
-        a.xf = c->xg; a.ldx = D.d_pad; a.ssq = c->ssq; a.n_ssq = D.n_ssq; a.eps = c->cfg.rms_eps;
+        int rc = norm_input(a);
+        if (rc) return rc;
         a.qbuf = c->qbuf; a.kc = layer_k(c, l); a.vc = layer_v(c, l);
         a.cache_len = c->cache_len; a.q = q; a.H = D.H; a.Dh = D.Dh; a.S_max = D.S; a.mask = mask;
         a.rope = c->rope;
-        int rc = run_gemm(c, PK_QKV, EP_QKV, M, D.nt_qkv, D.ks_d, 3 * D.d, D.d, c->w_qkv[l], a);
+        rc = run_gemm(c, PK_QKV, EP_QKV, M, D.nt_qkv, D.ks_d, 3 * D.d, D.d, c->w_qkv[l], a);
         if (rc) return rc;
         rc = attention_layer(c, l, B, q, mask, (const float*)c->qbuf, c->obuf, 0, D.d_pad);
         if (rc) return rc;
@@ -390,7 +409,8 @@ int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const 
         if (rc) return rc;
         // feed-forward sub-block: RMSNorm -> gate/up (+SwiGLU) -> down (+residual)
         GemmArgs f{};
-        f.xf = c->xg; f.ldx = D.d_pad; f.ssq = c->ssq; f.n_ssq = D.n_ssq; f.eps = c->cfg.rms_eps;
+        rc = norm_input(f);
+        if (rc) return rc;
         f.uout = c->ubuf; f.F = D.F; f.ldu = D.F_pad;
         rc = run_gemm(c, PK_GATEUP, EP_SWIGLU, M, D.nt_gu, D.ks_d, 2 * D.F, D.d, c->w_gu[l], f);
         if (rc) return rc;
@@ -402,9 +422,10 @@ int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const 
     }
     if (logits) {
         GemmArgs h{};
-        h.xf = c->xg; h.ldx = D.d_pad; h.ssq = c->ssq; h.n_ssq = D.n_ssq; h.eps = c->cfg.rms_eps;
+        int rc = norm_input(h);
+        if (rc) return rc;
         h.y = logits; h.ldy = D.V;
-        int rc = run_gemm(c, PK_LM, EP_STORE, M, D.nt_lm, D.ks_d, D.V, D.d, c->w_lm, h);
+        rc = run_gemm(c, PK_LM, EP_STORE, M, D.nt_lm, D.ks_d, D.V, D.d, c->w_lm, h);
         if (rc) return rc;
     }
     prof_end(c, evb);
@@ -539,6 +560,7 @@ int sdsat_init(const sdsat_config* cfg, const void* const* weights, int32_t n_we
         (void)launch_fill_i32((int*)c->xg, (size_t)D.maxM * D.d_pad, 0, c->stream);
         (void)launch_fill_i32((int*)c->obuf, (size_t)D.maxM * D.d_pad * D.esz / 4, 0, c->stream);
         (void)launch_fill_i32((int*)c->ubuf, (size_t)D.maxM * D.F_pad * D.esz / 4, 0, c->stream);
+        (void)launch_fill_i32((int*)c->hbuf, (size_t)D.maxM * D.d_pad * D.esz / 4, 0, c->stream);
         (void)launch_fill_i32(c->verify_cnt, D.maxB, 0, c->stream);
         (void)launch_fill_i32(c->cache_len, D.maxB, 0, c->stream);
         (void)launch_fill_i32(c->err_flag, 1, 0, c->stream);

@@ -259,7 +259,8 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int tile, const f32x
 }
 
 template <typename T, int EP, int MT, int NTW, bool XF>
-__global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(GemmArgs a) {
+// Workgroups of several tiles have 4 waves, the others at most 8.
+__global__ void __launch_bounds__(NTW > 1 ? 256 : 512) gemm_kernel(GemmArgs a) {
     constexpr int U = Batch<T, MT, XF>::U;
     using XT = typename XIn<T, XF>::type;
     extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -424,7 +425,7 @@ __global__ void __launch_bounds__(NTW == 1 && !XF ? 1024 : 512) gemm_kernel(Gemm
 template <typename T, int EP, bool XF>
 static hipError_t launch_mt(const GemmPlan& p, const GemmArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     const dim3 grid(p.grid), block(64 * p.waves);
-    if ((p.ntw > 1 || XF) && p.waves > 8) return hipErrorInvalidValue;
+    if (p.waves > (p.ntw > 1 ? 4 : 8)) return hipErrorInvalidValue;
     auto go = [&](auto kernel) {
         if (ev0) hipExtLaunchKernelGGL(kernel, grid, block, p.lds_bytes, s, ev0, ev1, 0, a);
         else hipLaunchKernelGGL(kernel, grid, block, p.lds_bytes, s, a);
@@ -442,8 +443,9 @@ static hipError_t launch_mt(const GemmPlan& p, const GemmArgs& a, hipStream_t s,
     return hipGetLastError();
 }
 
-// RMSNorm-input GEMMs (QKV, gate/up, LM head) read float x o g rows; O and
-// down read element-type rows (attention output, SwiGLU product).
+// RMSNorm-input GEMMs (QKV, gate/up, LM head) read float x o g rows, or those
+// rows already normalised and rounded (blocks of more than one row tile); O
+// and down read element-type rows (attention output, SwiGLU product).
 template <typename T>
 static hipError_t launch_t(int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
     const bool xf = a.xf != nullptr;
@@ -451,9 +453,10 @@ static hipError_t launch_t(int ep, const GemmPlan& p, const GemmArgs& a, hipStre
     switch (ep) {
         case EP_STORE:
             return xf ? launch_mt<T, EP_STORE, true>(p, a, s, e0, e1) : launch_mt<T, EP_STORE, false>(p, a, s, e0, e1);
-        case EP_QKV: return xf ? launch_mt<T, EP_QKV, true>(p, a, s, e0, e1) : hipErrorInvalidValue;
+        case EP_QKV: return xf ? launch_mt<T, EP_QKV, true>(p, a, s, e0, e1) : launch_mt<T, EP_QKV, false>(p, a, s, e0, e1);
         case EP_RESID: return xf ? hipErrorInvalidValue : launch_mt<T, EP_RESID, false>(p, a, s, e0, e1);
-        case EP_SWIGLU: return xf ? launch_mt<T, EP_SWIGLU, true>(p, a, s, e0, e1) : hipErrorInvalidValue;
+        case EP_SWIGLU:
+            return xf ? launch_mt<T, EP_SWIGLU, true>(p, a, s, e0, e1) : launch_mt<T, EP_SWIGLU, false>(p, a, s, e0, e1);
         default: return hipErrorInvalidValue;
     }
 }

@@ -14,22 +14,37 @@
 namespace sdsat {
 
 // h[m][k] = elem(xg[m][k] / rms_m), rms_m = sqrt(sum_t ssq[m][t] / K + eps).
-// One workgroup per row; the first wave sums the row's partials in the order
-// the decode GEMM does (lane-strided, then a wave butterfly).
+// Workgroup (m, chunk) writes 4 * 256 columns of row m; every thread's four
+// values are requested first, then the first wave sums the row's partials in
+// the order the decode GEMM does (lane-strided, then a wave butterfly).
 template <typename T>
 __global__ void __launch_bounds__(256) rms_rows_kernel(const float* xg, int ldxg, const float* ssq, int n_ssq, int K,
                                                        float eps, T* h, int ldh) {
     __shared__ float s_inv;
     const int m = blockIdx.x;
+    const int k0 = (blockIdx.y * 256 + threadIdx.x) * 4;
+    const float* xr = xg + (size_t)m * ldxg;
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    const bool whole = k0 + 3 < K;   // ldxg and the row start are multiples of 4 floats
+    if (whole) {
+        const float4 t = *reinterpret_cast<const float4*>(xr + k0);
+        v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = k0 + i < K ? xr[k0 + i] : 0.f;
+    }
     if (threadIdx.x < 64) {
-        float v = 0.f;
-        for (int col = threadIdx.x; col < n_ssq; col += 64) v += ssq[(size_t)m * n_ssq + col];
-        v = wave_sum(v);
-        if (threadIdx.x == 0) s_inv = 1.0f / sqrtf(v / (float)K + eps);
+        float sum = 0.f;
+        for (int col = threadIdx.x; col < n_ssq; col += 64) sum += ssq[(size_t)m * n_ssq + col];
+        sum = wave_sum(sum);
+        if (threadIdx.x == 0) s_inv = 1.0f / sqrtf(sum / (float)K + eps);
     }
     __syncthreads();
     const float inv = s_inv;
-    for (int k = threadIdx.x; k < K; k += blockDim.x) h[(size_t)m * ldh + k] = to_elem<T>(xg[(size_t)m * ldxg + k] * inv);
+    T* hr = h + (size_t)m * ldh;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        if (k0 + i < K) hr[k0 + i] = to_elem<T>(v[i] * inv);
 }
 
 // Q, K, V of row m from the float GEMM output c[m][0..3d) (Q | K | V): rotary
@@ -96,11 +111,13 @@ __global__ void __launch_bounds__(256) swiglu_rows_kernel(const float* g, const 
 hipError_t launch_rms_rows(int dtype, const float* xg, int ldxg, const float* ssq, int n_ssq, int K, float eps, int M,
                            void* h, int ldh, hipStream_t s) {
     if (M < 1) return hipSuccess;
+    if (ldxg % 4) return hipErrorInvalidValue;   // float4 row loads
+    const dim3 grid(M, (K + 1023) / 1024);
     if (dtype == 1)
-        hipLaunchKernelGGL(rms_rows_kernel<uint16_t>, dim3(M), dim3(256), 0, s, xg, ldxg, ssq, n_ssq, K, eps,
+        hipLaunchKernelGGL(rms_rows_kernel<uint16_t>, grid, dim3(256), 0, s, xg, ldxg, ssq, n_ssq, K, eps,
                            static_cast<uint16_t*>(h), ldh);
     else
-        hipLaunchKernelGGL(rms_rows_kernel<float>, dim3(M), dim3(256), 0, s, xg, ldxg, ssq, n_ssq, K, eps,
+        hipLaunchKernelGGL(rms_rows_kernel<float>, grid, dim3(256), 0, s, xg, ldxg, ssq, n_ssq, K, eps,
                            static_cast<float*>(h), ldh);
     return hipGetLastError();
 }
