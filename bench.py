@@ -47,11 +47,13 @@ def block_bytes(sh, B, q, ctx_len):
 
 
 def gateup_bytes(sh, M):
-    """Algorithmic bytes of one gate/up launch: the [2F, d] bf16 weight tiles, the M float rows x o g of
-    its RMSNorm input (gain applied by the producing epilogue), their per-16-column sums of squares,
-    and the bf16 SwiGLU output."""
+    """Algorithmic bytes of one gate/up launch: the [2F, d] bf16 weight tiles, its M input rows and the
+    bf16 SwiGLU output.  A block of several rows reads the normalised rows already rounded to bf16; a
+    one-row block reads the float row x o g (gain applied by the producing epilogue) and its
+    per-16-column sums of squares."""
     d, F = sh.d_model, sh.d_ffn
-    return 2 * F * d * 2 + M * d * 4 + M * (d // 16) * 4 + M * F * 2
+    x = M * d * 2 if M > 1 else M * d * 4 + M * (d // 16) * 4
+    return 2 * F * d * 2 + x + M * F * 2
 
 
 def profiled_traffic():

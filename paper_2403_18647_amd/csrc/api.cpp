@@ -48,7 +48,7 @@ struct Dims {
 
 constexpr int kMaxBlock = 4096;   // rows per sequence per block
 constexpr int kSkinnyRows = 64;   // blocks of at most this many rows (B*q) run the skinny GEMM kernels
-constexpr int kPreRoundRows = 16; // past one 16-row tile, normalised GEMM inputs are rounded once (rms_rows)
+constexpr int kPreRoundRows = 1;  // blocks of more rows round normalised GEMM inputs once (rms_rows)
 
 int make_dims(const sdsat_config* c, Dims* D, std::string* why) {
     if (!c) { *why = "config is NULL"; return SDSAT_EINVAL; }
@@ -369,9 +369,9 @@ int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const 
     const int M = B * q;
     if (M > kSkinnyRows) return large_block_impl(c, B, q, tokens, logits);
     // The GEMMs behind an RMSNorm read X either as the float rows x o g, scaled
-    // and rounded at the matrix-core input, or (more than 16 rows) as those rows
-    // rounded once by rms_rows: every workgroup re-reads X, and past one row
-    // tile the float rows cost as much traffic as the weights.  Both give the
+    // and rounded at the matrix-core input (one-row blocks), or as those rows
+    // rounded once by rms_rows: every workgroup re-reads X, and the float rows
+    // of even a 6-row block cost more than the extra launch.  Both give the
     // same element-type values (same partial-sum order, same rounding).
     const bool pre = M > kPreRoundRows;
     auto norm_input = [&](GemmArgs& g) -> int {
