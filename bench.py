@@ -171,6 +171,10 @@ def ksweep(B, synth, ctx, wl, prompts, new_tokens=64, k_max=13):
         rows.append({"k": k, "q": k + 1, "block_ms": round(blk_ms / max(1, n_blk), 4),
                      "loop_ms": round(st_f["decode_ms"] / max(1, st_f["loops"]), 4),
                      "tokens_per_loop_full_accept": k + 2 if k else 2,
+                     # the loop rate: k + 2 tokens per loop time (the run's own rate also pays for the
+                     # overshoot of its last loop past new_tokens, which depends on new_tokens mod k + 2)
+                     "loop_tokens_per_s_full_accept": round((k + 2 if k else 2) * wl.batch /
+                                                            (st_f["decode_ms"] / max(1, st_f["loops"]) / 1e3), 1),
                      "decode_tokens_per_s_full_accept": round(new_tokens * wl.batch / (st_f["decode_ms"] / 1e3), 2),
                      "tokens_equal_ar": bool((out_f == ref[:, :new_tokens]).all())})
     return {"metric": "k sweep: block forward and loop time vs k", "unit": "ms", "workload": wl.name,
