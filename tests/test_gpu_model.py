@@ -289,6 +289,32 @@ def test_out_of_range_token_reports_edata():
     ctx.close()
 
 
+def test_tree_and_forced_argument_errors():
+    wl = synth.workload("tiny")
+    sh = wl.shape
+    ctx = helpers.make_ctx(wl, max_batch=1, max_ctx=128, max_block=6)
+    pr = synth.prompts(wl)
+    ad = synth.adaptive_ids(sh, 5)
+    cases = [(dict(width=9), -1),                                            # tree widths are 1..8
+             (dict(width=2), -4),                                            # 1 + 5 * 2 = 11 rows > max_block 6
+             (dict(ref=np.zeros((1, 0), np.int32)), -1),                     # empty reference
+             (dict(ref=np.full((1, 20), sh.vocab + sh.n_adaptive, np.int32)), -1)]   # id out of range
+    for kw, code in cases:
+        with pytest.raises(B.SdsatError) as e:
+            B.sdsat_generate(ctx.handle, pr, 8, 5, ad, **kw)
+        assert e.value.code == code, kw
+    out, _ = B.sdsat_generate(ctx.handle, pr, 8, 5, ad)   # the context still works
+    assert out.shape == (1, 8)
+    ctx.close()
+    # a tree block of batch x (1 + k * width) rows must fit the 64-row decode kernels
+    wl6 = synth.workload("tiny", batch=6)
+    ctx = helpers.make_ctx(wl6, max_batch=6, max_ctx=128, max_block=11)
+    with pytest.raises(B.SdsatError) as e:
+        B.sdsat_generate(ctx.handle, synth.prompts(wl6), 8, 5, ad, width=2)
+    assert e.value.code == -4
+    ctx.close()
+
+
 def test_capacity_errors():
     wl = synth.workload("tiny")
     ctx = helpers.make_ctx(wl, max_batch=1, max_ctx=64, max_block=6)
