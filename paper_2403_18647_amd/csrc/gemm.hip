@@ -12,11 +12,14 @@
 //    global memory (the few X rows stay in L2), and reduce their partial tiles
 //    through LDS in wave order: deterministic, with no device-scope fences or
 //    atomics.
-//  * An RMSNorm input arrives as the float rows x o g (gain applied by the
-//    producer); the kernel reduces the producer's per-tile sums of squares to
-//    each row's 1/rms before its first matrix-core step and rounds
-//    x o g / rms to the element type at the matrix-core input: the normalised
-//    activation a bf16 model stores, rounded once.
+//  * An RMSNorm input arrives either already normalised and rounded to the
+//    element type (rms_rows; blocks of several rows, whose float rows re-read by
+//    every workgroup would cost as much traffic as the weights), or, for one-row
+//    blocks, as the float rows x o g (gain applied by the producer): the kernel
+//    then reduces the producer's per-tile sums of squares to each row's 1/rms
+//    before its first matrix-core step and rounds x o g / rms to the element
+//    type at the matrix-core input.  Both give the normalised activation a bf16
+//    model stores, rounded once, bit for bit the same.
 //  * Fused epilogues, run by wave 0 on the reduced tile:
 //      EP_STORE   float output (LM-head logits)
 //      EP_QKV     RoPE on Q and K columns, Q (float) to its buffer, K and V into
@@ -85,11 +88,13 @@ void launch_pack(const PackArgs& a, hipStream_t s) {
 //    narrow [d, d] / [d, F] matrices (256 tiles, one workgroup per compute
 //    unit), 4 for the wide ones; at least 4 contraction steps per wave
 //    (several tiles per workgroup, or X staged in LDS, measured slower);
-//  * blocks of more than 16 rows (prefill chunks) reload their X fragments
-//    for every weight fragment: for the wide matrices a workgroup of 4 waves
-//    takes 4 column tiles so that one X load feeds 4 tiles' matrix-core steps
-//    (M = 64: QKV 55 -> 37 us, gate/up 103 -> 62 us); the narrow ones keep one
-//    tile per workgroup.
+//  * blocks of more than 16 rows (batch 4 decode, prefill chunks) reload their
+//    X fragments for every weight fragment: for the wide matrices a workgroup
+//    of 4 waves takes 4 column tiles so that one X load feeds 4 tiles'
+//    matrix-core steps (M = 64: QKV 55 -> 37 us, gate/up 103 -> 62 us); the
+//    narrow ones keep one tile per workgroup.  The waves per workgroup depend
+//    on the matrix shape only where block-size invariance needs it: one row
+//    tile and four column tiles both use 4 waves on the wide matrices.
 GemmPlan plan_gemm(int M, int n_tiles, int k_steps) {
     GemmPlan p;
     p.mt = (M + 15) / 16;
