@@ -331,6 +331,135 @@ __device__ __forceinline__ uint32_t radix_threshold(const uint32_t (&keys)[kCPT]
     return prefix;
 }
 
+// ---- top-k of at most kSmallK ids: candidate list
+static constexpr int kSmallK = 64;
+
+__device__ __forceinline__ uint32_t shfl_xor_any(uint32_t v, int o) { return (uint32_t)__shfl_xor((int)v, o, 64); }
+__device__ __forceinline__ uint64_t shfl_xor_any(uint64_t v, int o) {
+    return ((uint64_t)shfl_xor_any((uint32_t)(v >> 32), o) << 32) | shfl_xor_any((uint32_t)v, o);
+}
+__device__ __forceinline__ uint32_t readlane_u(uint32_t v, int lane) {
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
+}
+
+// Bitonic sort of one value per lane across the wave, descending (lane 0 holds the largest).
+template <typename U>
+__device__ __forceinline__ U wave_sort_desc(U v) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int size = 2; size <= 64; size <<= 1)
+#pragma unroll
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            const U o = shfl_xor_any(v, stride);
+            const bool keep_max = ((lane & stride) == 0) == ((lane & size) == 0);
+            v = keep_max ? (v > o ? v : o) : (v < o ? v : o);
+        }
+    return v;
+}
+
+// Top-k with k <= kSmallK (ties keep lower ids), then top-p and the inverse
+// CDF, on a candidate list.  The k-th largest of the 1024 threads' maxima is at
+// most the row's k-th largest key (k distinct ids reach it), so every id at or
+// above it is a candidate and the kept ids are among them; it is found by
+// sorting each wave's maxima and a k-round tournament over the waves' sorted
+// lists.  The candidates are gathered in
+// id order; wave 0 sorts them by (key descending, id ascending), keeps the
+// first k and finishes in float64: the total mass and the threshold in that
+// order, the inverse CDF over the nucleus in ascending id order.  Returns false
+// (nothing decided) when more than kSmallK ids reach the bound.
+__device__ __forceinline__ bool sample_small_topk(const uint32_t (&keys)[kCPT], Bits kept, int id0, double T,
+                                                  double p, int top_k, double u, int* s_i, int* out) {
+    __shared__ uint32_t s_top[kWaves * kSmallK];   // each wave's k largest thread maxima, descending
+    __shared__ uint32_t s_bound;
+    __shared__ uint32_t s_ck[kSmallK];
+    __shared__ int s_cid[kSmallK];
+    __shared__ double s_ne[kSmallK];
+    __shared__ int s_nid[kSmallK];
+    __shared__ int s_tok;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    uint32_t tmax = 0;
+#pragma unroll
+    for (int i = 0; i < kCPT; ++i) if ((kept >> i) & 1u) tmax = max(tmax, keys[i]);
+    const uint32_t srt = wave_sort_desc(tmax);
+    if (lane < top_k) s_top[wave * kSmallK + lane] = srt;
+    __syncthreads();
+    if (wave == 0) {
+        // k rounds of a tournament over the waves' lists: the k-th largest thread maximum
+        int pos = 0;
+        uint32_t head = lane < kWaves ? s_top[lane * kSmallK] : 0u;
+        uint32_t last = 0;
+        for (int r = 0; r < top_k; ++r) {
+            uint64_t c = lane < kWaves ? ((uint64_t)head << 32) | (uint32_t)(63 - lane) : 0ull;
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) {
+                const uint64_t t = shfl_xor_any(c, o);
+                c = c > t ? c : t;
+            }
+            last = (uint32_t)(c >> 32);
+            if (lane == 63 - (int)(uint32_t)c) {   // the list that held it moves on
+                ++pos;
+                head = pos < top_k ? s_top[lane * kSmallK + pos] : 0u;
+            }
+        }
+        if (lane == 0) s_bound = last;
+    }
+    __syncthreads();
+    const uint32_t bound = s_bound;
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < kCPT; ++i) cnt += ((kept >> i) & 1u) && keys[i] >= bound;
+    const int C = block_sum_i(cnt, s_i);   // >= top_k
+    if (C > kSmallK) return false;
+    int slot = block_exscan_i(cnt, s_i);
+#pragma unroll
+    for (int i = 0; i < kCPT; ++i)
+        if (((kept >> i) & 1u) && keys[i] >= bound) { s_ck[slot] = keys[i]; s_cid[slot] = id0 + i; ++slot; }
+    __syncthreads();
+    if (wave == 0) {
+        // (key descending, id ascending) as the composite (key, ~id) sorted descending;
+        // lanes past C hold 0 and sort last
+        uint64_t v = lane < C ? ((uint64_t)s_ck[lane] << 32) | (uint32_t)~(uint32_t)s_cid[lane] : 0ull;
+        v = wave_sort_desc(v);
+        const uint32_t key = (uint32_t)(v >> 32);
+        const int id = (int)~(uint32_t)v;
+        const int k = top_k;
+        const double zmax = (double)key_value(readlane_u(key, 0)) / T;
+        const double e = lane < k ? exp((double)key_value(key) / T - zmax) : 0.0;
+        double tot = 0.0;
+        for (int j = 0; j < k; ++j) tot += readlane_d(e, j);
+        const double pE = (p < 1.0 ? p : 1.0) * tot;
+        // threshold: the first group of equal keys (in descending order) at which the mass
+        // from the top reaches p * E; the whole group is in the nucleus
+        double acc = 0.0, mass = -1.0;
+        int nstar = k;
+        for (int j = 0; j < k; ++j) {
+            acc += readlane_d(e, j);
+            const bool group_end = j + 1 == k || readlane_u(key, min(j + 1, 63)) != readlane_u(key, j);
+            if (group_end && acc >= pE) { nstar = j + 1; mass = acc; break; }
+        }
+        if (mass < 0.0) mass = acc;   // rounding left every sum short of p * E: all k
+        // the nucleus in ascending id order, then the inverse CDF
+        if (lane < nstar) {
+            int rank = 0;
+            for (int i = 0; i < nstar; ++i) rank += (int)__builtin_amdgcn_readlane(id, i) < id;
+            s_nid[rank] = id;
+            s_ne[rank] = e;
+        }
+        const double target = u * mass;
+        double cum = 0.0;
+        int tok = -1;
+        for (int r = 0; r < nstar; ++r) {
+            cum += s_ne[r];
+            if (cum > target) { tok = s_nid[r]; break; }
+        }
+        if (tok < 0) tok = s_nid[nstar - 1];
+        if (lane == 0) s_tok = tok;
+    }
+    __syncthreads();
+    *out = s_tok;
+    return true;
+}
+
 __device__ __forceinline__ int sample_row(const float* row, int V, double T, double p, int top_k, double u) {
     __shared__ double s_hist[kBins * kNT];   // 128 KiB: per-thread digit columns
     __shared__ double s_tot[kBins];          // digit totals (read by every thread after the last pass)
@@ -355,6 +484,11 @@ __device__ __forceinline__ int sample_row(const float* row, int V, double T, dou
 #pragma unroll
     for (int i = 0; i < kCPT; ++i) if (id0 + i < V) kept |= 1u << i;
 
+    // k up to 3/4 of the list: the candidates (about k) rarely overflow it
+    if (top_k > 0 && top_k <= kSmallK * 3 / 4 && top_k < V) {
+        int tok;
+        if (sample_small_topk(keys, kept, id0, T, p, top_k, u, s_i, &tok)) return tok;
+    }
     if (top_k > 0 && top_k < V) {
         // largest key Kk with count(key >= Kk) >= top_k (counts are exact in double)
         double cnt;
