@@ -48,6 +48,7 @@ struct Dims {
 
 constexpr int kMaxBlock = 4096;   // rows per sequence per block
 constexpr int kSkinnyRows = 64;   // blocks of at most this many rows (B*q) run the skinny GEMM kernels
+constexpr int kRecLoops = 64;     // generation loops enqueued between two host synchronisations, at most
 constexpr int kPreRoundRows = 1;  // blocks of more rows round normalised GEMM inputs once (rms_rows)
 
 int make_dims(const sdsat_config* c, Dims* D, std::string* why) {
@@ -124,6 +125,9 @@ struct sdsat_ctx {
     rocblas_handle blas = nullptr;
     int* h_pin = nullptr;   // pinned host staging
     size_t h_pin_ints = 0;
+    int* h_rec = nullptr;      // pinned host copy of the loop records
+    int* loop_rec = nullptr;   // device loop records [kRecLoops][maxB][kLoopRecCols]
+    int* produced = nullptr;   // tokens each sequence has emitted in the current generation (device)
     // upper bounds of cache_len, tracked on the host for launch planning
     std::vector<int> len_hint;
     // profiling
@@ -136,6 +140,7 @@ struct sdsat_ctx {
     ~sdsat_ctx() {
         for (hipEvent_t e : events) (void)hipEventDestroy(e);
         if (h_pin) (void)hipHostFree(h_pin);
+        if (h_rec) (void)hipHostFree(h_rec);
         if (blas) (void)rocblas_destroy_handle(blas);
     }
 };
@@ -181,6 +186,8 @@ void carve(sdsat_ctx* c, Carver& cv) {
     c->cache_len = (int*)cv.take((size_t)D.maxB * 4);
     c->err_flag = (int*)cv.take(4);
     c->verify_cnt = (int*)cv.take((size_t)D.maxB * 4);
+    c->produced = (int*)cv.take((size_t)D.maxB * 4);
+    c->loop_rec = (int*)cv.take((size_t)kRecLoops * D.maxB * kLoopRecCols * 4);
     const size_t bq = (size_t)D.maxB * D.maxQ;
     c->tok1 = (int*)cv.take(bq * 4);
     c->out1 = (int*)cv.take(bq * 4);
@@ -570,7 +577,9 @@ int sdsat_init(const sdsat_config* cfg, const void* const* weights, int32_t n_we
         }
     }
     c->h_pin_ints = (size_t)D.maxB * D.maxQ * 4 + 64;
-    if (hipHostMalloc((void**)&c->h_pin, c->h_pin_ints * 4, hipHostMallocDefault) != hipSuccess) {
+    if (hipHostMalloc((void**)&c->h_pin, c->h_pin_ints * 4, hipHostMallocDefault) != hipSuccess ||
+        hipHostMalloc((void**)&c->h_rec, (size_t)kRecLoops * D.maxB * kLoopRecCols * 4, hipHostMallocDefault) !=
+            hipSuccess) {
         c->err = "pinned host allocation failed";
         return init_fail(SDSAT_ENOMEM);
     }
@@ -730,101 +739,125 @@ int generate_impl(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t
     const auto t1 = clk::now();
 
     std::vector<int> produced(batch, 0);
-    int* h_act = c->h_pin;                       // [batch]
-    int* h_o1 = c->h_pin + 64;                   // [batch*q]
-    int* h_o2 = h_o1 + (size_t)batch * q;        // [batch*q2]
-    int* h_m = h_o2 + (size_t)batch * q2;        // [batch]
-    int* h_err = h_m + batch;
+    std::vector<int> len_exact(c->len_hint.begin(), c->len_hint.begin() + batch);
+    // the device tracks each sequence's progress (produced, active) so that loops run back to back;
+    // every sequence starts active
+    for (int b = 0; b < batch; ++b) c->h_pin[b] = max_new > 0 ? 1 : 0;
+    HIPCHK(c, hipMemcpyAsync(c->active, c->h_pin, (size_t)batch * 4, hipMemcpyHostToDevice, c->stream));
+    HIPCHK(c, launch_fill_i32(c->produced, batch, 0, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));   // the pinned staging buffer is reused
+    int* h_err = c->h_pin;
+    const size_t rec_stride = (size_t)D.maxB * kLoopRecCols;
     for (;;) {
-        bool any = false;
-        for (int b = 0; b < batch; ++b) { h_act[b] = produced[b] < max_new; any |= h_act[b] != 0; }
-        if (!any) break;
-        HIPCHK(c, hipMemcpyAsync(c->active, h_act, (size_t)batch * 4, hipMemcpyHostToDevice, c->stream));
-        // draft step 1 (Eq. 1): [pending, a_1..a_k]
-        HIPCHK(c, launch_build_draft1(c->pending, c->adaptive, batch, k, c->tok1, c->stream));
-        rc = forward_block_impl(c, batch, q, c->tok1, nullptr, c->logits);
-        if (rc) return rc;
-        if (nucleus) {
-            HIPCHK(c, launch_pos0(c->cache_len, batch, 1, c->pos0, c->stream));
-            HIPCHK(c, launch_verify_nucleus(c->logits, batch, q, D.V, nullptr, q - 1, temperature, top_p, top_k, seed,
-                                            c->pos0, c->out1, nullptr, c->verify_cnt, c->stream));
-        } else {
-            HIPCHK(c, launch_verify_greedy(c->logits, batch, q, D.V, nullptr, q - 1, c->out1, nullptr, c->verify_cnt,
-                                           c->stream));
-        }
-        HIPCHK(c, launch_commit(c->cache_len, batch, c->active, D.S, c->err_flag, c->stream));   // keep row 0 (active: 1)
-        for (int b = 0; b < batch; ++b) c->len_hint[b] += h_act[b];
-        if (h_ref && k > 0) {   // drafts from the reference continuation (pinned staging after h_err)
-            int* dr = h_err + 1;
+        // Loops of this batch: as many as the least advanced active sequence needs at the least
+        // (k + 2 tokens per loop), so every loop of the batch has an active sequence.  Drafts taken
+        // from a reference depend on the host's counts: one loop per batch then.
+        int minp = -1;
+        for (int b = 0; b < batch; ++b)
+            if (produced[b] < max_new && (minp < 0 || produced[b] < minp)) minp = produced[b];
+        if (minp < 0) break;
+        const int n_b = h_ref ? 1 : std::min(kRecLoops, std::max(1, (max_new - minp + k + 1) / (k + 2)));
+        for (int i = 0; i < n_b; ++i) {
+            // upper bounds of the cache lengths for the attention plans (an over-estimate only adds
+            // empty key splits); the exact lengths are restored after the batch
+            if (i > 0)
+                for (int b = 0; b < batch; ++b)
+                    if (produced[b] < max_new) c->len_hint[b] = std::min(D.S, c->len_hint[b] + k + 1);
+            // draft step 1 (Eq. 1): [pending, a_1..a_k]
+            HIPCHK(c, launch_build_draft1(c->pending, c->adaptive, batch, k, c->tok1, c->stream));
+            rc = forward_block_impl(c, batch, q, c->tok1, nullptr, c->logits);
+            if (rc) return rc;
+            if (nucleus) {
+                HIPCHK(c, launch_pos0(c->cache_len, batch, 1, c->pos0, c->stream));
+                HIPCHK(c, launch_verify_nucleus(c->logits, batch, q, D.V, nullptr, q - 1, temperature, top_p, top_k,
+                                                seed, c->pos0, c->out1, nullptr, c->verify_cnt, c->stream));
+            } else {
+                HIPCHK(c, launch_verify_greedy(c->logits, batch, q, D.V, nullptr, q - 1, c->out1, nullptr,
+                                               c->verify_cnt, c->stream));
+            }
+            HIPCHK(c, launch_commit(c->cache_len, batch, c->active, D.S, c->err_flag, c->stream));   // keep row 0
             for (int b = 0; b < batch; ++b)
-                for (int j = 0; j < k; ++j) {
-                    const long i = (long)produced[b] + 1 + j;
-                    dr[b * k + j] = i < ref_len ? h_ref[(size_t)b * ref_len + i] : 0;
+                if (produced[b] < max_new) c->len_hint[b] = std::min(D.S, c->len_hint[b] + 1);
+            if (h_ref && k > 0) {   // drafts from the reference continuation (pinned staging after h_err)
+                int* dr = h_err + 1;
+                for (int b = 0; b < batch; ++b)
+                    for (int j = 0; j < k; ++j) {
+                        const long idx = (long)produced[b] + 1 + j;
+                        dr[b * k + j] = idx < ref_len ? h_ref[(size_t)b * ref_len + idx] : 0;
+                    }
+                HIPCHK(c, hipMemcpy2DAsync(c->out1 + 1, (size_t)q * 4, dr, (size_t)k * 4, (size_t)k * 4, batch,
+                                           hipMemcpyHostToDevice, c->stream));
+            }
+            if (tree) {
+                // draft step 2 over the tree (Section 2.1.2): candidates of draft step 1's adaptive rows, rows
+                // at position L + depth seeing their ancestors; the target's token at every node; the longest
+                // confirmed branch; its rows gathered to slots L.. and committed, pending = the last token
+                HIPCHK(c, launch_tree_build(c->logits, batch, q, D.V, c->out1, k, width, q2, c->tree_tok,
+                                            c->tree_mask, c->tree_depth, c->stream));
+                rc = forward_block_impl(c, batch, q2, c->tree_tok, c->tree_mask, c->logits);
+                if (rc) return rc;
+                if (nucleus) {
+                    HIPCHK(c, launch_pos0(c->cache_len, batch, 1, c->pos0, c->stream));
+                    HIPCHK(c, launch_verify_nucleus(c->logits, batch, q2, D.V, nullptr, 0, temperature, top_p, top_k,
+                                                    seed, c->pos0, c->tree_target, nullptr, c->verify_cnt, c->stream,
+                                                    c->tree_depth));
+                } else {
+                    HIPCHK(c, launch_verify_greedy(c->logits, batch, q2, D.V, nullptr, 0, c->tree_target, nullptr,
+                                                   c->verify_cnt, c->stream));
                 }
-            HIPCHK(c, hipMemcpy2DAsync(c->out1 + 1, (size_t)q * 4, dr, (size_t)k * 4, (size_t)k * 4, batch,
-                                       hipMemcpyHostToDevice, c->stream));
-        }
-        if (tree) {
-            // draft step 2 over the tree (Section 2.1.2): candidates of draft step 1's adaptive rows, rows at
-            // position L + depth seeing their ancestors; the target's token at every node; the longest
-            // confirmed branch; its rows gathered to slots L.. and committed, pending = the last token
-            HIPCHK(c, launch_tree_build(c->logits, batch, q, D.V, c->out1, k, width, q2, c->tree_tok, c->tree_mask,
-                                        c->tree_depth, c->stream));
-            rc = forward_block_impl(c, batch, q2, c->tree_tok, c->tree_mask, c->logits);
-            if (rc) return rc;
-            if (nucleus) {
-                HIPCHK(c, launch_pos0(c->cache_len, batch, 1, c->pos0, c->stream));
-                HIPCHK(c, launch_verify_nucleus(c->logits, batch, q2, D.V, nullptr, 0, temperature, top_p, top_k,
-                                                seed, c->pos0, c->tree_target, nullptr, c->verify_cnt, c->stream,
-                                                c->tree_depth));
+                HIPCHK(c, launch_tree_walk(batch, q2, k, width, c->tree_tok, c->tree_target, c->active, c->out2,
+                                           c->n_accept, c->tree_rows, c->pending, c->n_commit, c->stream));
+                HIPCHK(c, launch_commit_gather(D.dtype, c->kc, c->vc, c->layer_elems, D.L, batch, D.H, D.Dh, D.S,
+                                               c->cache_len, c->n_commit, c->tree_rows, q2, c->err_flag, c->stream));
+                HIPCHK(c, launch_commit(c->cache_len, batch, c->n_commit, D.S, c->err_flag, c->stream));
             } else {
-                HIPCHK(c, launch_verify_greedy(c->logits, batch, q2, D.V, nullptr, 0, c->tree_target, nullptr,
-                                               c->verify_cnt, c->stream));
+                // draft step 2 (Eq. 2): [t1, d_1..d_k] = out1
+                rc = forward_block_impl(c, batch, q, c->out1, nullptr, c->logits);
+                if (rc) return rc;
+                if (nucleus) {
+                    HIPCHK(c, launch_pos0(c->cache_len, batch, 1, c->pos0, c->stream));
+                    HIPCHK(c, launch_verify_nucleus(c->logits, batch, q, D.V, c->out1 + 1, q, temperature, top_p,
+                                                    top_k, seed, c->pos0, c->out2, c->n_accept, c->verify_cnt,
+                                                    c->stream));
+                } else {
+                    HIPCHK(c, launch_verify_greedy(c->logits, batch, q, D.V, c->out1 + 1, q, c->out2, c->n_accept,
+                                                   c->verify_cnt, c->stream));
+                }
+                // verification (Eq. 3): commit rows 0..m, pending = o_m
+                HIPCHK(c, launch_loop_commit(c->cache_len, batch, q, c->active, c->n_accept, c->out2, c->pending,
+                                             c->n_commit, c->stream));
             }
-            HIPCHK(c, launch_tree_walk(batch, q2, k, width, c->tree_tok, c->tree_target, c->active, c->out2,
-                                       c->n_accept, c->tree_rows, c->pending, c->n_commit, c->stream));
-            HIPCHK(c, launch_commit_gather(D.dtype, c->kc, c->vc, c->layer_elems, D.L, batch, D.H, D.Dh, D.S,
-                                           c->cache_len, c->n_commit, c->tree_rows, q2, c->err_flag, c->stream));
-            HIPCHK(c, launch_commit(c->cache_len, batch, c->n_commit, D.S, c->err_flag, c->stream));
-        } else {
-            // draft step 2 (Eq. 2): [t1, d_1..d_k] = out1
-            rc = forward_block_impl(c, batch, q, c->out1, nullptr, c->logits);
-            if (rc) return rc;
-            if (nucleus) {
-                HIPCHK(c, launch_pos0(c->cache_len, batch, 1, c->pos0, c->stream));
-                HIPCHK(c, launch_verify_nucleus(c->logits, batch, q, D.V, c->out1 + 1, q, temperature, top_p, top_k,
-                                                seed, c->pos0, c->out2, c->n_accept, c->verify_cnt, c->stream));
-            } else {
-                HIPCHK(c, launch_verify_greedy(c->logits, batch, q, D.V, c->out1 + 1, q, c->out2, c->n_accept,
-                                               c->verify_cnt, c->stream));
-            }
-            // verification (Eq. 3): commit rows 0..m, pending = o_m
-            HIPCHK(c, launch_loop_commit(c->cache_len, batch, q, c->active, c->n_accept, c->out2, c->pending,
-                                         c->n_commit, c->stream));
+            HIPCHK(c, launch_loop_record(c->loop_rec + i * rec_stride, batch, q, q2, k, max_new, c->out1, c->out2,
+                                         c->n_accept, c->active, c->produced, c->stream));
         }
-        HIPCHK(c, hipMemcpyAsync(h_o1, c->out1, (size_t)batch * q * 4, hipMemcpyDeviceToHost, c->stream));
-        HIPCHK(c, hipMemcpyAsync(h_o2, c->out2, (size_t)batch * q2 * 4, hipMemcpyDeviceToHost, c->stream));
-        HIPCHK(c, hipMemcpyAsync(h_m, c->n_accept, (size_t)batch * 4, hipMemcpyDeviceToHost, c->stream));
+        HIPCHK(c, hipMemcpyAsync(c->h_rec, c->loop_rec, (size_t)n_b * rec_stride * 4, hipMemcpyDeviceToHost,
+                                 c->stream));
         HIPCHK(c, hipMemcpyAsync(h_err, c->err_flag, 4, hipMemcpyDeviceToHost, c->stream));
         HIPCHK(c, hipStreamSynchronize(c->stream));
         if (*h_err) {
             rc = read_err_flag(c);
             return rc ? rc : fail(c, SDSAT_EDATA, "device error flag set");
         }
-        st.loops++;
-        st.blocks += 2;
-        for (int b = 0; b < batch; ++b) {
-            if (!h_act[b]) continue;
-            const int m = h_m[b];
-            if (m < 0 || m > k) return fail(c, SDSAT_EDEVICE, "verification returned an invalid prefix length");
-            st.accepted += m;
-            st.accept_hist[m]++;
-            st.tokens += m + 2;
-            int* row = h_out + (size_t)b * max_new;
-            if (produced[b] < max_new) row[produced[b]++] = h_o1[b * q];
-            for (int j = 0; j <= m && produced[b] < max_new; ++j) row[produced[b]++] = h_o2[b * q2 + j];
-            c->len_hint[b] += m + 1;
+        // replay the batch's records with the same rule the device used for activity
+        for (int i = 0; i < n_b; ++i) {
+            const int* rec = c->h_rec + i * rec_stride;
+            st.loops++;
+            st.blocks += 2;
+            for (int b = 0; b < batch; ++b) {
+                if (produced[b] >= max_new) continue;
+                const int* r = rec + (size_t)b * kLoopRecCols;
+                const int m = r[0];
+                if (m < 0 || m > k) return fail(c, SDSAT_EDEVICE, "verification returned an invalid prefix length");
+                st.accepted += m;
+                st.accept_hist[m]++;
+                st.tokens += m + 2;
+                int* row = h_out + (size_t)b * max_new;
+                row[produced[b]++] = r[1];
+                for (int j = 0; j <= m && produced[b] < max_new; ++j) row[produced[b]++] = r[2 + j];
+                len_exact[b] += m + 2;
+            }
         }
+        for (int b = 0; b < batch; ++b) c->len_hint[b] = len_exact[b];
     }
     const auto t2 = clk::now();
     st.prefill_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();

@@ -161,5 +161,10 @@ hipError_t launch_build_draft1(const int* pending, const int* adaptive, int B, i
 hipError_t launch_loop_commit(int* cache_len, int B, int q, const int* active, const int* n_accept,
                               const int* tokens2, int* pending, int* n_commit_out, hipStream_t s);
 hipError_t launch_pos0(const int* cache_len, int B, int offset, int* pos0, hipStream_t s);
+// per-loop record for the host, [B][kLoopRecCols] ints: m, draft step 1's token, emitted rows 0..k; advances
+// the device's produced counts and active flags
+constexpr int kLoopRecCols = 66;   // k <= 63 (a block holds at most 64 rows)
+hipError_t launch_loop_record(int* rec, int B, int q1, int q2, int k, int max_new, const int* out1, const int* out2,
+                              const int* n_accept, int* active, int* produced, hipStream_t s);
 
 }  // namespace sdsat

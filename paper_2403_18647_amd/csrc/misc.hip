@@ -303,6 +303,33 @@ hipError_t launch_loop_commit(int* cache_len, int B, int q, const int* active, c
     return hipGetLastError();
 }
 
+// After a loop's verification: its record [m, t1, emitted 0..k] for the host,
+// and the sequence's progress (a loop emits m + 2 tokens: draft step 1's token
+// and verified rows 0..m); a sequence stays active while it has emitted fewer
+// than max_new, the rule the host applies when it replays the records.
+__global__ void loop_record_kernel(int* rec, int B, int q1, int q2, int k, int max_new, const int* out1,
+                                   const int* out2, const int* n_accept, int* active, int* produced) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    int* r = rec + (size_t)b * kLoopRecCols;
+    const int m = n_accept[b];
+    r[0] = m;
+    r[1] = out1[(size_t)b * q1];
+    for (int j = 0; j <= k; ++j) r[2 + j] = out2[(size_t)b * q2 + j];
+    if (active[b]) {
+        produced[b] += m + 2;
+        active[b] = produced[b] < max_new;
+    }
+}
+
+hipError_t launch_loop_record(int* rec, int B, int q1, int q2, int k, int max_new, const int* out1, const int* out2,
+                              const int* n_accept, int* active, int* produced, hipStream_t s) {
+    if (k + 3 > kLoopRecCols) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(loop_record_kernel, dim3((B + 63) / 64), dim3(64), 0, s, rec, B, q1, q2, k, max_new, out1, out2,
+                       n_accept, active, produced);
+    return hipGetLastError();
+}
+
 __global__ void pos0_kernel(const int* cache_len, int B, int offset, int* pos0) {
     const int b = blockIdx.x * blockDim.x + threadIdx.x;
     if (b < B) pos0[b] = cache_len[b] + offset;
