@@ -304,7 +304,7 @@ int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask,
     a.cache_len = c->cache_len; a.per_split = p.per_split; a.mask = mask;
     a.B = B; a.q = q; a.H = D.H; a.S_max = D.S;
     a.scale = (float)(1.0 / std::sqrt((double)D.Dh));
-    a.splits = p.splits; a.part = c->attn_part;
+    a.splits = p.splits; a.cols = p.cols; a.part = c->attn_part;
     a.out = out; a.out_f32 = out_f32; a.ldo = ldo; a.err = c->err_flag;
     hipEvent_t e0, e1;
     prof_pair(c, PK_ATTN, &e0, &e1);

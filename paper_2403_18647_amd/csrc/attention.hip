@@ -8,8 +8,11 @@
 //
 // Workgroups per (b, h, 16-row tile of the block): one per key split (the
 // splits are fixed 32-key block ranges, see plan_attention); a combine
-// kernel merges the splits' partials.  Waves take the workgroup's 32-key
-// blocks round-robin.
+// kernel merges the splits' partials.  Short caches take one split, and a
+// one-tile block then spreads each head over column slices instead: every
+// slice's workgroup forms all of the head's scores but only its share of the
+// columns of O (no combine).  Waves take the workgroup's 32-key blocks
+// round-robin.
 // Q arrives in float and the probabilities are formed in float; on bf16
 // models each enters the matrix cores as a pair of bf16 fragments (value and
 // rounding remainder, about 16 significant bits), so neither is rounded to
@@ -35,6 +38,9 @@ namespace sdsat {
 
 static constexpr int kMaxWaves = 8;
 static constexpr int kMaxSplits = 8;
+static constexpr int kMaxCols = 8;
+// caches of at most this many 32-key blocks use one split
+static constexpr int kOneSplitBlocks = 32;
 
 // Keys are partitioned by absolute 32-key block index only: split sp owns
 // blocks [sp * P, (sp + 1) * P) with P fixed by the cache capacity (at full
@@ -46,7 +52,10 @@ static constexpr int kMaxSplits = 8;
 // cannot see (later rows of its own block) add exact zeros.  So a token's
 // logits do not depend on how many draft rows share its block, and greedy
 // SDSAT reproduces autoregressive decoding bit for bit.  Waves per workgroup:
-// one per block of the split, at most 8.
+// one per block of the split, at most 8.  Column slices change which
+// workgroup writes a column of O, not how it is computed: each slice's values
+// are those of the single workgroup, bit for bit, so the slice count may
+// follow the block size.
 AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_max) {
     AttnPlan p;
     const int cap = std::max(1, S_max / 32);
@@ -54,14 +63,19 @@ AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_ma
     const int pairs = B * H;
     // one round of workgroups per row tile (a workgroup of 8 waves holds a compute unit's registers);
     // where that allows only two splits, one split without the combine is faster (measured at
-    // batch 4 x 32 heads: 26.4 -> 23.6 us per layer); more splits than one round is slower
+    // batch 4 x 32 heads: 26.4 -> 23.6 us per layer); more splits than one round is slower.  A short
+    // cache takes one split too: its column slices fill the round without a combine kernel.
     int target = std::max(1, std::min(kMaxSplits, 256 / pairs));
-    if (target <= 2) target = 1;
+    if (target <= 2 || cap <= kOneSplitBlocks) target = 1;
     p.per_split = (cap + target - 1) / target;
     p.splits = (nblk + p.per_split - 1) / p.per_split;
     p.row_tiles = (q + 15) / 16;
     p.waves = std::max(1, std::min(p.per_split, kMaxWaves));
-    p.grid = pairs * p.row_tiles * p.splits;
+    // column slices (one split, one row tile): as many as keep one round of 256 workgroups
+    p.cols = 1;
+    if (p.splits == 1 && p.row_tiles == 1)
+        while (p.cols * 2 <= std::min(kMaxCols, head_dim / 16) && pairs * p.cols * 2 <= 256) p.cols *= 2;
+    p.grid = pairs * p.row_tiles * p.splits * p.cols;
     p.lds_bytes = p.waves * (head_dim / 16) * 64 * 16;
     return p;
 }
@@ -76,7 +90,7 @@ size_t attention_partial_floats(int B, int H, int q_max, int head_dim) {
 // the register budget).
 template <typename T, int NDS, int NDT>
 __device__ __forceinline__ void load_kv(Frag<T> (&kf)[2][NDS], Frag<T> (&vf)[NDT], __amdgpu_buffer_rsrc_t kr,
-                                        __amdgpu_buffer_rsrc_t vr, int blk, int c, int g) {
+                                        __amdgpu_buffer_rsrc_t vr, int blk, int c, int g, uint32_t vsoff) {
     constexpr int DH = NDS * 32;
     constexpr uint32_t E = sizeof(T);
 #pragma unroll
@@ -87,7 +101,7 @@ __device__ __forceinline__ void load_kv(Frag<T> (&kf)[2][NDS], Frag<T> (&vf)[NDT
     }
     const uint32_t vo = ((uint32_t)blk * DH * 32 + c * 32 + 8 * g) * E;
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) vf[dt] = buf_frag<T>(vr, vo, dt * 16 * 32 * E);
+    for (int dt = 0; dt < NDT; ++dt) vf[dt] = buf_frag<T>(vr, vo, vsoff + dt * 16 * 32 * E);
 }
 
 // x as the matrix-core operand pair hi + lo (lo = the bf16 rounding remainder;
@@ -174,11 +188,12 @@ __device__ __forceinline__ void attend_block(const Frag<T> (&kf)[2][NDS], const 
     }
 }
 
-// One workgroup per (sequence, head, 16-row tile, key split).
-template <typename T, int DH>
+// One workgroup per (sequence, head, 16-row tile, key split, column slice).
+template <typename T, int DH, int CS>
 __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
-    constexpr int NDS = DH / 32;   // 32-wide steps over the head dimension
-    constexpr int NDT = DH / 16;   // 16-row output tiles over the head dimension
+    constexpr int NDS = DH / 32;        // 32-wide steps over the head dimension
+    constexpr int NDT = DH / 16 / CS;   // 16-row output tiles of this column slice
+    constexpr int RGN = DH / 16;        // f32x4 rows (of 64 lanes) in a wave's LDS region
     // Per wave DH * 64 bytes of LDS: its Q fragments of the row tile
     // ([hi / lo][ds][lane], read back in every block), then its partial O
     // ([dt][lane]) for the merge.
@@ -189,11 +204,18 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63, c = lane & 15, g = lane >> 4;
     Frag<T>* s_q = reinterpret_cast<Frag<T>*>(smem_raw + (size_t)wave * DH * 64);
-    const f32x4_t* opart = reinterpret_cast<const f32x4_t*>(smem_raw);   // [waves][NDT][64]
+    const f32x4_t* opart = reinterpret_cast<const f32x4_t*>(smem_raw);   // [waves][RGN][64]
     const int q = a.q;
     const int n_rt = (q + 15) / 16;
-    const int sp = blockIdx.x % a.splits, rt = (blockIdx.x / a.splits) % n_rt;
-    const int bh = blockIdx.x / (a.splits * n_rt);
+    // the column slice is the slowest index: the slices of one head sit on the same XCD (workgroups
+    // go to XCDs round-robin, and B * H * n_rt * splits is a multiple of 8 at the model shapes), so
+    // all but the first read its keys from that XCD's L2
+    const int n_in = a.B * a.H * n_rt * a.splits;
+    const int cx = CS == 1 ? 0 : (int)blockIdx.x / n_in;
+    const int bid = (int)blockIdx.x - cx * n_in;
+    const int sp = bid % a.splits, rt = (bid / a.splits) % n_rt;
+    const int bh = bid / (a.splits * n_rt);
+    const uint32_t vsoff = (uint32_t)(cx * NDT * 16 * 32 * sizeof(T));   // the slice's V columns
     const int b = bh / a.H, h = bh % a.H;
     const uint32_t slice_bytes = (uint32_t)a.S_max * DH * sizeof(T);
     const __amdgpu_buffer_rsrc_t kr =
@@ -235,13 +257,13 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
             qv[ds][1] = qsrc[ds * 8 + 1];
         }
         Frag<T> kA[2][NDS], kB[2][NDS], vA[NDT], vB[NDT];
-        load_kv<T, NDS, NDT>(kA, vA, kr, vr, min(first, last_blk), c, g);
+        load_kv<T, NDS, NDT>(kA, vA, kr, vr, min(first, last_blk), c, g, vsoff);
         // a wave of a split other than the last owns at most ceil(per_split / nw)
         // blocks: when that is one (decode at short contexts), its second block
         // is never used and is not requested (measured: 13.7 -> 13.0 us per
         // layer, 7B decode at context ~600)
         const bool second = sp == a.splits - 1 || a.per_split > nw;
-        if (second) load_kv<T, NDS, NDT>(kB, vB, kr, vr, min(first + nw, last_blk), c, g);
+        if (second) load_kv<T, NDS, NDT>(kB, vB, kr, vr, min(first + nw, last_blk), c, g, vsoff);
         __builtin_amdgcn_sched_barrier(0);   // keep the K/V requests ahead of the wait for Q
 #pragma unroll
         for (int ds = 0; ds < NDS; ++ds) {   // Q columns 32ds.. of the tile's rows as hi / lo
@@ -271,15 +293,15 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
         const int cnt = first < whi ? (whi - first + nw - 1) / nw : 0;
         // the loop below expects blocks 0 and 1 loaded; without the second request cnt <= 1, so this
         // only guards that invariant
-        if (!second && cnt >= 2) load_kv<T, NDS, NDT>(kB, vB, kr, vr, first + nw, c, g);
+        if (!second && cnt >= 2) load_kv<T, NDS, NDT>(kB, vB, kr, vr, first + nw, c, g, vsoff);
         int i = 0;
         // steady state (unconditional loads): blocks i and i + 1 are loaded
         for (; i + 4 <= cnt; i += 2) {
             attend_block<T, NDS, NDT>(kA, vA, s_q, lane, mrow, first + i * nw, m, L, Tb, q, tree, a.scale, g, rmax, rsum, o);
-            load_kv<T, NDS, NDT>(kA, vA, kr, vr, first + (i + 2) * nw, c, g);
+            load_kv<T, NDS, NDT>(kA, vA, kr, vr, first + (i + 2) * nw, c, g, vsoff);
             attend_block<T, NDS, NDT>(kB, vB, s_q, lane, mrow, first + (i + 1) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
                                       rsum, o);
-            load_kv<T, NDS, NDT>(kB, vB, kr, vr, first + (i + 3) * nw, c, g);
+            load_kv<T, NDS, NDT>(kB, vB, kr, vr, first + (i + 3) * nw, c, g, vsoff);
         }
         // 0 .. 3 blocks left, blocks i and i + 1 loaded.  Three left is its own
         // straight-line path, so its one load does not make the compiler wait
@@ -287,7 +309,7 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
         const int rem = cnt - i;
         if (rem == 3) {
             attend_block<T, NDS, NDT>(kA, vA, s_q, lane, mrow, first + i * nw, m, L, Tb, q, tree, a.scale, g, rmax, rsum, o);
-            load_kv<T, NDS, NDT>(kA, vA, kr, vr, first + (i + 2) * nw, c, g);
+            load_kv<T, NDS, NDT>(kA, vA, kr, vr, first + (i + 2) * nw, c, g, vsoff);
             attend_block<T, NDS, NDT>(kB, vB, s_q, lane, mrow, first + (i + 1) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
                                       rsum, o);
             attend_block<T, NDS, NDT>(kA, vA, s_q, lane, mrow, first + (i + 2) * nw, m, L, Tb, q, tree, a.scale, g, rmax,
@@ -334,9 +356,9 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
             f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int w = 0; w < kMaxWaves; ++w)
-                if (w < nw) acc += opart[(w * NDT + dt) * 64 + lane] * alpha[w];
+                if (w < nw) acc += opart[(w * RGN + dt) * 64 + lane] * alpha[w];
             if (m >= q) continue;
-            const int d = 16 * dt + 4 * g;
+            const int d = 16 * (cx * NDT + dt) + 4 * g;
             if (a.splits > 1) {
                 // partial of this workgroup: O scaled to its row maximum, the maximum, the sum
                 float* pr = a.part + (((size_t)bh * a.splits + sp) * (n_rt * 16) + m) * (DH + 4);
@@ -417,11 +439,14 @@ __global__ void __launch_bounds__(64) attn_combine_kernel(AttnArgs a, int rows) 
 template <typename T, int DH>
 static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     const bool comb = a.splits > 1;
+    void (*kern)(AttnArgs) = attn_kernel<T, DH, 1>;
+    if (p.cols == 2) kern = attn_kernel<T, DH, 2>;
+    else if (p.cols == 4) kern = attn_kernel<T, DH, 4>;
+    else if constexpr (DH / 16 >= 8) { if (p.cols == 8) kern = attn_kernel<T, DH, 8>; }
     if (ev0)
-        hipExtLaunchKernelGGL(attn_kernel<T, DH>, dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, ev0,
-                              comb ? nullptr : ev1, 0, a);
+        hipExtLaunchKernelGGL(kern, dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, ev0, comb ? nullptr : ev1, 0, a);
     else
-        hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, a);
+        hipLaunchKernelGGL(kern, dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !comb) return e;
     const int n = a.B * a.H * a.q * (DH / 4);
@@ -435,8 +460,9 @@ hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const At
                             hipEvent_t ev0, hipEvent_t ev1) {
     if (a.q < 1 || a.q > 4096 || (a.mask && a.q > 64) || p.waves < 1 || p.waves > kMaxWaves || a.splits < 1 || a.splits > kMaxSplits ||
         a.splits != p.splits || (a.splits > 1 && !a.part) || p.row_tiles != (a.q + 15) / 16 ||
-        p.grid != a.B * a.H * a.splits * p.row_tiles || a.ldo % 4 != 0 ||
-        a.per_split != p.per_split || a.per_split < 1)
+        p.grid != a.B * a.H * a.splits * p.row_tiles * p.cols || a.ldo % 4 != 0 ||
+        a.per_split != p.per_split || a.per_split < 1 || a.cols != p.cols || p.cols < 1 || p.cols > kMaxCols ||
+        (p.cols & (p.cols - 1)) != 0 || p.cols > head_dim / 16 || (p.cols > 1 && a.splits != 1))
         return hipErrorInvalidValue;
     if (dtype == 1) {
         if (head_dim == 128) return launch_dh<uint16_t, 128>(p, a, s, ev0, ev1);

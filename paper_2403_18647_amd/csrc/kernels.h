@@ -91,14 +91,16 @@ struct AttnArgs {
     int B, q, H, S_max;
     float scale;
     int splits;              // workgroups per (b, h); > 1: partials to `part`, then a combine kernel
+    int cols;                // column slices (splits == 1 only): workgroups per (b, h) that each write
+                             // Dh / cols columns of O
     float* part;             // [B*H][splits][16*MT rows][Dh + 4]: unnormalised O, row max, row sum
     void* out;               // T (or float if out_f32) [B*q][ldo], head h at columns h*Dh..
     int out_f32, ldo;
     int* err;                // device error flags (bit 4: read past the cache)
 };
-// `splits` workgroups of `waves` waves per (sequence, head, 16-row tile); max_len: the host's
-// upper bound of the cache lengths; S_max: key slots per sequence
-struct AttnPlan { int waves, splits, per_split, row_tiles, grid, lds_bytes; };
+// `splits` x `cols` workgroups of `waves` waves per (sequence, head, 16-row tile); max_len: the
+// host's upper bound of the cache lengths; S_max: key slots per sequence
+struct AttnPlan { int waves, splits, per_split, row_tiles, grid, lds_bytes, cols; };
 AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_max);
 size_t attention_partial_floats(int B, int H, int q_max, int head_dim);
 // ev0 / ev1 (optional): start of the attention kernel, end of the last kernel of the call
