@@ -50,6 +50,7 @@ constexpr int kMaxBlock = 4096;   // rows per sequence per block
 constexpr int kSkinnyRows = 64;   // blocks of at most this many rows (B*q) run the skinny GEMM kernels
 constexpr int kRecLoops = 64;     // generation loops enqueued between two host synchronisations, at most
 constexpr int kPreRoundRows = 1;  // blocks of more rows round normalised GEMM inputs once (rms_rows)
+constexpr int kQkvFloatRows = 8;  // except the QKV GEMM, which reads the float rows up to this many
 
 int make_dims(const sdsat_config* c, Dims* D, std::string* why) {
     if (!c) { *why = "config is NULL"; return SDSAT_EINVAL; }
@@ -376,14 +377,16 @@ int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const 
     const int M = B * q;
     if (M > kSkinnyRows) return large_block_impl(c, B, q, tokens, logits);
     // The GEMMs behind an RMSNorm read X either as the float rows x o g, scaled
-    // and rounded at the matrix-core input (one-row blocks), or as those rows
-    // rounded once by rms_rows: every workgroup re-reads X, and the float rows
-    // of even a 6-row block cost more than the extra launch.  Both give the
-    // same element-type values (same partial-sum order, same rounding).
-    const bool pre = M > kPreRoundRows;
-    auto norm_input = [&](GemmArgs& g) -> int {
+    // and rounded at the matrix-core input (one-row blocks; QKV up to 8 rows),
+    // or as those rows rounded once by rms_rows: every workgroup re-reads X.
+    // Both give the same element-type values (same partial-sum order, same
+    // rounding).  Measured on the 7B shape at 6 rows: the QKV GEMM's 768
+    // workgroups re-reading float rows cost less than an rms_rows launch (block
+    // 3.154 -> 3.148 ms), gate/up's 1376 more (3.154 -> 3.194 ms); at 13B's 11
+    // rows QKV also loses (6.86 -> 7.14 ms).
+    auto norm_input = [&](GemmArgs& g, int float_rows) -> int {
         g.ldx = D.d_pad;
-        if (!pre) {
+        if (M <= float_rows) {
             g.xf = c->xg; g.ssq = c->ssq; g.n_ssq = D.n_ssq; g.eps = c->cfg.rms_eps;
             return SDSAT_OK;
         }
@@ -400,7 +403,7 @@ int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const 
         // attention sub-block: RMSNorm -> QKV (+RoPE, KV write) -> attention -> O (+residual);
         // xg holds x o (the gain of the RMSNorm the next GEMM applies)
         GemmArgs a{};
-        int rc = norm_input(a);
+        int rc = norm_input(a, kQkvFloatRows);
         if (rc) return rc;
         a.qbuf = c->qbuf; a.kc = layer_k(c, l); a.vc = layer_v(c, l);
         a.cache_len = c->cache_len; a.q = q; a.H = D.H; a.Dh = D.Dh; a.S_max = D.S; a.mask = mask;
@@ -416,7 +419,7 @@ int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const 
         if (rc) return rc;
         // feed-forward sub-block: RMSNorm -> gate/up (+SwiGLU) -> down (+residual)
         GemmArgs f{};
-        rc = norm_input(f);
+        rc = norm_input(f, kPreRoundRows);
         if (rc) return rc;
         f.uout = c->ubuf; f.F = D.F; f.ldu = D.F_pad;
         rc = run_gemm(c, PK_GATEUP, EP_SWIGLU, M, D.nt_gu, D.ks_d, 2 * D.F, D.d, c->w_gu[l], f);
@@ -429,7 +432,7 @@ int forward_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, const 
     }
     if (logits) {
         GemmArgs h{};
-        int rc = norm_input(h);
+        int rc = norm_input(h, kPreRoundRows);
         if (rc) return rc;
         h.y = logits; h.ldy = D.V;
         rc = run_gemm(c, PK_LM, EP_STORE, M, D.nt_lm, D.ks_d, D.V, D.d, c->w_lm, h);
