@@ -113,6 +113,7 @@ struct sdsat_ctx {
     void* qbuf = nullptr; void* obuf = nullptr; void* ubuf = nullptr;
     // scratch
     float* attn_part = nullptr;
+    float* gemm_part = nullptr;   // partial tiles of split residual GEMMs
     int* cache_len = nullptr; int* err_flag = nullptr; int* verify_cnt = nullptr;
     // generation buffers
     int *tok1 = nullptr, *out1 = nullptr, *out2 = nullptr, *n_accept = nullptr, *pending = nullptr;
@@ -184,6 +185,12 @@ void carve(sdsat_ctx* c, Carver& cv) {
     c->obuf = cv.take((size_t)D.maxM * D.d_pad * e);
     c->ubuf = cv.take((size_t)D.maxM * D.F_pad * e);
     c->attn_part = (float*)cv.take(attention_partial_floats(D.maxB, D.H, D.maxQ, D.Dh) * 4);
+    {
+        const int rows = std::min(D.maxM, kSkinnyRows);
+        const size_t part = std::max(gemm_resid_part_bytes(D.nt_o, D.ks_d, rows),
+                                     gemm_resid_part_bytes(D.nt_down, D.ks_f, rows));
+        c->gemm_part = part ? (float*)cv.take(part) : nullptr;
+    }
     c->cache_len = (int*)cv.take((size_t)D.maxB * 4);
     c->err_flag = (int*)cv.take(4);
     c->verify_cnt = (int*)cv.take((size_t)D.maxB * 4);
@@ -262,8 +269,9 @@ void prof_end(sdsat_ctx* c, hipEvent_t start) {
 // ---------------------------------------------------------------- GEMM helpers
 int run_gemm(sdsat_ctx* c, int kind, int ep, int M, int n_tiles, int k_steps, int N, int K, const void* W,
              GemmArgs a) {
-    const GemmPlan p = plan_gemm(M, n_tiles, k_steps);
+    const GemmPlan p = ep == EP_RESID ? plan_gemm_resid(M, n_tiles, k_steps) : plan_gemm(M, n_tiles, k_steps);
     a.M = M; a.N = N; a.K = K; a.n_tiles = n_tiles; a.k_steps = k_steps; a.W = W; a.err = c->err_flag;
+    a.ksplit = p.ksplit; a.part = c->gemm_part;
     hipEvent_t e0, e1;
     prof_pair(c, kind, &e0, &e1);
     HIPCHK(c, launch_gemm(c->D.dtype, ep, p, a, c->stream, e0, e1));

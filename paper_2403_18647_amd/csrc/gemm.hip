@@ -20,6 +20,10 @@
 //    before its first matrix-core step and rounds x o g / rms to the element
 //    type at the matrix-core input.  Both give the normalised activation a bf16
 //    model stores, rounded once, bit for bit the same.
+//  * Residual GEMMs whose tile count would leave some compute units a second
+//    workgroup (13B: 320 tiles on 256 units) spread each tile's waves over
+//    several workgroups and fold the waves' partial tiles in a second kernel,
+//    in the same wave order (plan_gemm_resid).
 //  * Fused epilogues, run by wave 0 on the reduced tile:
 //      EP_STORE   float output (LM-head logits)
 //      EP_QKV     RoPE on Q and K columns, Q (float) to its buffer, K and V into
@@ -28,6 +32,7 @@
 //                 times the next RMSNorm's gain, and per-tile sums of squares
 //                 that the next RMSNorm reduces
 //      EP_SWIGLU  silu(gate) * up, rounded to the activation type
+#include <algorithm>
 #include <type_traits>
 
 #include "device.h"
@@ -104,7 +109,43 @@ GemmPlan plan_gemm(int M, int n_tiles, int k_steps) {
     p.waves = w;
     p.grid = (n_tiles + p.ntw - 1) / p.ntw;
     p.lds_bytes = w * p.mt * 64 * 16;
+    p.ksplit = 1;
     return p;
+}
+
+// Residual GEMMs (O, down) of narrow matrices whose tile count is not a
+// multiple of the 256 compute units (13B: 320 tiles) leave some units two
+// workgroups and the rest one.  Their tiles' waves are then spread over
+// ksplit workgroups (320 x 4 = 1280 workgroups of 2 waves, 5 per unit); each
+// wave keeps its slice of the contraction, and a fold kernel adds the waves'
+// partial tiles in wave order, as the single workgroup's LDS reduction does,
+// so the results are the same bit for bit.  Measured at 13B, 11 rows: down
+// (432 contraction steps) 39.4 -> 32.6 us; O (160 steps) 16.6 -> 17.1 us, its
+// waves' work too short to cover the fold kernel's launch, so it stays whole.
+GemmPlan plan_gemm_resid(int M, int n_tiles, int k_steps) {
+    GemmPlan p = plan_gemm(M, n_tiles, k_steps);
+    if (p.ntw != 1 || n_tiles <= 256 || k_steps < 256) return p;
+    auto spread = [&](int k) {   // workgroup rounds over the average, per compute unit
+        const long n = (long)n_tiles * k;
+        return (double)((n + 255) / 256) * 256.0 / (double)n;
+    };
+    int best = 1;
+    for (int k = 2; k <= p.waves; k *= 2)
+        if (spread(k) < spread(best) - 1e-9) best = k;
+    p.ksplit = best;
+    p.waves /= best;
+    p.grid = n_tiles * best;
+    p.lds_bytes = p.waves * p.mt * 64 * 16;
+    return p;
+}
+
+size_t gemm_resid_part_bytes(int n_tiles, int k_steps, int max_rows) {
+    size_t most = 0;
+    for (int m = 1; m <= std::min(std::max(max_rows, 1), 64); m += 16) {
+        const GemmPlan p = plan_gemm_resid(std::min(m + 15, std::min(std::max(max_rows, 1), 64)), n_tiles, k_steps);
+        if (p.ksplit > 1) most = std::max(most, (size_t)n_tiles * p.waves * p.ksplit * p.mt * 64 * 16);
+    }
+    return most;
 }
 
 // Steps per load batch (two batches in flight), sized so both batches of
@@ -275,12 +316,17 @@ __global__ void __launch_bounds__(NTW > 1 ? 256 : 512) gemm_kernel(GemmArgs a) {
     const int nw = blockDim.x >> 6;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int c = lane & 15, g = lane >> 4;
-    const int tile0 = blockIdx.x * NTW;
     const int M = a.M;
+    // a split residual GEMM: workgroup (kpart, tile) holds waves kpart * nw .. of the tile's nwt
+    const bool split = EP == EP_RESID && NTW == 1 && a.ksplit > 1;
+    const int kpart = split ? (int)blockIdx.x / a.n_tiles : 0;
+    const int tile0 = split ? (int)blockIdx.x - kpart * a.n_tiles : (int)blockIdx.x * NTW;
+    const int nwt = split ? nw * a.ksplit : nw;
+    const int gw = kpart * nw + wave;
 
     // this wave's contiguous slice of the contraction steps
-    const int chunk = (a.k_steps + nw - 1) / nw;
-    const int ks0 = wave * chunk;
+    const int chunk = (a.k_steps + nwt - 1) / nwt;
+    const int ks0 = gw * chunk;
     const int nks = max(0, min(a.k_steps, ks0 + chunk) - ks0);
     const T* wp[NTW];
 #pragma unroll
@@ -314,7 +360,7 @@ __global__ void __launch_bounds__(NTW > 1 ? 256 : 512) gemm_kernel(GemmArgs a) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) ep_in[j][mt][r] = 0.f;
     }
-    if (wave == 0) {
+    if (wave == 0 && !split) {
 #pragma unroll
         for (int j = 0; j < NTW; ++j) {
             const int tile = tile0 + j;
@@ -406,6 +452,13 @@ __global__ void __launch_bounds__(NTW > 1 ? 256 : 512) gemm_kernel(GemmArgs a) {
         if (s + 3 * U < nks) mma_batch<T, XF, XT, MT, NTW, U>(acc, w1, x1, inv);
     }
 
+    if (split) {   // raw partial tile of this wave, folded by gemm_fold_kernel
+        f32x4_t* pp = reinterpret_cast<f32x4_t*>(a.part) + ((size_t)tile0 * nwt + gw) * MT * 64 + lane;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) pp[mt * 64] = acc[0][mt];
+        return;
+    }
+
     // cross-wave reduction in wave order, one tile at a time (LDS holds
     // waves x MT fragments); wave 0 runs the tile's epilogue
 #pragma unroll
@@ -427,12 +480,41 @@ __global__ void __launch_bounds__(NTW > 1 ? 256 : 512) gemm_kernel(GemmArgs a) {
     }
 }
 
+// Split residual GEMM, second pass: one wave per column tile adds the nwt
+// waves' partial tiles in wave order (v = p0, then v += p1, p2, ...: the
+// single workgroup's LDS reduction) and runs the EP_RESID epilogue on the sum.
+template <typename T, int MT>
+__global__ void __launch_bounds__(64) gemm_fold_kernel(GemmArgs a, int nwt) {
+    const int tile = blockIdx.x, lane = threadIdx.x, c = lane & 15, g = lane >> 4;
+    const int M = a.M, n = tile * 16 + c;
+    float ep_in[MT][4];
+    const f32x4_t* pp = reinterpret_cast<const f32x4_t*>(a.part) + (size_t)tile * nwt * MT * 64 + lane;
+    f32x4_t t_acc[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int m = 16 * mt + 4 * g + r;
+            ep_in[mt][r] = (m < M && n < a.N) ? a.resid[(size_t)m * a.ldy + n] : 0.f;
+        }
+        f32x4_t v = pp[mt * 64];
+        for (int w = 1; w < nwt; ++w) v += pp[(w * MT + mt) * 64];
+        t_acc[mt] = v;
+    }
+    const float gn = n < a.N ? a.gnext[n] : 0.f;
+    epilogue<T, EP_RESID, MT>(a, tile, t_acc, ep_in, gn, c, g);
+}
+
 template <typename T, int EP, bool XF>
 static hipError_t launch_mt(const GemmPlan& p, const GemmArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     const dim3 grid(p.grid), block(64 * p.waves);
     if (p.waves > (p.ntw > 1 ? 4 : 8)) return hipErrorInvalidValue;
+    const bool split = p.ksplit > 1;
+    if (split && (EP != EP_RESID || p.ntw != 1 || !a.part || a.ksplit != p.ksplit || p.grid != a.n_tiles * p.ksplit))
+        return hipErrorInvalidValue;
+    if (!split && a.ksplit > 1) return hipErrorInvalidValue;
     auto go = [&](auto kernel) {
-        if (ev0) hipExtLaunchKernelGGL(kernel, grid, block, p.lds_bytes, s, ev0, ev1, 0, a);
+        if (ev0) hipExtLaunchKernelGGL(kernel, grid, block, p.lds_bytes, s, ev0, split ? nullptr : ev1, 0, a);
         else hipLaunchKernelGGL(kernel, grid, block, p.lds_bytes, s, a);
     };
     switch (p.mt * 10 + p.ntw) {
@@ -444,6 +526,24 @@ static hipError_t launch_mt(const GemmPlan& p, const GemmArgs& a, hipStream_t s,
         case 34: go(gemm_kernel<T, EP, 3, 4, XF>); break;
         case 44: go(gemm_kernel<T, EP, 4, 4, XF>); break;
         default: return hipErrorInvalidValue;
+    }
+    if constexpr (EP == EP_RESID && !XF) {
+        if (split) {
+            const hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            const int nwt = p.waves * p.ksplit;
+            auto fold = [&](auto kernel) {
+                if (ev0) hipExtLaunchKernelGGL(kernel, dim3(a.n_tiles), dim3(64), 0, s, nullptr, ev1, 0, a, nwt);
+                else hipLaunchKernelGGL(kernel, dim3(a.n_tiles), dim3(64), 0, s, a, nwt);
+            };
+            switch (p.mt) {
+                case 1: fold(gemm_fold_kernel<T, 1>); break;
+                case 2: fold(gemm_fold_kernel<T, 2>); break;
+                case 3: fold(gemm_fold_kernel<T, 3>); break;
+                case 4: fold(gemm_fold_kernel<T, 4>); break;
+                default: return hipErrorInvalidValue;
+            }
+        }
     }
     return hipGetLastError();
 }

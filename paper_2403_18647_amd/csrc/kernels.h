@@ -69,12 +69,21 @@ struct GemmArgs {
     const float* rope;                   // [S_max][Dh/2][2] rotary cos, sin of position x base^(-2i/Dh)
     void* uout; int F; int ldu;          // EP_SWIGLU: T [M][ldu]
     int* err;                            // device error flags (bit 4: write past the cache)
+    // EP_RESID split over ksplit workgroups per tile (ksplit > 1): every wave's raw partial tile goes to
+    // part [n_tiles][waves * ksplit][MT][64] (f32x4), folded in wave order by a second kernel
+    int ksplit; float* part;
 };
 
 struct GemmPlan {
-    int waves, mt, ntw, grid, lds_bytes;   // ntw: 16-column tiles per workgroup
+    int waves, mt, ntw, grid, lds_bytes;   // ntw: 16-column tiles per workgroup; waves per workgroup
+    int ksplit;                            // workgroups per column tile (EP_RESID only), 1 = one
 };
 GemmPlan plan_gemm(int M, int n_tiles, int k_steps);
+// The residual GEMMs' plan with each tile's waves spread over ksplit workgroups where that balances
+// the compute units (same wave slices, same fold order: the same values).
+GemmPlan plan_gemm_resid(int M, int n_tiles, int k_steps);
+// bytes of the partial-tile buffer the residual GEMMs of this shape need (0: never split)
+size_t gemm_resid_part_bytes(int n_tiles, int k_steps, int max_rows);
 // ev0 / ev1 (optional): events taken at the kernel's own start and end (its
 // dispatch packet's timestamps), for timing one launch
 hipError_t launch_gemm(int dtype, int ep, const GemmPlan& p, const GemmArgs& a, hipStream_t s,
