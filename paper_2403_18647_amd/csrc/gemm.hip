@@ -95,15 +95,18 @@ void launch_pack(const PackArgs& a, hipStream_t s) {
 //    (several tiles per workgroup, or X staged in LDS, measured slower);
 //  * blocks of more than 16 rows (batch 4 decode, prefill chunks) reload their
 //    X fragments for every weight fragment: for the wide matrices a workgroup
-//    of 4 waves takes 4 column tiles so that one X load feeds 4 tiles'
-//    matrix-core steps (M = 64: QKV 55 -> 37 us, gate/up 103 -> 62 us); the
-//    narrow ones keep one tile per workgroup.  The waves per workgroup depend
-//    on the matrix shape only where block-size invariance needs it: one row
-//    tile and four column tiles both use 4 waves on the wide matrices.
+//    of 4 waves takes several column tiles so that one X load feeds their
+//    matrix-core steps: 4 (M = 64: QKV 55 -> 37 us, gate/up 103 -> 62 us), or
+//    2 for two row tiles, which keeps more workgroups than compute units
+//    (batch 4 x 6 rows: QKV 192 -> 384 workgroups, 34.4 -> 31.5 us; gate/up
+//    47.5 -> 42.1 us; block 4.92 -> 4.67 ms); the narrow ones keep one tile
+//    per workgroup.  The waves per workgroup depend on the matrix shape only
+//    where block-size invariance needs it: one row tile and several column
+//    tiles both use 4 waves on the wide matrices.
 GemmPlan plan_gemm(int M, int n_tiles, int k_steps) {
     GemmPlan p;
     p.mt = (M + 15) / 16;
-    p.ntw = (p.mt > 1 && n_tiles > 512) ? 4 : 1;
+    p.ntw = (p.mt > 1 && n_tiles > 512) ? (p.mt == 2 ? 2 : 4) : 1;
     int w = p.ntw > 1 ? 4 : (n_tiles <= 512 ? 8 : 4);
     while (w > 1 && k_steps < 4 * w) w /= 2;
     p.waves = w;
@@ -522,6 +525,7 @@ static hipError_t launch_mt(const GemmPlan& p, const GemmArgs& a, hipStream_t s,
         case 21: go(gemm_kernel<T, EP, 2, 1, XF>); break;
         case 31: go(gemm_kernel<T, EP, 3, 1, XF>); break;
         case 41: go(gemm_kernel<T, EP, 4, 1, XF>); break;
+        case 22: go(gemm_kernel<T, EP, 2, 2, XF>); break;
         case 24: go(gemm_kernel<T, EP, 2, 4, XF>); break;
         case 34: go(gemm_kernel<T, EP, 3, 4, XF>); break;
         case 44: go(gemm_kernel<T, EP, 4, 4, XF>); break;
