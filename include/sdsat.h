@@ -241,8 +241,9 @@ int sdsat_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const float* d_
  * 7 whole block forward with logits (draft / verify blocks), 8 whole block
  * forward without logits (prefill).  period >= 1: one launch of that kind in
  * every `period` is timed.  Kinds 1-6 take their events from the kernel's own
- * dispatch (start and end of the kernel, or of the attention kernel and its
- * split combine), the interval a kernel trace reports; kinds 7 and 8 record a
+ * dispatch (start and end of the kernel, or of the first and last kernel of a
+ * pair: attention and its split combine, a split GEMM and its fold), the
+ * interval a kernel trace reports; kinds 7 and 8 record a
  * pair of events around the block (each pair costs a few microseconds of
  * queue time, so a period > 1 keeps timed runs undisturbed).
  * sdsat_kernel_time synchronizes the stream and returns the summed
