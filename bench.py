@@ -292,8 +292,8 @@ def main():
                          "size, for scaling hardware traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: this build runs the decode path on a single MI355X "
-              "(the path would shard data-parallel over sequences; no multi-GPU run is part of it)",
+        print("bench.py measures one GPU: the library drives the decode path on a single MI355X per "
+              "process (the path would shard data-parallel over sequences; there is no multi-GPU run)",
               file=sys.stderr)
         sys.exit(2)
 
@@ -377,7 +377,7 @@ def main():
     bblk = block_bytes(sh, wl.batch, q, avg_ctx)
     blk_gbs = bblk / (per_block_ms / 1e3) / 1e9
 
-    # in-build autoregressive baseline: the same kernels with k = 0 (one token per block forward)
+    # in-library autoregressive baseline: the same kernels with k = 0 (one token per block forward)
     ar = None
     if not args.no_ar_baseline:
         t0 = time.perf_counter()
