@@ -153,9 +153,13 @@ size_t gemm_resid_part_bytes(int n_tiles, int k_steps, int max_rows) {
 
 // Steps per load batch (two batches in flight), sized so both batches of
 // weight and X fragments fit the register budget (float X fragments of an
-// RMSNorm input take twice the registers of bf16 ones).
-template <typename T, int MT, bool XF> struct Batch {
-    static constexpr int U = MT == 1 ? (sizeof(T) == 2 ? (XF ? 3 : 4) : 2) : (sizeof(T) == 2 && !XF ? 2 : 1);
+// RMSNorm input take twice the registers of bf16 ones).  The QKV GEMM on float
+// rows takes 4 (142 VGPRs: its 3 workgroups of 4 waves per compute unit stay
+// resident; 7B, 6 rows: 22.1 -> 21.2 us); the other float-row GEMMs keep 3
+// (gate/up, 1376 workgroups, loses occupancy at 4: 32.4 -> 33.2 us at one row).
+template <typename T, int EP, int MT, bool XF> struct Batch {
+    static constexpr int U = MT == 1 ? (sizeof(T) == 2 ? (XF ? (EP == EP_QKV ? 4 : 3) : 4) : 2)
+                                     : (sizeof(T) == 2 && !XF ? 2 : 1);
 };
 
 // X fragment as loaded: the element type, or raw floats of an RMSNorm input.
@@ -310,7 +314,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int tile, const f32x
 template <typename T, int EP, int MT, int NTW, bool XF>
 // Workgroups of several tiles have 4 waves, the others at most 8.
 __global__ void __launch_bounds__(NTW > 1 ? 256 : 512) gemm_kernel(GemmArgs a) {
-    constexpr int U = Batch<T, MT, XF>::U;
+    constexpr int U = Batch<T, EP, MT, XF>::U;
     using XT = typename XIn<T, XF>::type;
     extern __shared__ __align__(16) unsigned char smem_raw[];
     f32x4_t* red = reinterpret_cast<f32x4_t*>(smem_raw);   // [waves][MT][64]
