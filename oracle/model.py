@@ -33,8 +33,10 @@ def bf16_round(x: np.ndarray) -> np.ndarray:
     A bf16 value is a float32 whose low 16 bits are zero; rounding goes
     float64 -> bf16 directly (no double rounding through float32).
     """
-    x = np.asarray(x, np.float64)
-    out = np.empty_like(x)
+    # C-contiguous copies, so that the flat views below alias ``out`` (a view of
+    # a transposed or strided array would be a copy, never written back)
+    x = np.ascontiguousarray(x, np.float64)
+    out = np.empty(x.shape, np.float64)
     flat, res = x.reshape(-1), out.reshape(-1)
     m, e = np.frexp(flat)                       # flat = m * 2**e, 0.5 <= |m| < 1
     # bf16 keeps 8 significant bits: scale so that the kept bits are integral

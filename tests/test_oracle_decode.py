@@ -196,6 +196,25 @@ def test_sampler_ties_at_threshold_are_all_kept():
     assert list(ids) == [0, 1, 2, 3]
 
 
+def test_top_k_keeps_exactly_k_ids_lower_ids_first_among_ties():
+    """Top-k with a tie at the cut keeps exactly k ids, the lower ids first (the
+    reading taken for the order of temperature, top-k and top-p): z = [1, 3, 2,
+    3, 2, 0] with k = 3 keeps ids 1 and 3 (value 3) and id 2 (the lower of the two
+    2s), never id 4.  With top-p 1 the nucleus is that set, weighted e^(z - 3)."""
+    lg = np.array([1.0, 3.0, 2.0, 3.0, 2.0, 0.0], np.float32)
+    ids, e, _ = S.nucleus_set(lg, 1.0, 1.0, 3)
+    assert list(ids) == [1, 2, 3]
+    np.testing.assert_allclose(e, [1.0, math.exp(-1.0), 1.0], rtol=1e-15)
+    # ascending-id inverse CDF over {1, 2, 3}: u just past the first id's mass picks id 2
+    tot = 2.0 + math.exp(-1.0)
+    assert S.sample(lg, 1.0, 1.0, 3, 0.999 / tot)[0] == 1
+    assert S.sample(lg, 1.0, 1.0, 3, 1.001 / tot)[0] == 2
+    assert S.sample(lg, 1.0, 1.0, 3, (1.0 + math.exp(-1.0)) * 1.001 / tot)[0] == 3
+    # top_k = 2 keeps both 3s; top_k = 4 keeps both 2s as well
+    assert list(S.nucleus_set(lg, 1.0, 1.0, 2)[0]) == [1, 3]
+    assert list(S.nucleus_set(lg, 1.0, 1.0, 4)[0]) == [1, 2, 3, 4]
+
+
 # ---------------------------------------------------------------- nucleus SDSAT
 def _peaked_tiny():
     sh = synth.small_shape(n_layers=2, d_model=64, n_heads=2, head_dim=32, d_ffn=128,

@@ -289,3 +289,159 @@ def test_out_of_range_token_rejected():
     with pytest.raises(ValueError):
         M.forward_block(sh, w, M.KVCache(sh.n_layers, sh.n_heads, sh.head_dim),
                         [sh.vocab + sh.n_adaptive], [0])
+
+
+def test_bf16_round_of_strided_and_transposed_arrays():
+    """Rounding is elementwise whatever the memory layout: a transposed or strided
+    view rounds to the same values as a C-contiguous copy of it."""
+    rng = np.random.default_rng(9)
+    a = rng.standard_normal((6, 4)) * 37.0
+    for view in (a.T, a[::2, ::-1], np.asfortranarray(a)):
+        ref = M.bf16_round(np.ascontiguousarray(view))
+        got = M.bf16_round(view)
+        np.testing.assert_array_equal(got, ref)
+        assert np.abs(got - view).max() <= np.abs(view).max() * 2.0 ** -8
+
+
+# ---------------------------------------------------------------- bf16 rounding points, hand-built models
+# Each model below uses embedding rows of +-1 entries (RMS 1, so RMSNorm leaves
+# them unchanged), eps 0, every token at position 0 (rotary embedding is the
+# identity), and float32 weights that are exact binary fractions.  One storage
+# rounding of the bf16 model turns a value that is not a bf16 number into one
+# that is, and a cancellation right after it makes the difference decide a
+# logit exactly.  bf16 keeps 8 significant bits: near 1 its spacing is 2**-7,
+# so 1 + e rounds to 1 for |e| < 2**-8.
+def _bf16_shape(**kw):
+    base = dict(n_layers=1, d_model=4, n_heads=1, head_dim=4, d_ffn=2, vocab=4, n_adaptive=0,
+                rms_eps=0.0, rope_base=10000.0, dtype="bf16")
+    base.update(kw)
+    return SimpleNamespace(**base)
+
+
+def _run_at_position_zero(sh, W, cached, query, bf16):
+    """Commit the tokens ``cached`` one at a time, then run ``query`` as a one-row
+    block; every row at position 0."""
+    w = M.Weights(sh, W)
+    cache = M.KVCache(sh.n_layers, sh.n_heads, sh.head_dim)
+    for t in cached:
+        _, kv = M.forward_block(sh, w, cache, [t], [0], bf16=bf16)
+        cache.commit(kv, [0])
+    logits, _ = M.forward_block(sh, w, cache, [query], [0], bf16=bf16)
+    return logits[0]
+
+
+def test_bf16_attention_norm_output_is_rounded():
+    """The first RMSNorm's output is stored in bf16.  Gain 1 + 2**-9 on dimension 0
+    rounds to 1, so Q_0 = h_0 - h_1 is exactly 0: the two keys (K_0 = -512 and
+    +512) get equal weight, the values -1 and +1 average to 0, and the residual
+    stream keeps the embedding [1, 1, 1, 1]; logit 0 reads h_0 - h_1 of the final
+    norm = 0.  Unrounded, Q_0 = 2**-9 makes the self weight sigmoid(1)."""
+    sh = _bf16_shape()
+    W = _zero_weights(sh)
+    W["embed"][0] = [1, 1, 1, 1]         # the query token
+    W["embed"][1] = [1, 1, -1, 1]        # the cached key
+    W["l0.attn_norm"][:] = [1 + 2.0 ** -9, 1, 1, 1]
+    W["l0.wq"][0] = [1, -1, 0, 0]
+    W["l0.wk"][0] = [0, 0, 512, 0]
+    W["l0.wv"][0] = [0, 0, 1, 0]
+    W["l0.wo"][0] = [1, 0, 0, 0]
+    W["lm_head"][0] = [1, -1, 0, 0]
+    W["lm_head"][1] = [0, 1, 0, 0]
+    lg = _run_at_position_zero(sh, W, [1], 0, bf16=True)
+    assert lg[0] == 0.0 and lg[1] == 1.0
+    # without the storage roundings the same model moves logit 0: the construction sees the rounding
+    assert abs(_run_at_position_zero(sh, W, [1], 0, bf16=False)[0]) > 0.1
+
+
+def test_bf16_attention_output_is_rounded():
+    """The attention output is stored in bf16.  Uniform weights over three keys
+    with V_0 = 1 + 2**-7, 1, 1 average to 1 + 2**-7/3, which rounds to 1; the
+    output projection adds it to x_0 = -1, leaving exactly 0 there, which logit 0
+    reads through the final norm (bf16(0) = 0)."""
+    sh = _bf16_shape()
+    W = _zero_weights(sh)
+    W["embed"][0] = [-1, 1, 1, 1]        # query, V_0 = -a + b = 1
+    W["embed"][1] = [1, 1, 1, 1]         # V_0 = a + b = 1 + 2**-7
+    W["embed"][2] = [-1, 1, -1, -1]      # V_0 = 1
+    W["l0.wv"][0] = [2.0 ** -8, 1 + 2.0 ** -8, 0, 0]
+    W["l0.wo"][0] = [1, 0, 0, 0]
+    W["lm_head"][0] = [1, 0, 0, 0]
+    lg = _run_at_position_zero(sh, W, [1, 2], 0, bf16=True)
+    assert lg[0] == 0.0
+    assert _run_at_position_zero(sh, W, [1, 2], 0, bf16=False)[0] != 0.0
+
+
+def test_bf16_swiglu_product_is_rounded():
+    """The SwiGLU product is stored in bf16: silu(16) * 2**-4 = 1 - 1.1e-7 rounds to
+    1, the down projection adds it to x_0 = -1, and logit 0 reads exactly 0."""
+    sh = _bf16_shape()
+    W = _zero_weights(sh)
+    W["embed"][0] = [-1, 1, 1, 1]
+    W["l0.w_gate"][0] = [0, 16, 0, 0]
+    W["l0.w_up"][0] = [0, 2.0 ** -4, 0, 0]
+    W["l0.w_down"][0] = [1, 0]
+    W["lm_head"][0] = [1, 0, 0, 0]
+    assert _run_at_position_zero(sh, W, [], 0, bf16=True)[0] == 0.0
+    assert _run_at_position_zero(sh, W, [], 0, bf16=False)[0] != 0.0
+
+
+def test_bf16_ffn_norm_output_is_rounded():
+    """The second RMSNorm's output is stored in bf16: gain 1 + 2**-9 rounds to 1,
+    so the gate input h_0 - h_1 is exactly 0, silu(0) = 0 and the feed-forward
+    adds nothing (unrounded it adds silu(2**-9) * 64 to x_0)."""
+    sh = _bf16_shape()
+    W = _zero_weights(sh)
+    W["embed"][0] = [1, 1, 1, 1]
+    W["l0.ffn_norm"][:] = [1 + 2.0 ** -9, 1, 1, 1]
+    W["l0.w_gate"][0] = [1, -1, 0, 0]
+    W["l0.w_up"][0] = [0, 0, 64, 0]
+    W["l0.w_down"][0] = [1, 0]
+    W["lm_head"][0] = [1, -1, 0, 0]
+    assert _run_at_position_zero(sh, W, [], 0, bf16=True)[0] == 0.0
+    assert _run_at_position_zero(sh, W, [], 0, bf16=False)[0] != 0.0
+
+
+def test_bf16_final_norm_output_is_rounded():
+    """The final RMSNorm's output is stored in bf16 before the LM head: gain
+    1 + 2**-9 rounds to 1, so the logit h_0 - h_1 is exactly 0 (unrounded 2**-9)."""
+    sh = _bf16_shape()
+    W = _zero_weights(sh)
+    W["embed"][0] = [1, 1, 1, 1]
+    W["final_norm"][:] = [1 + 2.0 ** -9, 1, 1, 1]
+    W["lm_head"][0] = [1, -1, 0, 0]
+    assert _run_at_position_zero(sh, W, [], 0, bf16=True)[0] == 0.0
+    assert _run_at_position_zero(sh, W, [], 0, bf16=False)[0] == 2.0 ** -9
+
+
+# ---------------------------------------------------------------- multi-head split
+def test_two_heads_split_projections_head_major():
+    """Two heads of 2: head h owns projection rows (and output columns) 2h, 2h+1.
+    Head 0 weighs the cached key and itself by the logistic of its score
+    difference; head 1 has zero queries and averages its values.  Each head's
+    output lands in its own two columns of the output projection's input.  A
+    dim-major split (head h on rows h, h+2) mixes the heads and changes the logits."""
+    sh = _shape(d_model=4, n_heads=2, head_dim=2, vocab=4, rms_eps=0.0)
+    W = _zero_weights(sh)
+    W["embed"][0] = [1, 1, -1, 1]        # query
+    W["embed"][1] = [1, -1, 1, -1]       # cached key
+    # head 0: q = 1.5 * h_0, k = h_1 (dimension 0 of the head); v = (h_2, h_3)
+    W["l0.wq"][0] = [1.5, 0, 0, 0]
+    W["l0.wk"][0] = [0, 1, 0, 0]
+    W["l0.wv"][0] = [0, 0, 1, 0]
+    W["l0.wv"][1] = [0, 0, 0, 1]
+    # head 1: q = 0, v = (h_0 + h_1, h_2 - h_3) / 2
+    W["l0.wv"][2] = [0.5, 0.5, 0, 0]
+    W["l0.wv"][3] = [0, 0, 0.5, -0.5]
+    W["l0.wo"][:] = np.array([[1, 0, 0, 0], [0, 2, 0, 0], [0, 0, 3, 0], [0, 0, 0, 4]], np.float32)
+    W["lm_head"][:] = np.eye(4)
+    lg = _run_at_position_zero(sh, W, [1], 0, bf16=False)
+    eq, ek = W["embed"][0].astype(np.float64), W["embed"][1].astype(np.float64)
+    # head 0 scores (scale 1/sqrt(2)): q = 1.5, keys k = ek_1 = -1 (cached), eq_1 = 1 (self)
+    s_c, s_s = 1.5 * ek[1] / math.sqrt(2), 1.5 * eq[1] / math.sqrt(2)
+    w_s = 1.0 / (1.0 + math.exp(-(s_s - s_c)))
+    o0 = w_s * eq[2:4] + (1 - w_s) * ek[2:4]
+    v1 = lambda e: np.array([(e[0] + e[1]) / 2, (e[2] - e[3]) / 2])
+    o1 = 0.5 * (v1(eq) + v1(ek))
+    o = np.concatenate([o0, o1])
+    x = eq + np.array([1, 2, 3, 4]) * o
+    np.testing.assert_allclose(lg, x / math.sqrt(np.mean(x ** 2)), rtol=1e-12, atol=1e-12)
