@@ -169,7 +169,11 @@ int sdsat_commit_kv(sdsat_ctx* ctx, int32_t batch, int32_t q, const int32_t* d_n
  * k adaptive ids h_adaptive_ids[k] (k+1 <= max_block); k = 0 gives plain
  * decoding at two blocks per loop.  mode SDSAT_MODE_GREEDY or _NUCLEUS
  * (temperature, top_p, top_k, seed as in sdsat_verify_nucleus).
- * h_out: [batch, max_new] int32.  h_stats may be NULL.  Synchronous. */
+ * h_out: [batch, max_new] int32.  h_stats may be NULL.  Synchronous.
+ * Capacity: max_ctx (rounded up to 32) must be at least P + max_new + k + 1,
+ * plus k more slots when batch > 1 (a finished sequence stops at up to
+ * P + max_new + k committed tokens and still receives blocks); otherwise
+ * SDSAT_ECAPACITY. */
 int sdsat_generate(sdsat_ctx* ctx, int32_t batch, const int32_t* h_prompts, int32_t P,
                    int32_t max_new, int32_t k, const int32_t* h_adaptive_ids, int32_t mode,
                    float temperature, float top_p, int32_t top_k, uint64_t seed,
@@ -230,11 +234,13 @@ int sdsat_linear_pack(int32_t dtype, int32_t N, int32_t K, const void* d_w, void
 
 /* Skinny GEMM y[M, N] = x[M, K] . W[N, K]^T with x float32 (rounded to dtype
  * as the matrix-core input), float32 accumulation and output; M <= 64.
- * d_scratch: sdsat_linear_scratch_bytes() bytes, zero-filled before first use
- * and left zero after each call.  Stream-ordered on hip_stream. */
+ * d_scratch: sdsat_linear_scratch_bytes() bytes of device memory (caller-owned;
+ * every call rewrites the part it reads, so it needs no initial contents).
+ * Stream-ordered on hip_stream. */
 size_t sdsat_linear_scratch_bytes(int32_t M, int32_t N, int32_t K);
 int sdsat_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const float* d_x,
                  const void* d_packed, float* d_y, void* d_scratch, void* hip_stream);
+
 
 /* Per-kernel timing with HIP events on the context's stream.  kind: 0 off,
  * 1 gate/up GEMM, 2 QKV GEMM, 3 attention, 4 down GEMM, 5 O GEMM, 6 LM head,

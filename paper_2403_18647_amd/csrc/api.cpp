@@ -714,7 +714,11 @@ int generate_impl(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t
     for (int j = 0; j < k; ++j)
         if (h_adaptive_ids[j] < 0 || h_adaptive_ids[j] >= D.V + D.A)
             return fail(c, SDSAT_EINVAL, "adaptive id out of range");
-    if ((long)P - 1 + (long)max_new + q2 + 1 > D.S) return fail(c, SDSAT_ECAPACITY, "prompt + max_new exceeds max_ctx");
+    // A sequence's last loop starts below max_new tokens and may overshoot to max_new + k + 1, i.e.
+    // cache_len P + max_new + k.  With batch > 1 a finished sequence keeps riding along (commit 0), its
+    // blocks written at that cache_len, so its rows reach slot P + max_new + k + q2 - 1.
+    const long need = (long)P + max_new + q2 + (batch > 1 ? k : 0);
+    if (need > D.S) return fail(c, SDSAT_ECAPACITY, "prompt + max_new (+ k + 1 rows for batch > 1) exceeds max_ctx");
     for (long i = 0; i < (long)batch * P; ++i)
         if (h_prompts[i] < 0 || h_prompts[i] >= D.V + D.A) return fail(c, SDSAT_EINVAL, "prompt id out of range");
 

@@ -42,24 +42,6 @@ def test_teacher_forced_k0_and_k10():
         rope_base=1e6, dtype="bf16")), 3e-2, k=10)
 
 
-def _first_mismatch_ok(sh, W, prompt, got, ref, bf16, mode="greedy"):
-    """Tokens agree, or the first disagreement is an oracle near-tie (top-2 gap < 1e-2)
-    where the GPU picked the runner-up."""
-    for i, (a, b) in enumerate(zip(got, ref)):
-        if a == b:
-            continue
-        assert mode == "greedy", f"nucleus tokens differ at {i}"
-        ctx_tokens = (list(prompt) + ref[: i - 1]) if i else list(prompt[:-1])
-        cache = M.prefill(sh, W, ctx_tokens, bf16=bf16)
-        last = ref[i - 1] if i else int(prompt[-1])
-        lg, _ = M.forward_block(sh, W, cache, [last], [cache.length], bf16=bf16)
-        srt = np.sort(lg[0])[::-1]
-        assert srt[0] - srt[1] < 1e-2, f"token {i}: gpu {a} oracle {b}, gap {srt[0] - srt[1]}"
-        assert a == int(np.argsort(lg[0])[::-1][1])
-        return i
-    return len(ref)
-
-
 @pytest.mark.parametrize("dtype,k,prompt_len", [("bf16", 5, 318), ("bf16", 10, 254), ("fp32", 5, 189),
                                                  ("bf16", 5, 40), ("bf16", 10, 1625)])
 def test_block_rows_bitwise_equal_single_token_steps(dtype, k, prompt_len):
@@ -173,14 +155,22 @@ def test_generate_tiny_greedy_matches_ar():
     sh = wl.shape
     ctx = helpers.make_ctx(wl, max_batch=1, max_ctx=wl.prompt_len + wl.max_new + 16, max_block=wl.k + 1)
     prompt = synth.prompts(wl)
-    out, st = B.sdsat_generate(ctx.handle, prompt, wl.max_new, wl.k, synth.adaptive_ids(sh, wl.k))
+    ad = synth.adaptive_ids(sh, wl.k)
+    out, st = B.sdsat_generate(ctx.handle, prompt, wl.max_new, wl.k, ad)
     W = helpers.oracle_weights(wl)
-    ref = D.generate_ar(sh, W, prompt[0], wl.max_new)
-    n = _first_mismatch_ok(sh, W, prompt[0], [int(t) for t in out[0]], ref, False)
-    print(f"tiny greedy: {n}/{wl.max_new} tokens identical, loops={st['loops']} hist={st['accept_hist']}")
+    tr = D.Trace()
+    ref = D.generate_ar(sh, W, prompt[0], wl.max_new, trace=tr)
+    equal, exempted = helpers.free_run_compare(
+        lambda p, n: B.sdsat_generate(ctx.handle, p, n, wl.k, ad)[0], prompt, [ref],
+        helpers.greedy_near_tie([[blk["logits"][0] for blk in tr.blocks]]))
+    print(f"tiny greedy: {equal}/{wl.max_new} tokens identical, {exempted} near-ties, loops={st['loops']} "
+          f"hist={st['accept_hist']}")
+    assert exempted <= 2
     assert st["blocks"] == 2 * st["loops"]
-    assert all(0 <= m <= wl.k for m in range(len(st["accept_hist"])))
-    assert sum(st["accept_hist"]) == st["loops"]
+    # accept values m lie in 0..k: the histogram has k + 1 bins and counts every loop
+    assert len(st["accept_hist"]) == wl.k + 1 and sum(st["accept_hist"]) == st["loops"]
+    assert st["accepted"] == sum(m * c for m, c in enumerate(st["accept_hist"]))
+    assert st["tokens"] == sum((m + 2) * c for m, c in enumerate(st["accept_hist"]))
     ctx.close()
 
 
@@ -189,11 +179,19 @@ def test_generate_bf16_batch_ragged_greedy():
     sh = wl.shape
     ctx = helpers.make_ctx(wl, max_batch=3, max_ctx=wl.prompt_len + wl.max_new + 16, max_block=wl.k + 1)
     prompts = synth.prompts(wl)
-    out, st = B.sdsat_generate(ctx.handle, prompts, wl.max_new, wl.k, synth.adaptive_ids(sh, wl.k))
+    ad = synth.adaptive_ids(sh, wl.k)
     W = helpers.oracle_weights(wl)
+    refs, logits = [], []
     for b in range(3):
-        ref, _ = D.generate_sdsat(sh, W, prompts[b], wl.k, wl.max_new, synth.adaptive_ids(sh, wl.k), bf16=True)
-        _first_mismatch_ok(sh, W, prompts[b], [int(t) for t in out[b]], ref, True)
+        tr = D.Trace()
+        refs.append(D.generate_ar(sh, W, prompts[b], wl.max_new, bf16=True, trace=tr))
+        logits.append([blk["logits"][0] for blk in tr.blocks])
+        sd, _ = D.generate_sdsat(sh, W, prompts[b], wl.k, wl.max_new, ad, bf16=True)
+        assert sd == refs[-1]
+    equal, exempted = helpers.free_run_compare(
+        lambda p, n: B.sdsat_generate(ctx.handle, p, n, wl.k, ad)[0], prompts, refs, helpers.greedy_near_tie(logits))
+    print(f"bf16 batch 3 greedy: {equal}/{3 * wl.max_new} tokens identical, {exempted} near-ties")
+    assert exempted <= 3
     ctx.close()
 
 
@@ -207,15 +205,22 @@ def test_generate_nucleus_matches_ar_nucleus(T, p, top_k):
     out, st = B.sdsat_generate(ctx.handle, prompts, wl.max_new, wl.k, synth.adaptive_ids(sh, wl.k),
                                mode=B.MODE_NUCLEUS, temperature=T, top_p=p, top_k=top_k, seed=seed)
     W = helpers.oracle_weights(wl)
+    refs, margins = [], []
     for b in range(2):
         tr = D.Trace()
-        ref = D.generate_ar(sh, W, prompts[b], wl.max_new, mode="nucleus", temperature=T, top_p=p, top_k=top_k,
-                            seed=seed, b=b, trace=tr)
-        # fp32 GPU logits differ from the float64 oracle by ~1e-7 relative: compare every
-        # token up to the first draw whose decision margin is within 20x of that
-        n = next((i for i, mg in enumerate(tr.margins) if mg < 2e-6), len(ref))
-        assert n >= 10
-        assert [int(t) for t in out[b]][:n] == ref[:n], b
+        refs.append(D.generate_ar(sh, W, prompts[b], wl.max_new, mode="nucleus", temperature=T, top_p=p,
+                                  top_k=top_k, seed=seed, b=b, trace=tr))
+        margins.append(tr.margins)
+    assert all([int(t) for t in out[b]][:5] == refs[b][:5] for b in range(2))
+    # fp32 GPU logits differ from the float64 oracle by ~1e-7 relative: a draw whose decision margin
+    # is within 20x of that may go either way; there the GPU is resynchronised onto the oracle's
+    # tokens (keyed uniforms: the same absolute positions and sequence indices draw the same u)
+    kw = dict(mode=B.MODE_NUCLEUS, temperature=T, top_p=p, top_k=top_k, seed=seed)
+    equal, exempted = helpers.free_run_compare(
+        lambda pr, n: B.sdsat_generate(ctx.handle, pr, n, wl.k, synth.adaptive_ids(sh, wl.k), **kw)[0],
+        prompts, refs, lambda b, pos, tok: margins[b][pos] < 2e-6)
+    print(f"nucleus T={T} p={p} top_k={top_k}: {equal}/{2 * wl.max_new} tokens identical, {exempted} exempt draws")
+    assert exempted <= 3
     ctx.close()
 
 
@@ -260,6 +265,18 @@ def test_tree_generate_matches_oracle_tree_and_ar(mode, width, T, top_k):
             accepted_leaf |= any(r > k for r in path) and pos <= n
     assert accepted_leaf
     assert st["accepted"] > 0 and st["blocks"] == 2 * st["loops"]
+    # every position against the oracle's AR tokens, resynchronising at draws within 2e-6 of a boundary
+    refs, margins, logits = [], [], []
+    for b in range(2):
+        tr = D.Trace()
+        refs.append(D.generate_ar(sh, W, prompts[b], wl.max_new, mode=mode, temperature=T, top_p=p, top_k=top_k,
+                                  seed=seed, b=b, trace=tr))
+        margins.append(tr.margins)
+        logits.append([blk["logits"][0] for blk in tr.blocks])
+    exempt = (lambda b, pos, tok: margins[b][pos] < 2e-6) if nucleus else helpers.greedy_near_tie(logits)
+    equal, exempted = helpers.free_run_compare(
+        lambda pr, n: B.sdsat_generate(ctx.handle, pr, n, k, ad, width=width, **kw)[0], prompts, refs, exempt)
+    assert exempted <= 3
     ctx.close()
 
 
@@ -325,4 +342,34 @@ def test_capacity_errors():
     with pytest.raises(B.SdsatError) as e:
         B.sdsat_generate(ctx.handle, synth.prompts(wl), 60, 5, synth.adaptive_ids(wl.shape, 5))
     assert e.value.code == -4
+    ctx.close()
+
+
+def test_finished_sequence_rides_along_at_the_smallest_capacity():
+    """Batch 2 through sdsat_generate_forced.  Sequence 0's drafts are its own AR continuation, so every
+    loop accepts all k drafts (Eq. 3) and its last loop overshoots max_new by k + 1, the most a loop can;
+    sequence 1's drafts are all wrong (m = 0), so it runs on while sequence 0 rides along with commit 0
+    (Section 2.1 loop; finished sequences keep their blocks).  With P + max_new + k + (k + 1) = 64 the
+    ride-along blocks fill the cache exactly: the call succeeds with the AR tokens; one prompt token more
+    is rejected up front with SDSAT_ECAPACITY instead of a device-side capacity error."""
+    k, max_new = 5, 22                      # 7 tokens per accepted loop: 0, 7, 14, 21 -> 28 = max_new + k + 1
+    wl = synth.workload("tiny", batch=2, prompt_len=31)
+    sh = wl.shape
+    ad = synth.adaptive_ids(sh, k)
+    prompts = synth.prompts(wl)
+    big = helpers.make_ctx(wl, max_batch=2, max_ctx=128, max_block=k + 1)
+    ar, _ = B.sdsat_generate(big.handle, prompts, max_new + k + 2, 0, ad)
+    big.close()
+    ref = np.stack([ar[0], (ar[1] + 1) % sh.vocab]).astype(np.int32)
+    assert prompts.shape[1] + max_new + k + (k + 1) == 64
+    ctx = helpers.make_ctx(wl, max_batch=2, max_ctx=64, max_block=k + 1)
+    out, st = B.sdsat_generate(ctx.handle, prompts, max_new, k, ad, ref=ref)
+    assert np.array_equal(out, ar[:, :max_new])
+    assert st["accept_hist"][k] == 4 and st["accept_hist"][0] == max_new // 2 and st["loops"] == max_new // 2
+    longer = np.concatenate([prompts, prompts[:, :1]], axis=1)
+    with pytest.raises(B.SdsatError) as e:
+        B.sdsat_generate(ctx.handle, longer, max_new, k, ad, ref=ref)
+    assert e.value.code == -4
+    out, _ = B.sdsat_generate(ctx.handle, prompts, max_new, k, ad, ref=ref)   # the context still works
+    assert np.array_equal(out, ar[:, :max_new])
     ctx.close()
