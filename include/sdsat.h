@@ -241,6 +241,18 @@ size_t sdsat_linear_scratch_bytes(int32_t M, int32_t N, int32_t K);
 int sdsat_linear(int32_t dtype, int32_t M, int32_t N, int32_t K, const float* d_x,
                  const void* d_packed, float* d_y, void* d_scratch, void* hip_stream);
 
+/* sdsat_linear for callers that cannot allocate device memory (code under
+ * stream capture, serving loops that forbid allocation): the same kernels and
+ * results, with the scratch taken from a 4 MiB array the library holds in
+ * static device memory (one copy per GPU, kept until the process ends).  It
+ * allocates nothing; the caller still owns d_x, d_packed and d_y.
+ * M * (K rounded up to 32) * (4 bytes fp32, 2 bf16) must be <= 4 MiB, else
+ * SDSAT_EINVAL.  Every call on one GPU shares that GPU's array: calls that
+ * overlap on one GPU (other streams, other threads) race and must be
+ * serialised by the caller.  The device is the current one.  Stream-ordered on
+ * hip_stream; the first call on a device also looks up its array's address. */
+int sdsat_linear_noalloc(int32_t dtype, int32_t M, int32_t N, int32_t K, const float* d_x,
+                         const void* d_packed, float* d_y, void* hip_stream);
 
 /* Per-kernel timing with HIP events on the context's stream.  kind: 0 off,
  * 1 gate/up GEMM, 2 QKV GEMM, 3 attention, 4 down GEMM, 5 O GEMM, 6 LM head,

@@ -63,6 +63,7 @@ _SIGNATURES = {
     "sdsat_linear_pack": ([_I32, _I32, _I32, _VP, _VP, _VP], _I32),
     "sdsat_linear_scratch_bytes": ([_I32, _I32, _I32], _SZ),
     "sdsat_linear": ([_I32, _I32, _I32, _I32, _VP, _VP, _VP, _VP, _VP], _I32),
+    "sdsat_linear_noalloc": ([_I32, _I32, _I32, _I32, _VP, _VP, _VP, _VP], _I32),
     "sdsat_profile_kernel": ([_VP, _I32, _I32], _I32),
     "sdsat_kernel_time": ([_VP, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64)], _I32),
     "sdsat_kernel_samples": ([_VP, ctypes.POINTER(ctypes.c_float), _I64, ctypes.POINTER(_I64)], _I32),
@@ -225,6 +226,10 @@ def sdsat_linear_scratch_bytes(M, N, K) -> int:
 
 def sdsat_linear(dtype, M, N, K, x, packed, y, scratch, stream=None):
     _check(lib().sdsat_linear(dtype, M, N, K, _ptr(x), _ptr(packed), _ptr(y), _ptr(scratch), _stream(stream)))
+
+
+def sdsat_linear_noalloc(dtype, M, N, K, x, packed, y, stream=None):
+    _check(lib().sdsat_linear_noalloc(dtype, M, N, K, _ptr(x), _ptr(packed), _ptr(y), _stream(stream)))
 
 
 def sdsat_profile_kernel(ctx, kind, period=1):

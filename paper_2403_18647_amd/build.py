@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsdsat.so")
-SOURCES = ["gemm.hip", "attention.hip", "verify.hip", "misc.hip", "prefill.hip", "api.cpp"]
+SOURCES = ["gemm.hip", "attention.hip", "verify.hip", "misc.hip", "prefill.hip", "noalloc.hip", "api.cpp"]
 ARCH = "gfx950"
 
 

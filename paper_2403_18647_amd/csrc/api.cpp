@@ -466,6 +466,8 @@ int read_err_flag(sdsat_ctx* c) {
 
 }  // namespace
 
+int sdsat::report_error(int code, const std::string& msg) { return fail(nullptr, code, msg); }
+
 // ================================================================= C-ABI
 extern "C" {
 

@@ -7,6 +7,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <string>
+
 namespace sdsat {
 
 // ---------------------------------------------------------------- packed weights
@@ -177,5 +179,11 @@ hipError_t launch_pos0(const int* cache_len, int B, int offset, int* pos0, hipSt
 constexpr int kLoopRecCols = 66;   // k <= 63 (a block holds at most 64 rows)
 hipError_t launch_loop_record(int* rec, int B, int q1, int q2, int k, int max_new, const int* out1, const int* out2,
                               const int* n_accept, int* active, int* produced, hipStream_t s);
+
+// ---------------------------------------------------------------- host runtime
+// Records msg as the text sdsat_last_error(NULL) returns and passes code through.
+int report_error(int code, const std::string& msg);
+// Size of the static device array behind sdsat_linear_noalloc.
+constexpr size_t kNoAllocScratchBytes = size_t(4) << 20;
 
 }  // namespace sdsat
