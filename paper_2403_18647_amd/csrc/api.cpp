@@ -113,6 +113,7 @@ struct sdsat_ctx {
     void* qbuf = nullptr; void* obuf = nullptr; void* ubuf = nullptr;
     // scratch
     float* attn_part = nullptr;
+    int* attn_ctr = nullptr;      // attention split arrival counters (zero between launches)
     float* gemm_part = nullptr;   // partial tiles of split residual GEMMs
     int* cache_len = nullptr; int* err_flag = nullptr; int* verify_cnt = nullptr;
     // generation buffers
@@ -184,7 +185,8 @@ void carve(sdsat_ctx* c, Carver& cv) {
     c->qbuf = cv.take((size_t)D.maxB * D.maxQ * D.d * 4);
     c->obuf = cv.take((size_t)D.maxM * D.d_pad * e);
     c->ubuf = cv.take((size_t)D.maxM * D.F_pad * e);
-    c->attn_part = (float*)cv.take(attention_partial_floats(D.maxB, D.H, D.maxQ, D.Dh) * 4);
+    c->attn_part = (float*)cv.take(std::max<size_t>(1, attention_partial_floats(D.maxB, D.H, D.maxQ, D.Dh, D.S)) * 4);
+    c->attn_ctr = (int*)cv.take(attention_counter_ints(D.maxB, D.H, D.maxQ) * 4);
     {
         const int rows = std::min(D.maxM, kSkinnyRows);
         const size_t part = std::max(gemm_resid_part_bytes(D.nt_o, D.ks_d, rows),
@@ -313,7 +315,7 @@ int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask,
     a.cache_len = c->cache_len; a.per_split = p.per_split; a.mask = mask;
     a.B = B; a.q = q; a.H = D.H; a.S_max = D.S;
     a.scale = (float)(1.0 / std::sqrt((double)D.Dh));
-    a.splits = p.splits; a.cols = p.cols; a.part = c->attn_part;
+    a.splits = p.splits; a.cols = p.cols; a.part = c->attn_part; a.counter = c->attn_ctr;
     a.out = out; a.out_f32 = out_f32; a.ldo = ldo; a.err = c->err_flag;
     hipEvent_t e0, e1;
     prof_pair(c, PK_ATTN, &e0, &e1);
@@ -582,6 +584,7 @@ int sdsat_init(const sdsat_config* cfg, const void* const* weights, int32_t n_we
         (void)launch_fill_i32((int*)c->ubuf, (size_t)D.maxM * D.F_pad * D.esz / 4, 0, c->stream);
         (void)launch_fill_i32((int*)c->hbuf, (size_t)D.maxM * D.d_pad * D.esz / 4, 0, c->stream);
         (void)launch_fill_i32(c->verify_cnt, D.maxB, 0, c->stream);
+        (void)launch_fill_i32(c->attn_ctr, attention_counter_ints(D.maxB, D.H, D.maxQ), 0, c->stream);
         (void)launch_fill_i32(c->cache_len, D.maxB, 0, c->stream);
         (void)launch_fill_i32(c->err_flag, 1, 0, c->stream);
         if (hipStreamSynchronize(c->stream) != hipSuccess) {

@@ -7,12 +7,15 @@
 // The block's own K/V rows were written into slots L_b.. by the QKV epilogue.
 //
 // Workgroups per (b, h, 16-row tile of the block): one per key split (the
-// splits are fixed 32-key block ranges, see plan_attention); a combine
-// kernel merges the splits' partials.  Short caches take one split, and a
-// one-tile block then spreads each head over column slices instead: every
-// slice's workgroup forms all of the head's scores but only its share of the
-// columns of O (no combine).  Waves take the workgroup's 32-key blocks
-// round-robin.
+// splits are fixed 32-key block ranges, see plan_attention).  Each split
+// writes its partial result (unnormalised O, row maximum, row sum) with
+// device-coherent stores and counts itself done on a per-tile counter; the
+// split that arrives last merges all partials of the tile in split order and
+// writes O, so no second kernel runs and every key is read once.  Where only
+// one split is planned, a one-tile block may instead spread each head over
+// column slices: every slice's workgroup forms all of the head's scores but
+// only its share of the columns of O.  Waves take the workgroup's 32-key
+// blocks round-robin.
 // Q arrives in float and the probabilities are formed in float; on bf16
 // models each enters the matrix cores as a pair of bf16 fragments (value and
 // rounding remainder, about 16 significant bits), so neither is rounded to
@@ -37,10 +40,13 @@
 namespace sdsat {
 
 static constexpr int kMaxWaves = 8;
-static constexpr int kMaxSplits = 8;
+static constexpr int kMaxSplits = 16;
 static constexpr int kMaxCols = 8;
-// caches of at most this many 32-key blocks use one split
-static constexpr int kOneSplitBlocks = 32;
+// workgroups a full cache is cut into per row tile (key splits x sequences x heads), at most
+#ifndef SDSAT_ATTN_WGS
+#define SDSAT_ATTN_WGS 256
+#endif
+static constexpr int kAttnWorkgroups = SDSAT_ATTN_WGS;
 
 // Keys are partitioned by absolute 32-key block index only: split sp owns
 // blocks [sp * P, (sp + 1) * P) with P fixed by the cache capacity (at full
@@ -61,12 +67,11 @@ AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_ma
     const int cap = std::max(1, S_max / 32);
     const int nblk = std::max(1, std::min(cap, (max_len + q + 31) / 32));
     const int pairs = B * H;
-    // one round of workgroups per row tile (a workgroup of 8 waves holds a compute unit's registers);
-    // where that allows only two splits, one split without the combine is faster (measured at
-    // batch 4 x 32 heads: 26.4 -> 23.6 us per layer); more splits than one round is slower.  A short
-    // cache takes one split too: its column slices fill the round without a combine kernel.
-    int target = std::max(1, std::min(kMaxSplits, 256 / pairs));
-    if (target <= 2 || cap <= kOneSplitBlocks) target = 1;
+    // a full cache gives about kAttnWorkgroups workgroups per row tile; where that allows only two
+    // splits, one split is planned (measured at batch 4 x 32 heads with a combine kernel: 26.4 ->
+    // 23.6 us per layer)
+    int target = std::max(1, std::min(kMaxSplits, kAttnWorkgroups / pairs));
+    if (target <= 2) target = 1;
     p.per_split = (cap + target - 1) / target;
     p.splits = (nblk + p.per_split - 1) / p.per_split;
     p.row_tiles = (q + 15) / 16;
@@ -80,9 +85,16 @@ AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_ma
     return p;
 }
 
-size_t attention_partial_floats(int B, int H, int q_max, int head_dim) {
-    return (size_t)B * H * kMaxSplits * ((q_max + 15) / 16 * 16) * (head_dim + 4);
+size_t attention_partial_floats(int B_max, int H, int q_max, int head_dim, int S_max) {
+    size_t most = 0;
+    for (int b = 1; b <= B_max; ++b) {
+        const AttnPlan p = plan_attention(b, H, q_max, head_dim, S_max, S_max);
+        if (p.splits > 1) most = std::max(most, (size_t)b * H * p.splits * p.row_tiles * 16 * (head_dim + 4));
+    }
+    return most;
 }
+
+size_t attention_counter_ints(int B_max, int H, int q_max) { return (size_t)B_max * H * ((q_max + 15) / 16); }
 
 // K and V of one 32-key block through buffer resources over this (sequence,
 // head)'s cache rows: one 32-bit lane offset per 16-key half of K and one for
@@ -188,6 +200,61 @@ __device__ __forceinline__ void attend_block(const Frag<T> (&kf)[2][NDS], const 
     }
 }
 
+// Merge the split partials of one (sequence, head, 16-row tile): each thread
+// takes 4 head dimensions of a row, log-sum-exp over the splits in split
+// order.  The partials are read with device-coherent (agent-scope) loads.
+// (Rows of a sequence whose cache overflowed were flagged; their output is
+// then unspecified.)
+template <typename T, int DH>
+__device__ __forceinline__ void combine_tile(const AttnArgs& a, int bh, int rt, int n_rt) {
+    constexpr int D4 = DH / 4;
+    const int b = bh / a.H, h = bh % a.H;
+    const int rows = n_rt * 16;
+    const size_t sstride = (size_t)rows * (DH + 4);
+    for (int e = threadIdx.x; e < 16 * D4; e += blockDim.x) {
+        const int m = 16 * rt + e / D4, d = 4 * (e % D4);
+        if (m >= a.q) continue;
+        const float* base = a.part + ((size_t)bh * a.splits * rows + m) * (DH + 4);
+        float mx[kMaxSplits], sm[kMaxSplits];
+        f32x4_t ov[kMaxSplits];
+#pragma unroll
+        for (int sp = 0; sp < kMaxSplits; ++sp) {
+            if (sp < a.splits) {
+                const float* pr = base + sp * sstride;
+                mx[sp] = __hip_atomic_load(pr + DH, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                sm[sp] = __hip_atomic_load(pr + DH + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    ov[sp][r] = __hip_atomic_load(pr + d + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        float gmax = -INFINITY;
+#pragma unroll
+        for (int sp = 0; sp < kMaxSplits; ++sp) if (sp < a.splits) gmax = fmaxf(gmax, mx[sp]);
+        float den = 0.f;
+        f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int sp = 0; sp < kMaxSplits; ++sp) {
+            if (sp < a.splits) {
+                const float w = mx[sp] == -INFINITY ? 0.f : expf(mx[sp] - gmax);
+                den += w * sm[sp];
+                acc += w * ov[sp];
+            }
+        }
+        const float inv = 1.0f / den;
+        const size_t row = ((size_t)b * a.q + m) * a.ldo + (size_t)h * DH + d;
+        if (a.out_f32) {
+            float* po = reinterpret_cast<float*>(a.out) + row;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) po[r] = acc[r] * inv;
+        } else {
+            T* po = reinterpret_cast<T*>(a.out) + row;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) po[r] = to_elem<T>(acc[r] * inv);
+        }
+    }
+}
+
 // One workgroup per (sequence, head, 16-row tile, key split, column slice).
 template <typename T, int DH, int CS>
 __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
@@ -275,12 +342,12 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
             if constexpr (sizeof(T) == 2) s_q[(NDS + ds) * 64 + lane] = fl;
         }
         const int L = __builtin_amdgcn_readfirstlane(Lv);
-        if (L + q > a.S_max) {   // the host checks capacity; never read past this sequence's cache
-            if (threadIdx.x == 0) atomicOr(a.err, 4);
-            return;
-        }
+        // the host checks capacity; never read past this sequence's cache (a workgroup of a split
+        // tile still takes part in the arrival count, with no keys, so the count stays whole)
+        const bool over = L + q > a.S_max;
+        if (over && threadIdx.x == 0) atomicOr(a.err, 4);
         // key blocks the tile's last row can see (keys up to L + that row)
-        const int nblk = (L + min(16 * rt + 15, q - 1) + 32) / 32;
+        const int nblk = over ? 0 : (L + min(16 * rt + 15, q - 1) + 32) / 32;
         const int whi = sp == a.splits - 1 ? nblk : min(nblk, wlo + a.per_split);
         const int Tb = L + q;
 
@@ -360,10 +427,15 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
             if (m >= q) continue;
             const int d = 16 * (cx * NDT + dt) + 4 * g;
             if (a.splits > 1) {
-                // partial of this workgroup: O scaled to its row maximum, the maximum, the sum
+                // partial of this workgroup: O scaled to its row maximum, the maximum, the sum; stored
+                // device-coherent (agent scope), since the tile's last split may run on another XCD
                 float* pr = a.part + (((size_t)bh * a.splits + sp) * (n_rt * 16) + m) * (DH + 4);
-                *reinterpret_cast<f32x4_t*>(pr + d) = acc;
-                if (dt == 0 && g == 0) { pr[DH] = gmax; pr[DH + 1] = den; }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) __hip_atomic_store(pr + d + r, acc[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (dt == 0 && g == 0) {
+                    __hip_atomic_store(pr + DH, gmax, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(pr + DH + 1, den, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
                 continue;
             }
             const float inv = 1.0f / den;
@@ -382,84 +454,42 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
             }
         }
     }
-}
-
-// Combine the split partials: one thread per (b, h, row, 4 head dims),
-// log-sum-exp over the splits in split order, all partial loads in flight at
-// once.  (Rows of a sequence whose cache overflowed were flagged by the
-// partial kernel; their output is then unspecified.)
-template <typename T, int DH>
-__global__ void __launch_bounds__(64) attn_combine_kernel(AttnArgs a, int rows) {
-    constexpr int D4 = DH / 4;
-    const int e = blockIdx.x * 64 + threadIdx.x;          // over B*H*q*D4
-    if (e >= a.B * a.H * a.q * D4) return;
-    const int d = 4 * (e % D4);
-    const int m = (e / D4) % a.q;
-    const int bh = e / (D4 * a.q);
-    const int b = bh / a.H, h = bh % a.H;
-    const float* base = a.part + ((size_t)bh * a.splits * rows + m) * (DH + 4);
-    const size_t sstride = (size_t)rows * (DH + 4);
-    float mx[kMaxSplits], sm[kMaxSplits];
-    f32x4_t ov[kMaxSplits];
-#pragma unroll
-    for (int sp = 0; sp < kMaxSplits; ++sp) {
-        if (sp < a.splits) {
-            const float* pr = base + sp * sstride;
-            mx[sp] = pr[DH];
-            sm[sp] = pr[DH + 1];
-            ov[sp] = *reinterpret_cast<const f32x4_t*>(pr + d);
+    if (a.splits > 1) {
+        // Arrival: every thread's partial stores have completed at device scope before the count is
+        // raised (the wait covers them; agent-scope stores write through to the coherence point), so
+        // the split that brings the count to `splits` sees every partial of the tile.  It resets the
+        // count for the next launch and merges.
+        __shared__ int s_last;
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int* ctr = a.counter + (size_t)bh * n_rt + rt;
+            const int old = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_last = old == a.splits - 1;
+            if (s_last) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-    }
-    float gmax = -INFINITY;
-#pragma unroll
-    for (int sp = 0; sp < kMaxSplits; ++sp) if (sp < a.splits) gmax = fmaxf(gmax, mx[sp]);
-    float den = 0.f;
-    f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int sp = 0; sp < kMaxSplits; ++sp) {
-        if (sp < a.splits) {
-            const float w = mx[sp] == -INFINITY ? 0.f : expf(mx[sp] - gmax);
-            den += w * sm[sp];
-            acc += w * ov[sp];
-        }
-    }
-    const float inv = 1.0f / den;
-    const size_t row = ((size_t)b * a.q + m) * a.ldo + (size_t)h * DH + d;
-    if (a.out_f32) {
-        float* po = reinterpret_cast<float*>(a.out) + row;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) po[r] = acc[r] * inv;
-    } else {
-        T* po = reinterpret_cast<T*>(a.out) + row;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) po[r] = to_elem<T>(acc[r] * inv);
+        __syncthreads();
+        if (s_last) combine_tile<T, DH>(a, bh, rt, n_rt);
     }
 }
 
 template <typename T, int DH>
 static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-    const bool comb = a.splits > 1;
     void (*kern)(AttnArgs) = attn_kernel<T, DH, 1>;
     if (p.cols == 2) kern = attn_kernel<T, DH, 2>;
     else if (p.cols == 4) kern = attn_kernel<T, DH, 4>;
     else if constexpr (DH / 16 >= 8) { if (p.cols == 8) kern = attn_kernel<T, DH, 8>; }
     if (ev0)
-        hipExtLaunchKernelGGL(kern, dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, ev0, comb ? nullptr : ev1, 0, a);
+        hipExtLaunchKernelGGL(kern, dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, ev0, ev1, 0, a);
     else
         hipLaunchKernelGGL(kern, dim3(p.grid), dim3(64 * p.waves), p.lds_bytes, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !comb) return e;
-    const int n = a.B * a.H * a.q * (DH / 4);
-    const int rows = (a.q + 15) / 16 * 16;
-    if (ev0) hipExtLaunchKernelGGL(attn_combine_kernel<T, DH>, dim3((n + 63) / 64), dim3(64), 0, s, nullptr, ev1, 0, a, rows);
-    else hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3((n + 63) / 64), dim3(64), 0, s, a, rows);
     return hipGetLastError();
 }
 
 hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s,
                             hipEvent_t ev0, hipEvent_t ev1) {
     if (a.q < 1 || a.q > 4096 || (a.mask && a.q > 64) || p.waves < 1 || p.waves > kMaxWaves || a.splits < 1 || a.splits > kMaxSplits ||
-        a.splits != p.splits || (a.splits > 1 && !a.part) || p.row_tiles != (a.q + 15) / 16 ||
+        a.splits != p.splits || (a.splits > 1 && (!a.part || !a.counter)) || p.row_tiles != (a.q + 15) / 16 ||
         p.grid != a.B * a.H * a.splits * p.row_tiles * p.cols || a.ldo % 4 != 0 ||
         a.per_split != p.per_split || a.per_split < 1 || a.cols != p.cols || p.cols < 1 || p.cols > kMaxCols ||
         (p.cols & (p.cols - 1)) != 0 || p.cols > head_dim / 16 || (p.cols > 1 && a.splits != 1))

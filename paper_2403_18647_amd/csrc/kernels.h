@@ -101,10 +101,11 @@ struct AttnArgs {
     const uint64_t* mask;    // [B*q] or null
     int B, q, H, S_max;
     float scale;
-    int splits;              // workgroups per (b, h); > 1: partials to `part`, then a combine kernel
+    int splits;              // workgroups per (b, h); > 1: partials to `part`, merged by the last split
     int cols;                // column slices (splits == 1 only): workgroups per (b, h) that each write
                              // Dh / cols columns of O
     float* part;             // [B*H][splits][16*MT rows][Dh + 4]: unnormalised O, row max, row sum
+    int* counter;            // [B*H][row tiles] arrival counts of the splits (zero between launches)
     void* out;               // T (or float if out_f32) [B*q][ldo], head h at columns h*Dh..
     int out_f32, ldo;
     int* err;                // device error flags (bit 4: read past the cache)
@@ -113,8 +114,10 @@ struct AttnArgs {
 // host's upper bound of the cache lengths; S_max: key slots per sequence
 struct AttnPlan { int waves, splits, per_split, row_tiles, grid, lds_bytes, cols; };
 AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_max);
-size_t attention_partial_floats(int B, int H, int q_max, int head_dim);
-// ev0 / ev1 (optional): start of the attention kernel, end of the last kernel of the call
+// partial buffer and arrival counters a context needs for its largest blocks
+size_t attention_partial_floats(int B_max, int H, int q_max, int head_dim, int S_max);
+size_t attention_counter_ints(int B_max, int H, int q_max);
+// ev0 / ev1 (optional): start and end of the attention kernel
 hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s,
                             hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 

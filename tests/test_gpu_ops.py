@@ -255,8 +255,10 @@ def test_commit_chain_and_tree_gather():
 
 
 def test_attention_column_slices_do_not_change_values():
-    """One sequence alone (8 column slices per head) and the same sequence replicated 8 times (one
-    workgroup per head): the outputs are bitwise equal."""
+    """One key split per head: the sequence replicated 4 times (2 column slices per head) and 8 times
+    (one workgroup per head) gives bitwise equal outputs.  Batch 1 (key splits merged by the last
+    split to arrive) run three times in a row gives bitwise the same output each time, so the arrival
+    counters are back at zero after every launch."""
     shape = synth.small_shape(n_layers=1, d_model=4096, n_heads=32, head_dim=128, d_ffn=64, vocab=64,
                               n_adaptive=2, rope_base=1e6, dtype="bf16")
     H, Dh, L, q = 32, 128, 200, 6
@@ -266,28 +268,34 @@ def test_attention_column_slices_do_not_change_values():
     V = rng.standard_normal((n, H, Dh)).astype(np.float32)
     Q = rng.standard_normal((q, H, Dh)).astype(np.float32)
     outs = []
-    for Bn in (1, 8):
+    for Bn in (1, 4, 8):
         wl = synth.Workload("heads32", shape, seed=5, batch=Bn, k=5, prompt_len=1, max_new=1)
         ctx = helpers.make_ctx(wl, max_batch=Bn, max_ctx=n + 40, max_block=q)
         pos = np.tile(np.arange(n, dtype=np.int32), (Bn, 1))
         B.sdsat_kv_write(ctx.handle, 0, Bn, n, torch.from_numpy(np.stack([K] * Bn)).cuda(),
                          torch.from_numpy(np.stack([V] * Bn)).cuda(), torch.from_numpy(pos).cuda())
         B.sdsat_set_cache_len(ctx.handle, np.full(Bn, L, np.int32))
-        out = torch.empty((Bn * q, H * Dh), dtype=torch.float32, device="cuda")
-        B.sdsat_attention(ctx.handle, 0, Bn, q, torch.from_numpy(np.concatenate([Q.reshape(q, H * Dh)] * Bn)).cuda(),
-                          None, out)
-        torch.cuda.synchronize()
-        outs.append(out.cpu().numpy().reshape(Bn, q, H * Dh))
+        for _ in range(3 if Bn == 1 else 1):
+            out = torch.empty((Bn * q, H * Dh), dtype=torch.float32, device="cuda")
+            B.sdsat_attention(ctx.handle, 0, Bn, q,
+                              torch.from_numpy(np.concatenate([Q.reshape(q, H * Dh)] * Bn)).cuda(), None, out)
+            torch.cuda.synchronize()
+            outs.append(out.cpu().numpy().reshape(Bn, q, H * Dh))
         ctx.close()
-    one, eight = outs
+    one, again, third, four, eight = outs
+    assert np.array_equal(one.view(np.uint32), again.view(np.uint32))
+    assert np.array_equal(one.view(np.uint32), third.view(np.uint32))
     for b in range(8):
-        assert np.array_equal(one[0].view(np.uint32), eight[b].view(np.uint32)), b
+        assert np.array_equal(four[b % 4].view(np.uint32), eight[b].view(np.uint32)), b
+    # key splits and one split agree to float rounding
+    assert np.abs(one[0] - eight[0]).max() < 1e-5
 
 
 @pytest.mark.parametrize("lens", [[300], [300, 0], [300, 0, 31, 64], [300, 0, 31, 64, 129, 5, 250, 77]])
 def test_attention_32_heads_column_slices(lens):
-    """32 heads of 128 over a short cache (one key split): batch 1, 2, 4, 8 spread each head over 8,
-    4, 2 and 1 workgroups (column slices of the output); every slice count matches the reference."""
+    """32 heads of 128 over a short cache: batch 1 and 2 split each head's keys over workgroups (the
+    last to arrive merges), batch 4 and 8 take one split with 2 and 1 column slices of the output;
+    every plan matches the reference."""
     print(f"attention 32 heads, batch {len(lens)}", flush=True)
     shape = synth.small_shape(n_layers=1, d_model=4096, n_heads=32, head_dim=128, d_ffn=64, vocab=64,
                               n_adaptive=2, rope_base=1e6, dtype="bf16")
