@@ -113,16 +113,20 @@ def _block(shape, weights, cache, tokens, bf16, per_row, trace):
 
 def generate_sdsat(shape, weights, prompt, k, max_new, adaptive, mode="greedy",
                    temperature=1.0, top_p=1.0, top_k=0, seed=0, b=0,
-                   bf16=False, per_row=False, force_drafts=None, trace=None):
+                   bf16=False, per_row=False, force_drafts=None, trace=None, prefill_chunk=0,
+                   on_prefill_chunk=None):
     """SDSAT generation of ``max_new`` tokens for one sequence.
 
     ``force_drafts(n, k)``, if given, replaces the drafts of draft step 1 by
     the tokens it returns for output positions n..n+k-1 (used to force the
-    all-accept and all-reject bounds).  Returns (tokens, per-loop m list).
+    all-accept and all-reject bounds).  ``prefill_chunk`` > 0 prefills the
+    prompt in blocks of that many rows (the same values up to summation
+    order).  Returns (tokens, per-loop m list).
     """
     prompt = np.asarray(prompt, np.int64)
     adaptive = [int(a) for a in adaptive[:k]]
-    cache = M.prefill(shape, weights, prompt[:-1], bf16=bf16, per_row=per_row)
+    cache = M.prefill(shape, weights, prompt[:-1], bf16=bf16, per_row=per_row, chunk=prefill_chunk,
+                      on_chunk=on_prefill_chunk)
     pending = int(prompt[-1])
     out: list[int] = []
     ms: list[int] = []

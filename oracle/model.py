@@ -14,7 +14,12 @@ The block's K/V rows are returned, not stored: the caller commits the ones
 it accepts (``KVCache.commit``), which is what draft step 1 and the
 verification step do.
 
-Arithmetic is float64 throughout.  With ``bf16=True`` the oracle also rounds
+Arithmetic is float64 throughout, except that weights held as float32
+(``Weights(..., dtype=np.float32)``, the float32-BLAS mode for the 7B / 13B
+shapes) make the linear layers float32 matrix products: their inputs are
+bf16 values on bf16 models (exact in float32), so that mode differs from the
+float64 one only by float32 accumulation in the library's summation order.
+With ``bf16=True`` the oracle also rounds
 to bf16 (round to nearest even) exactly where a bf16 model stores values:
 RMSNorm outputs, K and V (after RoPE, as stored in the cache), the attention
 output, and the SwiGLU product.  The residual stream and logits keep full
@@ -47,12 +52,13 @@ def bf16_round(x: np.ndarray) -> np.ndarray:
     return out
 
 
-def weight_f64(shape, w) -> np.ndarray:
-    """Widen a stored weight (float32 values, or uint16 bf16 bit patterns) to float64."""
+def weight_f64(shape, w, dtype=np.float64) -> np.ndarray:
+    """Widen a stored weight (float32 values, or uint16 bf16 bit patterns) to
+    float64 (or to ``dtype``; no copy when it already has it)."""
     w = np.asarray(w)
     if w.dtype == np.uint16:
-        return (w.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-    return w.astype(np.float64)
+        return (w.astype(np.uint32) << 16).view(np.float32).astype(dtype)
+    return np.asarray(w, dtype)
 
 
 def rms_norm(x: np.ndarray, gain: np.ndarray, eps: float) -> np.ndarray:
@@ -136,35 +142,45 @@ class KVCache:
 
 
 class Weights:
-    """Float64 view of a weight mapping, converted lazily and cached per tensor."""
+    """Float64 (or float32: the float32-BLAS mode) view of a weight mapping,
+    converted lazily and cached per tensor."""
 
-    def __init__(self, shape, tensors, cache: bool = True):
+    def __init__(self, shape, tensors, cache: bool = True, dtype=np.float64):
         self.shape = shape
         self.tensors = tensors
+        self.dtype = np.dtype(dtype)
         self._cache = {} if cache else None
 
     def __getitem__(self, name: str) -> np.ndarray:
         if self._cache is not None and name in self._cache:
             return self._cache[name]
-        w = weight_f64(self.shape, self.tensors[name])
+        w = weight_f64(self.shape, self.tensors[name], self.dtype)
         if self._cache is not None:
             self._cache[name] = w
         return w
 
 
 def _linear(x: np.ndarray, w: np.ndarray, per_row: bool) -> np.ndarray:
-    """y = x @ w.T for x [rows, in], w [out, in]."""
+    """y = x @ w.T for x [rows, in], w [out, in]; a float32 weight makes it a
+    float32 product (x converted to float32), returned as float64."""
+    if w.dtype == np.float32:
+        x32 = np.ascontiguousarray(x, np.float32)
+        if per_row:
+            return np.stack([w @ x32[r] for r in range(x.shape[0])]).astype(np.float64) \
+                if x.shape[0] else np.zeros((0, w.shape[0]))
+        return (x32 @ w.T).astype(np.float64)
     if per_row:
         return np.stack([w @ np.ascontiguousarray(x[r]) for r in range(x.shape[0])]) \
             if x.shape[0] else np.zeros((0, w.shape[0]))
     return x @ w.T
 
 
-def attention(qh, kh, vh, ck, cv, vis, scale, per_row=False):
+def attention(qh, kh, vh, ck, cv, vis, scale, per_row=False, dtype=np.float64):
     """softmax(q k^T * scale) v over the committed cache plus the visible block rows.
 
     qh, kh, vh: [q, H, Dh] block rows; ck, cv: [L, H, Dh] committed rows.
-    Scores are max-subtracted before exponentiation.
+    Scores are max-subtracted before exponentiation.  ``dtype`` float32 (the
+    float32-BLAS mode) forms scores, softmax and the weighted sum in float32.
     """
     q, H, Dh = qh.shape
     o = np.empty((q, H, Dh))
@@ -180,14 +196,14 @@ def attention(qh, kh, vh, ck, cv, vis, scale, per_row=False):
                 o[r, hd] = (e / e.sum()) @ vals[:, hd, :]
         return o
     L = ck.shape[0]
-    keys = np.concatenate([ck, kh], axis=0).transpose(1, 0, 2)      # [H, L+q, Dh]
-    vals = np.concatenate([cv, vh], axis=0).transpose(1, 0, 2)
+    keys = np.concatenate([ck, kh], axis=0).transpose(1, 0, 2).astype(dtype)      # [H, L+q, Dh]
+    vals = np.concatenate([cv, vh], axis=0).transpose(1, 0, 2).astype(dtype)
     allowed = np.concatenate([np.ones((q, L), bool), vis], axis=1)  # [q, L+q]
-    s = np.matmul(qh.transpose(1, 0, 2), keys.transpose(0, 2, 1)) * scale  # [H, q, L+q]
+    s = np.matmul(qh.transpose(1, 0, 2).astype(dtype), keys.transpose(0, 2, 1)) * dtype(scale)  # [H, q, L+q]
     s = np.where(allowed[None], s, -np.inf)
     e = np.exp(s - s.max(axis=-1, keepdims=True))
     p = e / e.sum(axis=-1, keepdims=True)
-    return np.matmul(p, vals).transpose(1, 0, 2)                     # [q, H, Dh]
+    return np.matmul(p, vals).transpose(1, 0, 2).astype(np.float64)  # [q, H, Dh]
 
 
 def chain_visibility(q: int) -> np.ndarray:
@@ -216,7 +232,7 @@ def forward_block(shape, weights: Weights, cache: KVCache, tokens, positions,
     rnd = bf16_round if bf16 else (lambda a: a)
     eps = shape.rms_eps
 
-    x = weights["embed"][tokens].copy()                       # [q, d]
+    x = weights["embed"][tokens].astype(np.float64)           # [q, d]
     cos, sin = rope_cos_sin(positions, Dh, shape.rope_base)
     scale = 1.0 / np.sqrt(Dh)
     block_kv = []
@@ -230,7 +246,8 @@ def forward_block(shape, weights: Weights, cache: KVCache, tokens, positions,
         kh = rnd(apply_rope(kh, cos, sin))
         vh = rnd(vh)
         block_kv.append((kh, vh))
-        o = attention(qh, kh, vh, cache.k[layer], cache.v[layer], vis, scale, per_row)
+        o = attention(qh, kh, vh, cache.k[layer], cache.v[layer], vis, scale, per_row,
+                      getattr(weights, "dtype", np.dtype(np.float64)).type)
         o = rnd(o.reshape(q, d))
         x = x + _linear(o, weights[p + "wo"], per_row)
         h2 = rnd(rms_norm(x, weights[p + "ffn_norm"], eps))
@@ -245,8 +262,10 @@ def forward_block(shape, weights: Weights, cache: KVCache, tokens, positions,
     return logits, block_kv
 
 
-def prefill(shape, weights: Weights, tokens, bf16=False, per_row=False, chunk: int = 0) -> KVCache:
-    """Commit the given tokens at positions 0..n-1 (in chunks of ``chunk`` rows; 0 = one block)."""
+def prefill(shape, weights: Weights, tokens, bf16=False, per_row=False, chunk: int = 0,
+            on_chunk=None) -> KVCache:
+    """Commit the given tokens at positions 0..n-1 (in chunks of ``chunk`` rows; 0 = one block).
+    ``on_chunk(rows_done)``, if given, is called after each chunk (progress reporting)."""
     cache = KVCache(shape.n_layers, shape.n_heads, shape.head_dim)
     tokens = np.asarray(tokens, np.int64)
     n = tokens.shape[0]
@@ -256,4 +275,6 @@ def prefill(shape, weights: Weights, tokens, bf16=False, per_row=False, chunk: i
         _, kv = forward_block(shape, weights, cache, t, np.arange(lo, lo + len(t)),
                               bf16=bf16, per_row=per_row, want_logits=False)
         cache.commit(kv, range(len(t)))
+        if on_chunk is not None:
+            on_chunk(lo + len(t))
     return cache

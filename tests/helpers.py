@@ -33,8 +33,9 @@ def small_bf16(**kw):
     return synth.Workload(**base)
 
 
-def replay(wl, tol, k=None, max_new=None, prefill_chunk=16):
-    """Replay the oracle's SDSAT block sequence on the GPU and compare logits."""
+def replay(wl, tol, k=None, max_new=None, prefill_chunk=16, identical=False):
+    """Replay the oracle's SDSAT block sequence on the GPU and compare logits (identical: every
+    adaptive row uses the same id, which allows k beyond the number of adaptive ids)."""
     sh = wl.shape
     k = wl.k if k is None else k
     q = k + 1
@@ -44,7 +45,7 @@ def replay(wl, tol, k=None, max_new=None, prefill_chunk=16):
     W = oracle_weights(wl)
     bf16 = sh.dtype == "bf16"
     prompt = synth.prompts(wl)[0]
-    ad = synth.adaptive_ids(sh, k)
+    ad = synth.adaptive_ids(sh, k, identical=identical)
     tr = D.Trace()
     D.generate_sdsat(sh, W, prompt, k, max_new, ad, bf16=bf16, trace=tr)
     ctx = make_ctx(wl, max_batch=1, max_ctx=len(prompt) + max_new + 2 * q + 8, max_block=max(q, prefill_chunk))
@@ -116,3 +117,76 @@ def greedy_near_tie(trace_logits):
         order = np.argsort(-lg, kind="stable")
         return lg[order[0]] - lg[order[1]] < 1e-2 and tok == int(order[1])
     return ok
+
+
+def full_model_weights(wl, device="cuda"):
+    """Generate every tensor of a workload once: upload it for the library and keep a
+    float32 copy for the oracle's float32-BLAS mode (bf16 values are exact in float32).
+    Returns (device tensors in the fixed order, oracle Weights)."""
+    import torch
+    sh = wl.shape
+    dev, host = [], {}
+    for n in synth.tensor_names(sh):
+        t = synth.tensor(wl, n)
+        f = synth.bf16_bits_to_f32(t) if t.dtype == np.uint16 else t
+        if synth.is_gain(n) or t.dtype != np.uint16:
+            dev.append(torch.from_numpy(np.ascontiguousarray(f)).to(device))
+        else:
+            dev.append(torch.from_numpy(t.view(np.int16)).view(torch.bfloat16).to(device))
+        host[n] = f
+        del t
+    return dev, M.Weights(sh, host, dtype=np.float32)
+
+
+def replay_batched(sh, W, dev_weights, prompts, k, max_new, adaptive, tol, mode="greedy", temperature=0.0,
+                   top_p=1.0, top_k=0, seed=0, log=print, tol_mean=None, prefill_chunk=256):
+    """The oracle's SDSAT block sequence of every sequence (bf16 storage roundings), replayed as
+    batched blocks through sdsat_forward_block / sdsat_commit_kv after the library prefills the
+    prompts with its large-block path (as sdsat_generate does); every block's logits are compared
+    with the oracle's: the largest |difference| must be <= tol and, with tol_mean, the mean over the
+    block's logits <= tol_mean.  Returns (largest, largest block mean)."""
+    import time
+    import torch
+    from oracle import decode as D
+    prompts = np.asarray(prompts, np.int32)
+    Bn, P = prompts.shape
+    q = k + 1
+    traces = []
+    for b in range(Bn):
+        t0 = time.time()
+        tr = D.Trace()
+        D.generate_sdsat(sh, W, prompts[b], k, max_new, adaptive, mode=mode, temperature=temperature,
+                         top_p=top_p, top_k=top_k, seed=seed, b=b, bf16=True, trace=tr,
+                         prefill_chunk=prefill_chunk)
+        traces.append(tr)
+        log(f"oracle sequence {b}: {len(tr.blocks)} blocks in {time.time() - t0:.1f}s")
+    n_blocks = min(len(tr.blocks) for tr in traces)
+    max_block = max(q, min(1024, P))
+    cfg = B.make_config(sh, max_batch=Bn, max_ctx=P + max_new + 4 * q + 32, max_block=max_block)
+    ctx = B.Context(cfg, dev_weights)
+    h = ctx.handle
+    B.sdsat_reset(h, Bn)
+    for lo in range(0, P - 1, max_block):
+        n = min(max_block, P - 1 - lo)
+        t = torch.from_numpy(np.ascontiguousarray(prompts[:, lo:lo + n])).cuda()
+        B.sdsat_forward_block(h, Bn, n, t, None, None)
+        B.sdsat_commit_kv(h, Bn, n, torch.full((Bn,), n, dtype=torch.int32, device="cuda"))
+    V = sh.vocab
+    worst = worst_mean = 0.0
+    for i in range(n_blocks):
+        lens = ctx.cache_len()[:Bn]
+        assert [int(x) for x in lens] == [tr.blocks[i]["cache_len"] for tr in traces], i
+        toks = np.stack([tr.blocks[i]["tokens"] for tr in traces]).astype(np.int32)
+        lg = torch.empty((Bn * q, V), dtype=torch.float32, device="cuda")
+        B.sdsat_forward_block(h, Bn, q, torch.from_numpy(toks).cuda(), None, lg)
+        got = lg.cpu().numpy().reshape(Bn, q, V)
+        d = np.abs(got - np.stack([tr.blocks[i]["logits"] for tr in traces]))
+        errs = [float(d[b].max()) for b in range(Bn)]
+        worst, worst_mean = max(worst, *errs), max(worst_mean, float(d.mean()))
+        log(f"block {i}: max |logit diff| per sequence {['%.4f' % e for e in errs]}, mean {d.mean():.5f}")
+        assert max(errs) <= tol, (i, errs)
+        assert tol_mean is None or d.mean() <= tol_mean, (i, float(d.mean()))
+        n = [1 if i % 2 == 0 else tr.loop_m[i // 2] + 1 for tr in traces]
+        B.sdsat_commit_kv(h, Bn, q, torch.tensor(n, dtype=torch.int32, device="cuda"))
+    ctx.close()
+    return worst, worst_mean

@@ -303,6 +303,17 @@ def test_attention_32_heads_column_slices(lens):
     _attn_case(wl, lens, 6)
 
 
+@pytest.mark.parametrize("q", [6, 11])
+def test_attention_16384_keys_batch8(q):
+    """The attention micro-benchmark's shape: batch 8, 32 heads of 128, 16384 committed keys plus the
+    block's q rows (Q, K, V ~ N(0, 1)), every output element against the oracle's attention."""
+    print(f"attention B8 H32 keys 16384 q={q}", flush=True)
+    shape = synth.small_shape(n_layers=1, d_model=4096, n_heads=32, head_dim=128, d_ffn=64, vocab=64,
+                              n_adaptive=2, rope_base=1e6, dtype="bf16")
+    wl = synth.Workload("attn16k", shape, seed=4, batch=8, k=q - 1, prompt_len=1, max_new=1)
+    _attn_case(wl, [16384] * 8, q, seed=4)
+
+
 def test_stream_read_and_kernel_samples():
     print("stream read (ragged length) and per-launch samples", flush=True)
     # three whole 16 KiB workgroups plus 48 bytes; the kernel only reads

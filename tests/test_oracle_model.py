@@ -445,3 +445,22 @@ def test_two_heads_split_projections_head_major():
     o = np.concatenate([o0, o1])
     x = eq + np.array([1, 2, 3, 4]) * o
     np.testing.assert_allclose(lg, x / math.sqrt(np.mean(x ** 2)), rtol=1e-12, atol=1e-12)
+
+
+def test_float32_blas_mode_matches_float64_within_float32_rounding():
+    """Float32 weights switch the linear layers and attention to float32 products (the mode used
+    for the 7B / 13B shapes): the logits equal the float64 oracle's up to float32 rounding, and
+    differ from them (so the float32 path is really taken).  Float32 tensors are used in place."""
+    wl, w64 = _tiny()
+    W = {n: synth.tensor(wl, n) for n in synth.tensor_names(wl.shape)}
+    w32 = M.Weights(wl.shape, W, dtype=np.float32)
+    assert np.shares_memory(w32["l0.wq"], W["l0.wq"])
+    sh = wl.shape
+    pr = synth.prompts(wl)[0]
+    outs = []
+    for w in (w64, w32):
+        cache = M.prefill(sh, w, pr[:20], chunk=8)
+        lg, _ = M.forward_block(sh, w, cache, pr[20:26], np.arange(20, 26))
+        outs.append(lg)
+    d = np.abs(outs[0] - outs[1]).max()
+    assert 0 < d <= 1e-5 * np.abs(outs[0]).max()
