@@ -69,9 +69,10 @@ typedef struct sdsat_config {
     int32_t max_ctx;     /* KV slots per sequence (committed + one block) */
     int32_t max_block;   /* largest q (rows per sequence per block), <= 4096; also the
                             prefill block of sdsat_generate.  Blocks of more than 64 rows
-                            in total (batch * q) run their linear layers as library GEMMs
-                            (rocBLAS, no atomics) on the caller's weights and take no
-                            ancestor mask; decode blocks need batch * (k + 1) <= 64 */
+                            in total (batch * q) run their linear layers as matrix-core
+                            GEMMs on the caller's weights (d_ffn must then be a multiple
+                            of 8) and take no ancestor mask; decode blocks need
+                            batch * (k + 1) <= 64 */
 } sdsat_config;
 
 /* Statistics of sdsat_generate (Section 3.4 reports tokens/s and accept rate). */

@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsdsat.so")
-SOURCES = ["gemm.hip", "attention.hip", "verify.hip", "misc.hip", "prefill.hip", "noalloc.hip", "api.cpp"]
+SOURCES = ["gemm.hip", "attention.hip", "verify.hip", "misc.hip", "prefill.hip", "prefill_gemm.hip", "noalloc.hip", "api.cpp"]
 ARCH = "gfx950"
 
 
@@ -50,7 +50,7 @@ def build(verbose: bool = False) -> str:
     with ThreadPoolExecutor(len(SOURCES)) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-lrocblas", "-o", tmp]
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stdout + r.stderr)

@@ -2,7 +2,6 @@
 // weight packing, block forward, verification, KV commit and the draft/verify
 // generation loop (Section 2.1).  Declared in include/sdsat.h.
 #include <hip/hip_runtime.h>
-#include <rocblas/rocblas.h>
 
 #include <chrono>
 #include <cmath>
@@ -64,6 +63,10 @@ int make_dims(const sdsat_config* c, Dims* D, std::string* why) {
     if (c->d_model % 16) { *why = "d_model must be a multiple of 16"; return SDSAT_EUNSUPPORTED; }
     if (c->dtype != SDSAT_DTYPE_FP32 && c->dtype != SDSAT_DTYPE_BF16) { *why = "dtype must be 0 or 1"; return SDSAT_EINVAL; }
     if (c->max_block > kMaxBlock) { *why = "max_block must be <= 4096"; return SDSAT_EUNSUPPORTED; }
+    if ((long)c->max_batch * c->max_block > kSkinnyRows && c->d_ffn % 8) {
+        *why = "blocks of more than 64 rows need d_ffn to be a multiple of 8";
+        return SDSAT_EUNSUPPORTED;
+    }
     if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) { *why = "rms_eps must be >= 0 and rope_base > 0"; return SDSAT_EINVAL; }
     D->L = c->n_layers; D->d = c->d_model; D->H = c->n_heads; D->Dh = c->head_dim; D->F = c->d_ffn;
     D->V = c->vocab; D->A = c->n_adaptive; D->dtype = c->dtype; D->esz = c->dtype == SDSAT_DTYPE_BF16 ? 2 : 4;
@@ -113,6 +116,7 @@ struct sdsat_ctx {
     void* qbuf = nullptr; void* obuf = nullptr; void* ubuf = nullptr;
     // scratch
     float* attn_part = nullptr;
+    size_t attn_part_floats = 0;
     int* attn_ctr = nullptr;      // attention split arrival counters (zero between launches)
     float* gemm_part = nullptr;   // partial tiles of split residual GEMMs
     int* cache_len = nullptr; int* err_flag = nullptr; int* verify_cnt = nullptr;
@@ -125,7 +129,6 @@ struct sdsat_ctx {
     float* logits = nullptr;
     // large blocks (more than kSkinnyRows rows): normalised rows (element type) and float GEMM outputs
     void* hbuf = nullptr; float* c_qkv = nullptr; float* c_gu = nullptr; float* c_y = nullptr;
-    rocblas_handle blas = nullptr;
     int* h_pin = nullptr;   // pinned host staging
     size_t h_pin_ints = 0;
     int* h_rec = nullptr;      // pinned host copy of the loop records
@@ -144,7 +147,6 @@ struct sdsat_ctx {
         for (hipEvent_t e : events) (void)hipEventDestroy(e);
         if (h_pin) (void)hipHostFree(h_pin);
         if (h_rec) (void)hipHostFree(h_rec);
-        if (blas) (void)rocblas_destroy_handle(blas);
     }
 };
 
@@ -185,7 +187,8 @@ void carve(sdsat_ctx* c, Carver& cv) {
     c->qbuf = cv.take((size_t)D.maxB * D.maxQ * D.d * 4);
     c->obuf = cv.take((size_t)D.maxM * D.d_pad * e);
     c->ubuf = cv.take((size_t)D.maxM * D.F_pad * e);
-    c->attn_part = (float*)cv.take(std::max<size_t>(1, attention_partial_floats(D.maxB, D.H, D.maxQ, D.Dh, D.S)) * 4);
+    c->attn_part_floats = std::max<size_t>(1, attention_partial_floats(D.maxB, D.H, D.maxQ, D.Dh, D.S));
+    c->attn_part = (float*)cv.take(c->attn_part_floats * 4);
     c->attn_ctr = (int*)cv.take(attention_counter_ints(D.maxB, D.H, D.maxQ) * 4);
     {
         const int rows = std::min(D.maxM, kSkinnyRows);
@@ -219,7 +222,7 @@ void carve(sdsat_ctx* c, Carver& cv) {
     if (D.maxM > kSkinnyRows) {
         c->c_qkv = (float*)cv.take((size_t)D.maxM * 3 * D.d * 4);
         c->c_gu = (float*)cv.take((size_t)D.maxM * 2 * D.F * 4);
-        c->c_y = (float*)cv.take((size_t)D.maxM * D.d * 4);
+        c->c_y = (float*)cv.take((size_t)D.maxM * D.d * 4 * 2);   // two split-K halves
     }
 }
 
@@ -310,6 +313,8 @@ int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask,
                     int out_f32, int ldo) {
     const Dims& D = c->D;
     const AttnPlan p = plan_attention(B, D.H, q, D.Dh, max_hint(c, B), D.S);
+    if (attention_plan_partial_floats(p, B, D.H, D.Dh) > c->attn_part_floats)   // sized at init for every plan
+        return fail(c, SDSAT_EDEVICE, "attention plan needs more split partials than the workspace holds");
     AttnArgs a{};
     a.qbuf = qbuf; a.kc = layer_k(c, layer); a.vc = layer_v(c, layer);
     a.cache_len = c->cache_len; a.per_split = p.per_split; a.mask = mask;
@@ -324,21 +329,24 @@ int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask,
 }
 
 // C[M][N] (row stride ldc, float) = A[M][K] (row stride lda) . W[N][K]^T, A and W in the model's element
-// type, W the caller's row-major [out, in] weight: a plain library GEMM (column-major C^T = W^T' . A^T').
-int lib_gemm(sdsat_ctx* c, int M, int N, int K, const void* A, int lda, const void* W, float* C, int ldc) {
-    const rocblas_datatype t = c->D.dtype == SDSAT_DTYPE_BF16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
-    const float alpha = 1.f, beta = 0.f;
-    const rocblas_status st = rocblas_gemm_ex(c->blas, rocblas_operation_transpose, rocblas_operation_none, N, M, K,
-                                              &alpha, W, t, K, A, t, lda, &beta, C, rocblas_datatype_f32_r, ldc, C,
-                                              rocblas_datatype_f32_r, ldc, rocblas_datatype_f32_r,
-                                              rocblas_gemm_algo_standard, 0, 0);
-    if (st != rocblas_status_success)
-        return fail(c, SDSAT_EDEVICE, std::string("rocblas_gemm_ex: ") + rocblas_status_to_string(st));
+// type, W the caller's row-major [out, in] weights (up to three of n_per rows each, stacked along N): the
+// matrix-core GEMM of large blocks.
+// With c_part > 0 (the offset of a second output) a GEMM with fewer than 256 tiles and a long contraction
+// is split in two halves; *split tells the caller to add them.
+int big_gemm(sdsat_ctx* c, int M, int N, int K, const void* A, int lda, const void* W0, const void* W1,
+             const void* W2, int n_per, float* C, int ldc, size_t c_part = 0, bool* split = nullptr) {
+    PrefillGemmArgs p{};
+    p.M = M; p.N = N; p.K = K; p.A = A; p.lda = lda; p.W0 = W0; p.W1 = W1; p.W2 = W2; p.n_per = n_per;
+    p.C = C; p.ldc = ldc;
+    p.ksplit = c_part ? prefill_gemm_ksplit(M, N, K) : 1;
+    p.c_part = c_part;
+    if (split) *split = p.ksplit > 1;
+    HIPCHK(c, launch_prefill_gemm(c->D.dtype, p, c->stream));
     return SDSAT_OK;
 }
 
-// Block forward of a large block (B*q > kSkinnyRows rows, chain mask): linear layers as library GEMMs on
-// the caller's weights, the rest in row-wise kernels that round where the skinny path rounds.
+// Block forward of a large block (B*q > kSkinnyRows rows, chain mask): linear layers as matrix-core GEMMs
+// on the caller's weights, the rest in row-wise kernels that round where the skinny path rounds.
 int large_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, float* logits) {
     const Dims& D = c->D;
     const int M = B * q;
@@ -350,32 +358,30 @@ int large_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, float* l
     for (int l = 0; l < D.L; ++l) {
         const void* const* w = c->w_src.data() + 1 + 9 * l;   // attn_norm, wq, wk, wv, wo, ffn_norm, wg, wu, wd
         HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, eps, M, c->hbuf, D.d_pad, c->stream));
-        for (int j = 0; j < 3; ++j) {
-            int rc = lib_gemm(c, M, D.d, D.d, c->hbuf, D.d_pad, w[1 + j], c->c_qkv + j * D.d, 3 * D.d);
-            if (rc) return rc;
-        }
+        int rc = big_gemm(c, M, 3 * D.d, D.d, c->hbuf, D.d_pad, w[1], w[2], w[3], D.d, c->c_qkv, 3 * D.d);
+        if (rc) return rc;
         HIPCHK(c, launch_qkv_rope(D.dtype, c->c_qkv, 3 * D.d, M, q, D.H, D.Dh, c->cache_len, D.S, c->rope,
                                   (float*)c->qbuf, layer_k(c, l), layer_v(c, l), c->err_flag, c->stream));
-        int rc = attention_layer(c, l, B, q, nullptr, (const float*)c->qbuf, c->obuf, 0, D.d_pad);
+        rc = attention_layer(c, l, B, q, nullptr, (const float*)c->qbuf, c->obuf, 0, D.d_pad);
         if (rc) return rc;
-        rc = lib_gemm(c, M, D.d, D.d, c->obuf, D.d_pad, w[4], c->c_y, D.d);
+        const size_t y_part = (size_t)D.maxM * D.d;   // offset of the second split-K half in c_y
+        bool split = false;
+        rc = big_gemm(c, M, D.d, D.d, c->obuf, D.d_pad, w[4], nullptr, nullptr, D.d, c->c_y, D.d, y_part, &split);
         if (rc) return rc;
-        HIPCHK(c, launch_resid_rows(c->c_y, D.d, M, D.d, c->x, D.d, c->xg, D.d_pad, c->ffn_norm[l], c->ssq, D.n_ssq,
-                                    c->stream));
+        HIPCHK(c, launch_resid_rows(c->c_y, split ? c->c_y + y_part : nullptr, D.d, M, D.d, c->x, D.d, c->xg, D.d_pad,
+                                    c->ffn_norm[l], c->ssq, D.n_ssq, c->stream));
         HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, eps, M, c->hbuf, D.d_pad, c->stream));
-        for (int j = 0; j < 2; ++j) {
-            rc = lib_gemm(c, M, D.F, D.d, c->hbuf, D.d_pad, w[6 + j], c->c_gu + j * D.F, 2 * D.F);
-            if (rc) return rc;
-        }
-        HIPCHK(c, launch_swiglu_rows(D.dtype, c->c_gu, c->c_gu + D.F, 2 * D.F, M, D.F, c->ubuf, D.F_pad, c->stream));
-        rc = lib_gemm(c, M, D.d, D.F, c->ubuf, D.F_pad, w[8], c->c_y, D.d);
+        rc = big_gemm(c, M, 2 * D.F, D.d, c->hbuf, D.d_pad, w[6], w[7], nullptr, D.F, c->c_gu, 2 * D.F);
         if (rc) return rc;
-        HIPCHK(c, launch_resid_rows(c->c_y, D.d, M, D.d, c->x, D.d, c->xg, D.d_pad,
+        HIPCHK(c, launch_swiglu_rows(D.dtype, c->c_gu, c->c_gu + D.F, 2 * D.F, M, D.F, c->ubuf, D.F_pad, c->stream));
+        rc = big_gemm(c, M, D.d, D.F, c->ubuf, D.F_pad, w[8], nullptr, nullptr, D.d, c->c_y, D.d, y_part, &split);
+        if (rc) return rc;
+        HIPCHK(c, launch_resid_rows(c->c_y, split ? c->c_y + y_part : nullptr, D.d, M, D.d, c->x, D.d, c->xg, D.d_pad,
                                     l + 1 < D.L ? c->attn_norm[l + 1] : c->final_norm, c->ssq, D.n_ssq, c->stream));
     }
     if (logits) {
         HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, eps, M, c->hbuf, D.d_pad, c->stream));
-        int rc = lib_gemm(c, M, D.V, D.d, c->hbuf, D.d_pad, c->w_src[2 + 9 * D.L], logits, D.V);
+        int rc = big_gemm(c, M, D.V, D.d, c->hbuf, D.d_pad, c->w_src[2 + 9 * D.L], nullptr, nullptr, D.V, logits, D.V);
         if (rc) return rc;
     }
     prof_end(c, evb);
@@ -598,14 +604,6 @@ int sdsat_init(const sdsat_config* cfg, const void* const* weights, int32_t n_we
             hipSuccess) {
         c->err = "pinned host allocation failed";
         return init_fail(SDSAT_ENOMEM);
-    }
-    if (D.maxM > kSkinnyRows) {   // large blocks: deterministic library GEMMs (no atomics) on the context's stream
-        if (rocblas_create_handle(&c->blas) != rocblas_status_success ||
-            rocblas_set_stream(c->blas, c->stream) != rocblas_status_success ||
-            rocblas_set_atomics_mode(c->blas, rocblas_atomics_not_allowed) != rocblas_status_success) {
-            c->err = "rocBLAS handle creation failed";
-            return init_fail(SDSAT_EDEVICE);
-        }
     }
     *out = c;
     return SDSAT_OK;

@@ -70,11 +70,14 @@ AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_ma
     // a full cache gives about kAttnWorkgroups workgroups per row tile; where that allows only two
     // splits, one split is planned (measured at batch 4 x 32 heads with a combine kernel: 26.4 ->
     // 23.6 us per layer)
+    // A block of several 16-row tiles (a prefill chunk) has workgroups enough across its row tiles and
+    // takes one split (the key partition only has to be the same for every decode block size, and a
+    // decode block is one row tile).
+    p.row_tiles = (q + 15) / 16;
     int target = std::max(1, std::min(kMaxSplits, kAttnWorkgroups / pairs));
-    if (target <= 2) target = 1;
+    if (target <= 2 || p.row_tiles > 1) target = 1;
     p.per_split = (cap + target - 1) / target;
     p.splits = (nblk + p.per_split - 1) / p.per_split;
-    p.row_tiles = (q + 15) / 16;
     p.waves = std::max(1, std::min(p.per_split, kMaxWaves));
     // column slices (one split, one row tile): as many as keep one round of 256 workgroups
     p.cols = 1;
@@ -85,12 +88,18 @@ AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_ma
     return p;
 }
 
+size_t attention_plan_partial_floats(const AttnPlan& p, int B, int H, int head_dim) {
+    return p.splits > 1 ? (size_t)B * H * p.splits * p.row_tiles * 16 * (head_dim + 4) : 0;
+}
+
+// The most any block of up to q_max rows and up to B_max sequences needs: a one-row-tile (decode) block
+// may take more key splits than a longer one, so both sizes are planned, at full cache length.
 size_t attention_partial_floats(int B_max, int H, int q_max, int head_dim, int S_max) {
     size_t most = 0;
-    for (int b = 1; b <= B_max; ++b) {
-        const AttnPlan p = plan_attention(b, H, q_max, head_dim, S_max, S_max);
-        if (p.splits > 1) most = std::max(most, (size_t)b * H * p.splits * p.row_tiles * 16 * (head_dim + 4));
-    }
+    for (int b = 1; b <= B_max; ++b)
+        for (int q : {std::min(q_max, 16), q_max})
+            most = std::max(most, attention_plan_partial_floats(plan_attention(b, H, q, head_dim, S_max, S_max), b, H,
+                                                                head_dim));
     return most;
 }
 

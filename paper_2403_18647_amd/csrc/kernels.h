@@ -114,8 +114,9 @@ struct AttnArgs {
 // host's upper bound of the cache lengths; S_max: key slots per sequence
 struct AttnPlan { int waves, splits, per_split, row_tiles, grid, lds_bytes, cols; };
 AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_max);
-// partial buffer and arrival counters a context needs for its largest blocks
+// partial buffer and arrival counters a context needs for its largest blocks; what one plan needs
 size_t attention_partial_floats(int B_max, int H, int q_max, int head_dim, int S_max);
+size_t attention_plan_partial_floats(const AttnPlan& p, int B, int H, int head_dim);
 size_t attention_counter_ints(int B_max, int H, int q_max);
 // ev0 / ev1 (optional): start and end of the attention kernel
 hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s,
@@ -141,6 +142,20 @@ hipError_t launch_stream_read(const void* src, size_t bytes, hipStream_t s);
 hipError_t launch_rope_table(const double* inv_freq, int S, int half, float* rope, hipStream_t s);
 
 // ---------------------------------------------------------------- large blocks (prefill)
+// C[M][ldc] (float) = A[M][lda] (element type) . W[N][K]^T on the matrix cores, W = up to three
+// row-major [n_per, K] matrices stacked along N (W0 rows 0..n_per-1, W1 the next n_per, ...).
+// K must be a multiple of 8 (16-byte loads); rows of A past K read as zero only up to K.
+// With ksplit 2 (prefill_gemm_ksplit) the contraction is split in two halves whose partial products go
+// to C and C + c_part; the consumer adds them (partial 0 + partial 1).
+struct PrefillGemmArgs {
+    int M, N, K;
+    const void* A; int lda;
+    const void* W0; const void* W1; const void* W2; int n_per;
+    float* C; int ldc;
+    int ksplit; size_t c_part;
+};
+int prefill_gemm_ksplit(int M, int N, int K);
+hipError_t launch_prefill_gemm(int dtype, const PrefillGemmArgs& p, hipStream_t s);
 // Row-wise steps around the library GEMMs of blocks of more than 64 rows.
 // h = elem(xg / rms) with rms from the row's per-16-column sums of squares
 hipError_t launch_rms_rows(int dtype, const float* xg, int ldxg, const float* ssq, int n_ssq, int K, float eps, int M,
@@ -148,9 +163,10 @@ hipError_t launch_rms_rows(int dtype, const float* xg, int ldxg, const float* ss
 // c[m] = Q | K | V (float, row stride ldc): RoPE, Q to qbuf [M][H][Dh], K / V into the cache at cache_len[b] + row
 hipError_t launch_qkv_rope(int dtype, const float* c, int ldc, int M, int q, int H, int Dh, const int* cache_len,
                            int S_max, const float* rope, float* qbuf, void* kc, void* vc, int* err, hipStream_t s);
-// x += y; xg = x o gnext; ssq = per-16-column sums of squares of x
-hipError_t launch_resid_rows(const float* y, int ldy, int M, int N, float* x, int ldx, float* xg, int ldxg,
-                             const float* gnext, float* ssq, int n_tiles, hipStream_t s);
+// x += y (y = y0 + y1 when y1 is given: two split-K partials); xg = x o gnext; ssq = per-16-column sums
+// of squares of x
+hipError_t launch_resid_rows(const float* y, const float* y1, int ldy, int M, int N, float* x, int ldx, float* xg,
+                             int ldxg, const float* gnext, float* ssq, int n_tiles, hipStream_t s);
 // u = elem(silu(g) * up)
 hipError_t launch_swiglu_rows(int dtype, const float* g, const float* up, int ldg, int M, int F, void* u, int ldu,
                               hipStream_t s);

@@ -82,12 +82,14 @@ __global__ void qkv_rope_kernel(const float* c, int ldc, int q, int H, int Dh, c
 
 // x[m][n] += y[m][n]; xg[m][n] = x[m][n] * gnext[n]; ssq[m][n/16] = the sum of
 // squares over each 16-column group (butterfly in the decode epilogue's order).
-__global__ void __launch_bounds__(256) resid_rows_kernel(const float* y, int ldy, int N, float* x, int ldx, float* xg,
-                                                         int ldxg, const float* gnext, float* ssq, int n_tiles) {
+__global__ void __launch_bounds__(256) resid_rows_kernel(const float* y, const float* y1, int ldy, int N, float* x,
+                                                         int ldx, float* xg, int ldxg, const float* gnext, float* ssq,
+                                                         int n_tiles) {
     const int m = blockIdx.y, n = blockIdx.x * blockDim.x + threadIdx.x;
     float ss = 0.f;
     if (n < N) {
-        const float v = x[(size_t)m * ldx + n] + y[(size_t)m * ldy + n];
+        const float yv = y1 ? y[(size_t)m * ldy + n] + y1[(size_t)m * ldy + n] : y[(size_t)m * ldy + n];
+        const float v = x[(size_t)m * ldx + n] + yv;
         x[(size_t)m * ldx + n] = v;
         xg[(size_t)m * ldxg + n] = v * gnext[n];
         ss = v * v;
@@ -134,11 +136,11 @@ hipError_t launch_qkv_rope(int dtype, const float* c, int ldc, int M, int q, int
     return hipGetLastError();
 }
 
-hipError_t launch_resid_rows(const float* y, int ldy, int M, int N, float* x, int ldx, float* xg, int ldxg,
-                             const float* gnext, float* ssq, int n_tiles, hipStream_t s) {
+hipError_t launch_resid_rows(const float* y, const float* y1, int ldy, int M, int N, float* x, int ldx, float* xg,
+                             int ldxg, const float* gnext, float* ssq, int n_tiles, hipStream_t s) {
     if (M < 1) return hipSuccess;
-    hipLaunchKernelGGL(resid_rows_kernel, dim3((N + 255) / 256, M), dim3(256), 0, s, y, ldy, N, x, ldx, xg, ldxg, gnext,
-                       ssq, n_tiles);
+    hipLaunchKernelGGL(resid_rows_kernel, dim3((N + 255) / 256, M), dim3(256), 0, s, y, y1, ldy, N, x, ldx, xg, ldxg,
+                       gnext, ssq, n_tiles);
     return hipGetLastError();
 }
 
