@@ -84,6 +84,28 @@ def profiled_traffic(workload):
         return None
 
 
+def profiled_block_traffic(workload):
+    """HBM bytes per decode block forward from the committed counter summary of this workload
+    (profiles/block_forward_<workload>_decode.md), if every decode kernel source it lists still has
+    the recorded hash (else None)."""
+    import hashlib
+    prof = os.path.join(ROOT, "profiles", f"block_forward_{workload}_decode.md")
+    try:
+        text = open(prof).read().splitlines()
+        traffic = None
+        for line in text:
+            if line.startswith("traffic_bytes_per_block: "):
+                traffic = int(line.split(": ", 1)[1])
+            elif line.startswith("source_sha256 "):
+                name, digest = line[len("source_sha256 "):].split(": ", 1)
+                src = os.path.join(ROOT, "paper_2403_18647_amd", "csrc", name)
+                if hashlib.sha256(open(src, "rb").read()).hexdigest() != digest.strip():
+                    return None
+        return traffic
+    except (OSError, ValueError):
+        return None
+
+
 def stream_read_peak(B, torch, region_gib=1, regions=4, iters=12):
     """Achievable HBM read rate on this device: the library's read-only stream kernel over rotating
     1 GiB regions (4 GiB in all, far beyond the 256 MB memory-side cache), events around each launch,
@@ -520,7 +542,7 @@ def main():
                      "kernel": "block forward: all kernels of one draft or verify block (embed .. LM head, "
                                "M=%d rows)" % M_rows,
                      "achieved": round(blk_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(blk_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(blk_gbs / HBM_PEAK_GBS, 4), "traffic": profiled_block_traffic(wl.name),
                      "bytes_per_launch": int(bblk), "avg_launch_us": round(per_block_ms * 1e3, 2),
                      "launches": blk_n,
                      "dominant_kernel": {"kernel": "gate/up GEMM + SwiGLU (M=%d)" % M_rows,
