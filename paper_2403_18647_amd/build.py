@@ -28,7 +28,7 @@ def hipcc() -> str:
 
 
 def flags() -> list[str]:
-    return [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
+    return [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-Werror",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
@@ -57,6 +57,10 @@ def build(verbose: bool = False) -> str:
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}")
+    from . import build_hostsan   # the host runtime again, with address / undefined-behaviour sanitizers
+    san = build_hostsan.build()
+    if verbose:
+        print(f"built {san}")
     return LIB
 
 

@@ -34,6 +34,8 @@
 // requested from the host's upper bound of the cache length before the true
 // length has arrived.  The waves' partial results are merged in LDS with a
 // log-sum-exp combine in wave order (deterministic).
+#include <hip/hip_ext.h>
+
 #include "device.h"
 #include "kernels.h"
 

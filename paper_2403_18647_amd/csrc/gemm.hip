@@ -35,6 +35,8 @@
 #include <algorithm>
 #include <type_traits>
 
+#include <hip/hip_ext.h>
+
 #include "device.h"
 #include "kernels.h"
 

@@ -80,3 +80,21 @@ def test_measurement_helpers_reject_bad_arguments_on_the_host():
     assert L.sdsat_stream_read(None, 16, None) == -1            # NULL source with bytes to read
     assert L.sdsat_stream_read(ctypes.c_void_p(4096), 24, None) == -1   # not a multiple of 16
     assert b"multiple of 16" in L.sdsat_last_error(None)
+
+
+def test_host_runtime_under_address_and_undefined_behaviour_sanitizers():
+    """The host runtime built with ASan + UBSan (libsdsat_hostsan.so, built with the library): size
+    queries over many configurations, every argument check that returns before a device call, the
+    NULL-context paths and error texts, driven in a process with the sanitizer runtime preloaded.
+    Any heap overflow, use after free or undefined behaviour in those paths aborts the process."""
+    import subprocess
+    import sys
+    lib = os.path.join(ROOT, "paper_2403_18647_amd", "libsdsat_hostsan.so")
+    assert os.path.exists(lib), "libsdsat_hostsan.so is not built; run __graft_entry__.build()"
+    rt = subprocess.run(["gcc", "-print-file-name=libasan.so"], capture_output=True, text=True).stdout.strip()
+    assert os.path.isabs(rt) and os.path.exists(rt), "no libasan to preload"
+    env = dict(os.environ, LD_PRELOAD=rt, ASAN_OPTIONS="detect_leaks=0:abort_on_error=1",
+               UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "tests", "hostsan_driver.py"), lib], env=env,
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0 and "OK" in r.stdout, r.stdout[-2000:] + r.stderr[-4000:]
