@@ -6,14 +6,16 @@
 // feeds hundreds of flops, so unlike the decode GEMM this kernel is bound by
 // the matrix cores and by how often operands are re-read, not by HBM.
 //
-// Tiling: a workgroup of 4 waves computes a BM x BN tile of C, the waves in a
-// WM x WN grid, each a (16 TM) x (16 TN) sub-tile of matrix-core 16x16 tiles.
-// The contraction runs in 32-wide steps; both operands' step tiles are staged
-// in LDS (double-buffered), with the global loads of the next two steps in
-// flight in registers while the current step's fragments are read from LDS
-// and multiplied; one barrier per step.  LDS rows are padded by 16 bytes so that the 16 lanes reading one
-// fragment column hit distinct banks.  Every element of C is accumulated by
-// one wave in one fixed order of k, so results repeat bit for bit.
+// Tiling: a workgroup of WM x WN waves computes a BM x BN tile of C, each wave
+// a (16 TM) x (16 TN) sub-tile of matrix-core 16x16 tiles (bf16: 8 waves of
+// 32 x 64 in a 128 x 128 tile).  The contraction runs in stages of BK columns
+// (bf16: 64, two matrix-core steps); both operands' stage tiles are staged in
+// LDS (double-buffered), with the global loads of the next two stages in
+// flight in registers while the current stage's fragments are read from LDS
+// and multiplied; one barrier per stage.  LDS rows are padded by 16 bytes so
+// that the 16 lanes reading one fragment column hit distinct banks.  Every
+// element of C is accumulated by one wave in one fixed order of k, so results
+// repeat bit for bit.
 // Workgroups that share a weight tile (the same N tile, different M tiles) are
 // placed on the same XCD (workgroups go to the 8 XCDs round-robin), so the
 // weights come from HBM once and the other row tiles read them from that L2.
@@ -24,65 +26,75 @@ namespace sdsat {
 
 namespace {
 
-// contraction elements per LDS stage: one matrix-core step (measured on MI355X, 7B 511-row prefill:
-// 21.5 ms against 22.7 ms with two steps per stage, whose larger LDS tiles allow one workgroup less
-// per compute unit)
-template <typename T> struct PTile {
-    static constexpr int BK = 32;
+// Stage geometry: BK contraction elements per LDS stage.  Measured on MI355X, 7B 511-row prefill
+// (whole prefill, bf16): 8 waves of 32 x 64, BK 64, two register stages in flight: 14.0 ms; the same
+// with BK 32: 17.4 ms, with BK 128 (one workgroup per compute unit): 15.6 ms; 8 waves of 64 x 32:
+// 14.1 ms; 4 waves of 64 x 64, BK 32: 17.3 ms, BK 64: 18.8 ms; 16 waves of 32 x 32, BK 64: 14.7 ms;
+// one register stage instead of two: 14.9 ms.
+template <typename T, int BK_> struct PTile {
+    static constexpr int BK = BK_;
     static constexpr int EPC = 16 / sizeof(T);          // elements per 16-byte chunk
     static constexpr int LDR = BK + 16 / sizeof(T);     // LDS row stride in elements (16 bytes of padding)
 };
 
-// Global -> registers: this thread's chunks of the A and W step tiles (zero past M, N or K).
-template <typename T, int BM, int BN>
+// Global -> registers: this thread's chunks of the A and W step tiles.  The loads are unconditional
+// (indices clamped into the operands, the chunks past M, N or K zeroed when they are written to LDS), so
+// the loop has no divergent branches and the waits for a register set count only the loads before it.
+template <typename T, int BM, int BN, int NT, int BK>
 struct StepLoad {
-    static constexpr int EPC = PTile<T>::EPC;
-    static constexpr int CPR = PTile<T>::BK / EPC;        // chunks per row of a stage tile
-    static constexpr int NA = BM * CPR / 256, NW = BN * CPR / 256;
+    static constexpr int EPC = PTile<T, BK>::EPC;
+    static constexpr int CPR = PTile<T, BK>::BK / EPC;        // chunks per row of a stage tile
+    static constexpr int NA = (BM * CPR + NT - 1) / NT, NW = (BN * CPR + NT - 1) / NT;
+    static_assert(NA * NT == BM * CPR || NA == 1, "whole chunks per thread");
+    static_assert(NW * NT == BN * CPR || NW == 1, "whole chunks per thread");
     u32x4_t a[NA], w[NW];
+    bool ka[NA], kw[NW];
 
     __device__ __forceinline__ void load(const PrefillGemmArgs& p, int m0, int n0, int k0, int tid) {
 #pragma unroll
         for (int i = 0; i < NA; ++i) {
-            const int c = tid + 256 * i, row = c / CPR, kc = k0 + (c % CPR) * EPC;
-            const int m = m0 + row;
-            a[i] = u32x4_t{0u, 0u, 0u, 0u};
-            if (m < p.M && kc < p.K)
-                a[i] = *reinterpret_cast<const u32x4_t*>(reinterpret_cast<const T*>(p.A) + (size_t)m * p.lda + kc);
+            const int c = tid + NT * i, kc = k0 + (c % CPR) * EPC, m = m0 + c / CPR;
+            ka[i] = m < p.M && kc < p.K;
+            a[i] = *reinterpret_cast<const u32x4_t*>(reinterpret_cast<const T*>(p.A) + (size_t)min(m, p.M - 1) * p.lda +
+                                                     min(kc, p.K - EPC));
         }
 #pragma unroll
         for (int i = 0; i < NW; ++i) {
-            const int c = tid + 256 * i, row = c / CPR, kc = k0 + (c % CPR) * EPC;
-            const int n = n0 + row;
-            w[i] = u32x4_t{0u, 0u, 0u, 0u};
-            if (n < p.N && kc < p.K) {
-                const int j = n / p.n_per;
-                const T* src = reinterpret_cast<const T*>(j == 0 ? p.W0 : (j == 1 ? p.W1 : p.W2));
-                // cached: the other row tiles of this column tile read the same weights from L2
-                w[i] = *reinterpret_cast<const u32x4_t*>(src + (size_t)(n - j * p.n_per) * p.K + kc);
-            }
+            const int c = tid + NT * i, kc = k0 + (c % CPR) * EPC, n = n0 + c / CPR;
+            kw[i] = n < p.N && kc < p.K;
+            const int nn = min(n, p.N - 1), j = nn / p.n_per;
+            // matrix j as an element offset from W0 (arithmetic, not a branch per lane; the pointer
+            // stays a global one, so the load is a global load)
+            const T* w0 = reinterpret_cast<const T*>(p.W0);
+            const ptrdiff_t d1 = (reinterpret_cast<intptr_t>(p.W1) - reinterpret_cast<intptr_t>(p.W0)) / (ptrdiff_t)sizeof(T);
+            const ptrdiff_t d2 = (reinterpret_cast<intptr_t>(p.W2) - reinterpret_cast<intptr_t>(p.W0)) / (ptrdiff_t)sizeof(T);
+            const ptrdiff_t off = j == 0 ? 0 : (j == 1 ? d1 : d2);
+            // cached: the other row tiles of this column tile read the same weights from L2
+            w[i] = *reinterpret_cast<const u32x4_t*>(w0 + off + (ptrdiff_t)(nn - j * p.n_per) * p.K + min(kc, p.K - EPC));
         }
     }
     __device__ __forceinline__ void store(T* sa, T* sw, int tid) const {
-        constexpr int LDR = PTile<T>::LDR;
+        constexpr int LDR = PTile<T, BK>::LDR;
+        const u32x4_t zero = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int i = 0; i < NA; ++i) {
-            const int c = tid + 256 * i;
-            *reinterpret_cast<u32x4_t*>(sa + (c / CPR) * LDR + (c % CPR) * EPC) = a[i];
+            const int c = tid + NT * i;
+            if (NA * NT == BM * CPR || c < BM * CPR)
+                *reinterpret_cast<u32x4_t*>(sa + (c / CPR) * LDR + (c % CPR) * EPC) = ka[i] ? a[i] : zero;
         }
 #pragma unroll
         for (int i = 0; i < NW; ++i) {
-            const int c = tid + 256 * i;
-            *reinterpret_cast<u32x4_t*>(sw + (c / CPR) * LDR + (c % CPR) * EPC) = w[i];
+            const int c = tid + NT * i;
+            if (NW * NT == BN * CPR || c < BN * CPR)
+                *reinterpret_cast<u32x4_t*>(sw + (c / CPR) * LDR + (c % CPR) * EPC) = kw[i] ? w[i] : zero;
         }
     }
 };
 
-template <typename T, int WM, int WN, int TM, int TN>
-__global__ void __launch_bounds__(256) prefill_gemm_kernel(PrefillGemmArgs p) {
-    constexpr int BM = WM * TM * 16, BN = WN * TN * 16;
-    constexpr int LDR = PTile<T>::LDR, BK = PTile<T>::BK;
-    static_assert(WM * WN == 4, "four waves per workgroup");
+template <typename T, int WM, int WN, int TM, int TN, int BK>
+__global__ void __launch_bounds__(64 * WM * WN) prefill_gemm_kernel(PrefillGemmArgs p) {
+    constexpr int BM = WM * TM * 16, BN = WN * TN * 16, NT = 64 * WM * WN;
+    constexpr int LDR = PTile<T, BK>::LDR;
     __shared__ __align__(16) T s_a[2][BM * LDR];
     __shared__ __align__(16) T s_w[2][BN * LDR];
 
@@ -111,14 +123,15 @@ __global__ void __launch_bounds__(256) prefill_gemm_kernel(PrefillGemmArgs p) {
     const int kb = st0 * BK;
     // Two stages' global loads are in flight in registers while a third is read from LDS: at stage s
     // register set (s + 1) & 1 holds stage s + 1 (written to LDS after the stage-s products) and is
-    // then reloaded with stage s + 3; set s & 1 holds stage s + 2, still arriving.
-    StepLoad<T, BM, BN> r0, r1;
-    if (steps > 0) r0.load(p, m0, n0, kb, tid);
-    if (steps > 1) r1.load(p, m0, n0, kb + BK, tid);
-    if (steps > 0) r0.store(s_a[0], s_w[0], tid);
+    // then reloaded with stage s + 3; set s & 1 holds stage s + 2, still arriving.  Loads past the
+    // last stage read clamped, in-bounds addresses; their stage tiles are never read.
+    StepLoad<T, BM, BN, NT, BK> r0, r1;
+    r0.load(p, m0, n0, kb, tid);
+    r1.load(p, m0, n0, kb + BK, tid);
+    r0.store(s_a[0], s_w[0], tid);
     __syncthreads();
-    if (steps > 2) r0.load(p, m0, n0, kb + 2 * BK, tid);
-    auto stage = [&](int s, StepLoad<T, BM, BN>& next) {
+    r0.load(p, m0, n0, kb + 2 * BK, tid);
+    auto stage = [&](int s, StepLoad<T, BM, BN, NT, BK>& next) {
         const int buf = s & 1;
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 32) {
@@ -134,14 +147,24 @@ __global__ void __launch_bounds__(256) prefill_gemm_kernel(PrefillGemmArgs p) {
 #pragma unroll
                 for (int j = 0; j < TN; ++j) mma(acc[i][j], fa[i], fw[j]);
         }
-        if (s + 1 < steps) next.store(s_a[buf ^ 1], s_w[buf ^ 1], tid);
+        // keep the LDS write after the products and the next loads before the following stage's: left
+        // to itself the scheduler moves loads next to the write that consumes them, which then waits
+        // out their latency
+        __builtin_amdgcn_sched_barrier(0);
+        next.store(s_a[buf ^ 1], s_w[buf ^ 1], tid);
         __syncthreads();
-        if (s + 3 < steps) next.load(p, m0, n0, kb + (s + 3) * BK, tid);
+        next.load(p, m0, n0, kb + (s + 3) * BK, tid);
+        __builtin_amdgcn_sched_barrier(0);
     };
-    for (int s = 0; s < steps; s += 2) {
+    // stages in pairs, an odd last stage after the loop: with no exit between the two halves the
+    // waits before each LDS write count only the other register set's loads (a conditional second
+    // half makes the compiler wait for every load at the top of the loop)
+    int s = 0;
+    for (; s + 1 < steps; s += 2) {
         stage(s, r1);
-        if (s + 1 < steps) stage(s + 1, r0);
+        stage(s + 1, r0);
     }
+    if (s < steps) stage(s, r1);
     // acc[i][j][r] = C[row 16 i + 4 g + r of the wave tile][column 16 j + c]
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -157,12 +180,12 @@ __global__ void __launch_bounds__(256) prefill_gemm_kernel(PrefillGemmArgs p) {
         }
 }
 
-template <typename T, int WM, int WN, int TM, int TN>
+template <typename T, int WM, int WN, int TM, int TN, int BK>
 hipError_t go(const PrefillGemmArgs& p, hipStream_t s) {
     constexpr int BM = WM * TM * 16, BN = WN * TN * 16;
     const long tiles = (long)((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
-    hipLaunchKernelGGL((prefill_gemm_kernel<T, WM, WN, TM, TN>), dim3((unsigned)(tiles * p.ksplit)), dim3(256), 0, s,
-                       p);
+    hipLaunchKernelGGL((prefill_gemm_kernel<T, WM, WN, TM, TN, BK>), dim3((unsigned)(tiles * p.ksplit)),
+                       dim3(64 * WM * WN), 0, s, p);
     return hipGetLastError();
 }
 
@@ -173,7 +196,8 @@ int prefill_gemm_ksplit(int M, int N, int K) {
     return tiles < 256 && K >= 1024 ? 2 : 1;
 }
 
-// 128 x 128 tiles.  prefill_gemm_ksplit: a GEMM whose tiles make less than
+// 128 x 128 tiles (bf16: 8 waves of 32 x 64, float: 4 waves of 64 x 64, 32-wide
+// stages).  prefill_gemm_ksplit: a GEMM whose tiles make less than
 // one round of workgroups over the 256 compute units and whose contraction is
 // long is better split in two (O and down at 7B: 128 -> 256 workgroups), where
 // the caller can add the partials.
@@ -182,7 +206,8 @@ hipError_t launch_prefill_gemm(int dtype, const PrefillGemmArgs& p, hipStream_t 
         (p.N > p.n_per && !p.W1) || (p.N > 2 * p.n_per && !p.W2) || p.lda < p.K || p.ldc < p.N ||
         p.ksplit < 1 || p.ksplit > 2 || (p.ksplit > 1 && p.c_part < (size_t)p.M * p.ldc))
         return hipErrorInvalidValue;
-    return dtype == 1 ? go<uint16_t, 2, 2, 4, 4>(p, s) : go<float, 2, 2, 4, 4>(p, s);
+    if (dtype != 1) return go<float, 2, 2, 4, 4, 32>(p, s);
+    return go<uint16_t, 4, 2, 2, 4, 64>(p, s);
 }
 
 }  // namespace sdsat
