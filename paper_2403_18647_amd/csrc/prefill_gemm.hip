@@ -12,8 +12,11 @@
 // (bf16: 64, two matrix-core steps); both operands' stage tiles are staged in
 // LDS (double-buffered), with the global loads of the next two stages in
 // flight in registers while the current stage's fragments are read from LDS
-// and multiplied; one barrier per stage.  LDS rows are padded by 16 bytes so
-// that the 16 lanes reading one fragment column hit distinct banks.  Every
+// and multiplied; one barrier per stage.  LDS rows are padded by 32 bytes: a
+// 64-lane 16-byte fragment read then takes the LDS's 4 cycles with no bank
+// conflict (measured on MI355X with rocprofv3's SQ_LDS_BANK_CONFLICT: rows of
+// 80 or 144 bytes conflict two-way, rows of 160 bytes or 128 bytes with the
+// 16-byte chunks permuted by row do not).  Every
 // element of C is accumulated by one wave in one fixed order of k, so results
 // repeat bit for bit.
 // Workgroups that share a weight tile (the same N tile, different M tiles) are
@@ -34,7 +37,7 @@ namespace {
 template <typename T, int BK_> struct PTile {
     static constexpr int BK = BK_;
     static constexpr int EPC = 16 / sizeof(T);          // elements per 16-byte chunk
-    static constexpr int LDR = BK + 16 / sizeof(T);     // LDS row stride in elements (16 bytes of padding)
+    static constexpr int LDR = BK + 32 / sizeof(T);     // LDS row stride in elements (32 bytes of padding)
 };
 
 // Global -> registers: this thread's chunks of the A and W step tiles.  The loads are unconditional
