@@ -42,7 +42,6 @@
 namespace sdsat {
 
 static constexpr int kMaxWaves = 8;
-static constexpr int kLoadGroup = 8;   // split partials the merge requests together
 static constexpr int kMaxSplits = 16;
 static constexpr int kMaxCols = 8;
 // workgroups a full cache is cut into per row tile (key splits x sequences x heads), at most
@@ -229,26 +228,15 @@ __device__ __forceinline__ void combine_tile(const AttnArgs& a, int bh, int rt, 
         const float* base = a.part + ((size_t)bh * a.splits * rows + m) * (DH + 4);
         float mx[kMaxSplits], sm[kMaxSplits];
         f32x4_t ov[kMaxSplits];
-        // The first kLoadGroup splits' loads are unconditional (a split past the count re-reads the
-        // last one; only splits below the count enter the sums), so they are all in flight before
-        // the first wait; loads under a branch per split were waited for one split at a time.
-        auto load_split = [&](int sp) {
-            const float* pr = base + min(sp, a.splits - 1) * sstride;
-            mx[sp] = __hip_atomic_load(pr + DH, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            sm[sp] = __hip_atomic_load(pr + DH + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-                ov[sp][r] = __hip_atomic_load(pr + d + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        };
+        for (int sp = 0; sp < kMaxSplits; ++sp) {
+            if (sp < a.splits) {
+                const float* pr = base + sp * sstride;
+                mx[sp] = __hip_atomic_load(pr + DH, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                sm[sp] = __hip_atomic_load(pr + DH + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
-        for (int sp = 0; sp < kLoadGroup; ++sp) load_split(sp);
-        if (a.splits > kLoadGroup) {
-#pragma unroll
-            for (int sp = kLoadGroup; sp < kMaxSplits; ++sp) load_split(sp);
-        } else {
-#pragma unroll
-            for (int sp = kLoadGroup; sp < kMaxSplits; ++sp) {
-                mx[sp] = -INFINITY; sm[sp] = 0.f; ov[sp] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                for (int r = 0; r < 4; ++r)
+                    ov[sp][r] = __hip_atomic_load(pr + d + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         }
         float gmax = -INFINITY;
@@ -429,35 +417,24 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
         __syncthreads();
         // log-sum-exp merge of the waves' partials in wave order; output tiles
         // are spread over the waves
-        // (LDS reads unconditional: a wave slot past nw reads wave nw-1's values, which only waves
-        // below nw add in, so all reads are in flight before the first wait)
-        float alpha[kMaxWaves], wsum[kMaxWaves];
+        float alpha[kMaxWaves];
         float gmax = -INFINITY;
 #pragma unroll
         for (int w = 0; w < kMaxWaves; ++w) {
-            const int wr = min(w, nw - 1);
-            alpha[w] = s_max[wr][c];
-            wsum[w] = s_sum[wr][c];
-        }
-#pragma unroll
-        for (int w = 0; w < kMaxWaves; ++w) {
-            if (w >= nw) alpha[w] = -INFINITY;
+            alpha[w] = w < nw ? s_max[w][c] : -INFINITY;
             gmax = fmaxf(gmax, alpha[w]);
         }
         float den = 0.f;
 #pragma unroll
         for (int w = 0; w < kMaxWaves; ++w) {
             alpha[w] = alpha[w] == -INFINITY ? 0.f : expf(alpha[w] - gmax);
-            if (w < nw) den += alpha[w] * wsum[w];
+            if (w < nw) den += alpha[w] * s_sum[w][c];
         }
         for (int dt = wave; dt < NDT; dt += nw) {
             f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            f32x4_t ow[kMaxWaves];
-#pragma unroll
-            for (int w = 0; w < kMaxWaves; ++w) ow[w] = opart[(min(w, nw - 1) * RGN + dt) * 64 + lane];
 #pragma unroll
             for (int w = 0; w < kMaxWaves; ++w)
-                if (w < nw) acc += ow[w] * alpha[w];
+                if (w < nw) acc += opart[(w * RGN + dt) * 64 + lane] * alpha[w];
             if (m >= q) continue;
             const int d = 16 * (cx * NDT + dt) + 4 * g;
             if (a.splits > 1) {
