@@ -45,10 +45,7 @@ static constexpr int kMaxWaves = 8;
 static constexpr int kMaxSplits = 16;
 static constexpr int kMaxCols = 8;
 // workgroups a full cache is cut into per row tile (key splits x sequences x heads), at most
-#ifndef SDSAT_ATTN_WGS
-#define SDSAT_ATTN_WGS 256
-#endif
-static constexpr int kAttnWorkgroups = SDSAT_ATTN_WGS;
+static constexpr int kAttnWorkgroups = 256;
 
 // Keys are partitioned by absolute 32-key block index only: split sp owns
 // blocks [sp * P, (sp + 1) * P) with P fixed by the cache capacity (at full
