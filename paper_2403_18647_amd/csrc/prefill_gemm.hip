@@ -30,10 +30,12 @@ namespace sdsat {
 namespace {
 
 // Stage geometry: BK contraction elements per LDS stage.  Measured on MI355X, 7B 511-row prefill
-// (whole prefill, bf16): 8 waves of 32 x 64, BK 64, two register stages in flight: 14.0 ms; the same
-// with BK 32: 17.4 ms, with BK 128 (one workgroup per compute unit): 15.6 ms; 8 waves of 64 x 32:
-// 14.1 ms; 4 waves of 64 x 64, BK 32: 17.3 ms, BK 64: 18.8 ms; 16 waves of 32 x 32, BK 64: 14.7 ms;
-// one register stage instead of two: 14.9 ms.
+// (whole prefill, bf16, 16-byte row padding): 8 waves of 32 x 64, BK 64, two register stages in
+// flight: 14.0 ms (13.2 ms with the 32-byte padding used now); the same with BK 32: 17.4 ms, with
+// BK 128 (one workgroup per compute unit): 15.6 ms; 8 waves of 64 x 32: 14.1 ms; 4 waves of 64 x 64,
+// BK 32: 17.3 ms, BK 64: 18.8 ms; 16 waves of 32 x 32, BK 64: 14.7 ms; one register stage instead of
+// two: 14.9 ms.  Three register stages (at the register budget of two workgroups per compute unit,
+// with a small spill) measured slower than two: 13.6 against 12.8 ms in one run.
 template <typename T, int BK_> struct PTile {
     static constexpr int BK = BK_;
     static constexpr int EPC = 16 / sizeof(T);          // elements per 16-byte chunk
