@@ -100,7 +100,7 @@ struct sdsat_ctx {
     std::vector<const float*> attn_norm, ffn_norm;
     const float* final_norm = nullptr;
     // the caller's row-major weights (embed, {attn_norm, wq, wk, wv, wo, ffn_norm, w_gate, w_up, w_down} x L,
-    // final_norm, lm_head): the library GEMMs of large blocks read them
+    // final_norm, lm_head): the prefill GEMMs of large blocks read them
     std::vector<const void*> w_src;
     // packed weights
     std::vector<void*> w_qkv, w_o, w_gu, w_down;

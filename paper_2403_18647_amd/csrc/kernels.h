@@ -155,7 +155,7 @@ struct PrefillGemmArgs {
 };
 int prefill_gemm_ksplit(int M, int N, int K);
 hipError_t launch_prefill_gemm(int dtype, const PrefillGemmArgs& p, hipStream_t s);
-// Row-wise steps around the library GEMMs of blocks of more than 64 rows.
+// Row-wise steps around the prefill GEMMs of blocks of more than 64 rows.
 // h = elem(xg / rms) with rms from the row's per-16-column sums of squares
 hipError_t launch_rms_rows(int dtype, const float* xg, int ldxg, const float* ssq, int n_ssq, int K, float eps, int M,
                            void* h, int ldh, hipStream_t s);

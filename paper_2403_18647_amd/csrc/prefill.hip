@@ -1,9 +1,9 @@
-// Row-wise kernels around the library GEMMs of large blocks (prompt prefill).
+// Row-wise kernels around the matrix-core GEMMs of large blocks (prompt prefill).
 //
 // A block of more than 64 rows is weight-reuse bound rather than weight-stream
-// bound, so its linear layers run as plain matrix-core GEMMs from the BLAS
-// library (bf16 or float inputs, float accumulation and output) on the
-// caller's row-major weights.  The model's other arithmetic stays here and
+// bound, so its linear layers run as tiled matrix-core GEMMs (prefill_gemm.hip:
+// bf16 or float inputs, float accumulation and output) on the caller's
+// row-major weights.  The model's other arithmetic stays here and
 // rounds exactly where the decode kernels round (the values a bf16 model
 // stores): the RMSNorm output bf16(x o g / rms), K and V, the SwiGLU product;
 // Q and the residual stream stay float.  Rotary cos / sin come from the same

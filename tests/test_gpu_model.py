@@ -81,10 +81,13 @@ def test_block_rows_bitwise_equal_single_token_steps(dtype, k, prompt_len):
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 def test_large_block_matches_oracle(dtype):
-    """A block of more than 64 rows (the prompt-prefill path: library GEMMs on the caller's weights
+    """A block of more than 64 rows (the prompt-prefill path: matrix-core GEMMs on the caller's weights
     around row-wise kernels that round where the decode kernels round) matches the oracle's block
     forward: its logits, and the K/V it leaves in the cache, read back by the next (decode-size) block.
-    Batch 2 x 70 rows after a 40-token prefix prefilled in 16-row blocks."""
+    Batch 2 x 70 rows after a 40-token prefix prefilled in 16-row blocks: 140 GEMM rows (a partial
+    128-row tile), a 688-wide FFN (a down contraction that ends inside a 64-wide stage, and a gate|up
+    column tile that straddles the two stacked matrices) and a 1000-entry vocabulary (a partial
+    column tile)."""
     if dtype == "bf16":
         shape = synth.small_shape(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=688, vocab=1000,
                                   n_adaptive=5, rope_base=1e6, dtype="bf16")
