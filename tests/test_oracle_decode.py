@@ -132,6 +132,15 @@ def test_splitmix64_published_vectors():
             assert S.splitmix64(int(seed), n) == int(h, 16)
 
 
+def test_uniform_is_the_published_stream_from_output_one():
+    """U(seed, 0, pos) takes output number pos + 1 of the generator started at the seed: its top 53
+    bits, scaled to [0, 1).  The published first outputs fix both the offset and the scaling."""
+    vec = json.load(open(os.path.join(GOLDEN, "splitmix64_vectors.json")))["vectors"]
+    for seed, outs in vec.items():
+        for pos, h in enumerate(outs):
+            assert S.uniform(int(seed), 0, pos) == (int(h, 16) >> 11) / float(1 << 53)
+
+
 def test_uniform_keyed_stream_is_uniform():
     u = np.array([S.uniform(3, b, p) for b in range(4) for p in range(25000)])
     assert u.min() >= 0.0 and u.max() < 1.0
@@ -185,6 +194,36 @@ def test_sampler_reductions():
     # p = 1, no top-k: the full softmax
     sm = np.exp(lg.astype(np.float64) - lg.max())
     np.testing.assert_allclose(_interval_freqs(lg, 1.0, 1.0, 0), sm / sm.sum(), atol=5e-5)
+
+
+def test_nucleus_boundary_is_inclusive():
+    """The nucleus is the smallest top set whose probability reaches p (Section 2.1 uses nucleus
+    sampling; the set's mass may equal p exactly).  A temperature of 1e30 makes every weight
+    exp(z - zmax) exactly 1.0 in float64 while the order of the logits stays, so four ids have
+    probability 1/4 each: p = 0.5 keeps exactly the top two, p = 0.75 the top three, and the inverse
+    CDF over {0, 1} sends u = 0.9 to id 1 (a strict comparison would keep one id more)."""
+    lg = np.array([3.0, 2.0, 1.0, 0.0], np.float32)
+    ids, e, _ = S.nucleus_set(lg, 1e30, 0.5)
+    assert list(ids) == [0, 1] and list(e) == [1.0, 1.0]
+    ids, _, _ = S.nucleus_set(lg, 1e30, 0.75)
+    assert list(ids) == [0, 1, 2]
+    assert S.sample(lg, 1e30, 0.5, 0, 0.9)[0] == 1
+    assert S.sample(lg, 1e30, 0.5, 0, 0.4)[0] == 0
+    assert S.sample(lg, 1e30, 0.75, 0, 0.9)[0] == 2
+
+
+def test_draft_step1_nucleus_samples_row0_and_argmaxes_the_rest():
+    """Draft step 1 in nucleus mode (the reading of Eq. 1 in nucleus decoding): row 0 gives the next
+    token, sampled with the key of its position; rows 1..k are the drafts, each the most probable id
+    of its row (lowest id among ties).  Flat rows make a sampled row differ from the arg-max."""
+    V, q = 16, 6
+    lg = np.zeros((q, V), np.float32)
+    lg[:, 5] = 1e-3                                 # a unique arg-max, far from certain under T = 1
+    out, m, _ = D.verify_nucleus(lg, None, 1.0, 1.0, 0, 99, 0, 40)
+    assert m == 0 and list(out[1:]) == [5] * (q - 1)
+    assert out[0] == S.sample(lg[0], 1.0, 1.0, 0, S.uniform(99, 0, 40))[0]
+    # with these keys, sampling rows 1..k would not give the arg-max in every row
+    assert any(S.sample(lg[j], 1.0, 1.0, 0, S.uniform(99, 0, 40 + j))[0] != 5 for j in range(1, q))
 
 
 def test_sampler_ties_at_threshold_are_all_kept():
