@@ -203,6 +203,69 @@ def test_verify_nucleus_bit_exact(std, T, p, top_k):
     ctx.close()
 
 
+def test_verify_nucleus_exact_top_p_boundary():
+    """The top-p set is the smallest top set whose probability reaches p, inclusive of exact equality.
+    At temperature 1e30 every id of a row with distinct logits weighs exactly 1.0 in float64, so at
+    p = 0.5 the nucleus is exactly the top half (16008 of 32016 ids), where the mass equals p * E
+    exactly; the sampled ids and the accepted lengths must equal the oracle's."""
+    Bn, q, V = 2, 4, 32016
+    row = -np.arange(V, dtype=np.float32) * np.float32(1e-3)   # distinct, descending: id 0 largest
+    lg = np.ascontiguousarray(np.broadcast_to(row, (Bn, q, V)))
+    T, p, seed = 1e30, 0.5, 777
+    pos0 = np.array([5, 9000], np.int32)
+    ids, _, _ = S.nucleus_set(row, T, p)
+    assert len(ids) == V // 2
+    ref = [D.verify_nucleus(lg[b], np.zeros(q - 1), T, p, 0, seed, b, int(pos0[b])) for b in range(Bn)]
+    drafts = np.stack([ref[b][0][: q - 1] for b in range(Bn)]).astype(np.int32)   # accept every draft
+    ctx = _tiny_ctx(Bn, q, V)
+    tok = torch.empty(Bn * q, dtype=torch.int32, device="cuda")
+    m = torch.empty(Bn, dtype=torch.int32, device="cuda")
+    B.sdsat_verify_nucleus(ctx.handle, Bn, q, torch.from_numpy(lg).cuda(), torch.from_numpy(drafts).cuda(), T, p,
+                           0, seed, torch.from_numpy(pos0).cuda(), tok, m)
+    torch.cuda.synchronize()
+    tok, m = tok.cpu().numpy().reshape(Bn, q), m.cpu().numpy()
+    for b in range(Bn):
+        s_, rm, _ = D.verify_nucleus(lg[b], drafts[b], T, p, 0, seed, b, int(pos0[b]))
+        assert list(tok[b]) == list(s_) and m[b] == rm == q - 1, b
+        assert all(0 <= t < V // 2 for t in tok[b])
+    ctx.close()
+
+
+@pytest.mark.parametrize("top_k", [10, 60, 20000])
+def test_verify_nucleus_top_k_ties_keep_lower_ids(top_k):
+    """Top-k with ties at the cut keeps exactly k ids, the lower ids first.  Logits from {0, 1, 2}
+    put about 10700 ids in the top tie group: top_k 10 (the small top-k path) and 60 (the radix path)
+    cut inside it, 20000 keeps the whole group and cuts inside the next.  Samples and accepted
+    lengths must equal the oracle's."""
+    Bn, q, V = 4, 3, 32016
+    rng = np.random.default_rng(21)
+    lg = rng.integers(0, 3, (Bn, q, V)).astype(np.float32)
+    T, p, seed = 1.0, 0.9, 4242
+    pos0 = (50 + 13 * np.arange(Bn)).astype(np.int32)
+    ref = [D.verify_nucleus(lg[b], np.zeros(q - 1), T, p, top_k, seed, b, int(pos0[b])) for b in range(Bn)]
+    drafts = np.zeros((Bn, q - 1), np.int32)
+    for b in range(Bn):
+        s_ = ref[b][0]
+        mb = b % q
+        drafts[b] = (s_[: q - 1] + 1) % V
+        drafts[b, :mb] = s_[:mb]
+    ctx = _tiny_ctx(Bn, q, V)
+    tok = torch.empty(Bn * q, dtype=torch.int32, device="cuda")
+    m = torch.empty(Bn, dtype=torch.int32, device="cuda")
+    B.sdsat_verify_nucleus(ctx.handle, Bn, q, torch.from_numpy(lg).cuda(), torch.from_numpy(drafts).cuda(), T, p,
+                           top_k, seed, torch.from_numpy(pos0).cuda(), tok, m)
+    torch.cuda.synchronize()
+    tok, m = tok.cpu().numpy().reshape(Bn, q), m.cpu().numpy()
+    for b in range(Bn):
+        s_, rm, margin = D.verify_nucleus(lg[b], drafts[b], T, p, top_k, seed, b, int(pos0[b]))
+        assert margin > 1e-9
+        assert list(tok[b]) == list(s_) and m[b] == rm == b % q, b
+        for j in range(q):   # every sample lies among the k kept ids
+            top = np.lexsort((np.arange(V), -lg[b, j]))[:top_k]
+            assert tok[b, j] in set(top.tolist())
+    ctx.close()
+
+
 # ---------------------------------------------------------------- commit
 def test_commit_chain_and_tree_gather():
     wl = helpers.small_bf16()
