@@ -147,7 +147,7 @@ int sdsat_verify_greedy(sdsat_ctx* ctx, int32_t batch, int32_t q, const float* d
  * With d_drafts: every row is sampled and n_accept counts leading matches as in
  * sdsat_verify_greedy.  Without (draft step 1): row 0 is sampled, rows 1..q-1
  * are arg-maxed (the chain of most probable drafts), n_accept = 0.
- * Requires V <= 32768.  Stream-ordered. */
+ * Requires V <= 131072 (SDSAT_EUNSUPPORTED otherwise).  Stream-ordered. */
 int sdsat_verify_nucleus(sdsat_ctx* ctx, int32_t batch, int32_t q, const float* d_logits,
                          const int32_t* d_drafts, float temperature, float top_p, int32_t top_k,
                          uint64_t seed, const int32_t* d_pos0, int32_t* d_tokens_out,

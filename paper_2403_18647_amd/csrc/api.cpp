@@ -669,7 +669,7 @@ int sdsat_verify_nucleus(sdsat_ctx* c, int32_t batch, int32_t q, const float* d_
     if (rc) return rc;
     if (!d_logits || !d_tokens_out || !d_pos0 || (d_drafts && !d_n_accept))
         return fail(c, SDSAT_EINVAL, "NULL logits, tokens_out, pos0, or n_accept with drafts");
-    if (c->D.V > 32768) return fail(c, SDSAT_EUNSUPPORTED, "nucleus verification needs vocab <= 32768");
+    if (c->D.V > 131072) return fail(c, SDSAT_EUNSUPPORTED, "nucleus verification needs vocab <= 131072");
     if (!(top_p > 0.f) || std::isnan(temperature)) return fail(c, SDSAT_EINVAL, "top_p must be > 0");
     HIPCHK(c, launch_verify_nucleus(d_logits, batch, q, c->D.V, d_drafts, q - 1, temperature, top_p, top_k, seed,
                                     d_pos0, d_tokens_out, d_n_accept, c->verify_cnt, c->stream));
@@ -713,7 +713,7 @@ int generate_impl(sdsat_ctx* c, int32_t batch, const int32_t* h_prompts, int32_t
     if (batch * q2 > 64) return fail(c, SDSAT_ECAPACITY, "batch * (k + 1) (tree: 1 + k * width) must be <= 64");
     if (mode != SDSAT_MODE_GREEDY && mode != SDSAT_MODE_NUCLEUS) return fail(c, SDSAT_EINVAL, "bad mode");
     const bool nucleus = mode == SDSAT_MODE_NUCLEUS && temperature > 0.f;
-    if (nucleus && D.V > 32768) return fail(c, SDSAT_EUNSUPPORTED, "nucleus verification needs vocab <= 32768");
+    if (nucleus && D.V > 131072) return fail(c, SDSAT_EUNSUPPORTED, "nucleus verification needs vocab <= 131072");
     for (int j = 0; j < k; ++j)
         if (h_adaptive_ids[j] < 0 || h_adaptive_ids[j] >= D.V + D.A)
             return fail(c, SDSAT_EINVAL, "adaptive id out of range");

@@ -116,7 +116,8 @@ hipError_t launch_verify_greedy(const float* logits, int B, int q, int V, const 
 
 // ---------------------------------------------------------------- nucleus
 // 1024 threads x 32 contiguous ids (V <= 32768); each thread keeps its ids' keys and float64
-// weights in registers and a bit mask (one bit per id) of the kept and nucleus ids
+// weights in registers and a bit mask (one bit per id) of the kept and nucleus ids.  Longer
+// vocabularies go chunk by chunk (sample_row_chunked).
 static constexpr int kNT = 1024;
 static constexpr int kCPT = 32;
 using Bits = uint32_t;
@@ -276,56 +277,74 @@ __device__ float block_max_f(float v, float* s_buf) {
 // Every thread keeps private per-digit sums of its own ids in LDS (column t of
 // hist[digit][thread]), so no atomics are needed and the totals of each digit
 // are formed in a fixed order: wave w sums digit w, lane l over threads l,
-// l + 64, ... in turn, then a butterfly.  Returns the largest key K whose
+// l + 64, ... in turn, then a butterfly.  The result is the largest key K whose
 // weight sum over kept ids with key >= K reaches `goal` (the lowest key of the
 // final range if rounding leaves every sum short of it) and, in *mass, that
-// sum.  w_of(i) gives id id0 + i's weight (0 for ids outside the kept set).
+// sum.
+
+// One id's weight into the thread's own column of the pass's digit histogram
+// (a no-return LDS add: no round trip, and the adds to one word land in
+// program order, one writer, so the sums repeat bit for bit).
+__device__ __forceinline__ void radix_add(double* hist, uint32_t key, int shift, double w) {
+    __hip_atomic_fetch_add(&hist[((key >> shift) & 15u) * kNT + threadIdx.x], w, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+__device__ __forceinline__ void radix_clear(double* hist) {
+#pragma unroll
+    for (int v = 0; v < kBins; ++v) hist[v * kNT + threadIdx.x] = 0.0;
+}
+
+// After a pass's adds: the digit totals in a fixed order, then the digit whose
+// running sum from the top first reaches `goal` (every wave takes the same
+// decision); extends `prefix` and the mass above / at it.
+__device__ __forceinline__ void radix_pick(const double* hist, double* s_tot, int shift, double goal,
+                                           uint32_t& prefix, double& above, double& at) {
+    const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < kBins / kWaves; ++h) {
+        const int bin = wave + h * kWaves;
+        double sum = 0.0;
+#pragma unroll
+        for (int j = 0; j < kNT / 64; ++j) sum += hist[bin * kNT + j * 64 + lane];
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) sum += dshfl_xor(sum, o);
+        if (lane == 0) s_tot[bin] = sum;
+    }
+    __syncthreads();
+    // lane v holds digit v's total; walk the digits from the top
+    const double mine = s_tot[lane & (kBins - 1)];
+    double acc = above, before = above;
+    int best = 0;
+    for (int v = kBins - 1; v >= 0; --v) {
+        before = acc;
+        acc += readlane_d(mine, v);
+        if (acc >= goal) { best = v; break; }
+    }
+    prefix |= (uint32_t)best << shift;
+    above = before;
+    at = acc;
+}
+
+// w_of(i) gives id id0 + i's weight (0 for ids outside the kept set).
 template <typename WeightFn>
 __device__ __forceinline__ uint32_t radix_threshold(const uint32_t (&keys)[kCPT], Bits kept, WeightFn w_of, double goal,
                                     double* hist, double* s_tot, double* mass) {
-    const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
     uint32_t prefix = 0;
     double above = 0.0, at = 0.0;
 #pragma unroll 1
     for (int shift = 28; shift >= 0; shift -= 4) {
         const uint32_t hi = shift == 28 ? 0u : 0xFFFFFFFFu << (shift + 4);
-#pragma unroll
-        for (int v = 0; v < kBins; ++v) hist[v * kNT + t] = 0.0;
+        radix_clear(hist);
 #pragma unroll
         for (int i = 0; i < kCPT; ++i) {
             if (!((kept >> i) & 1u)) continue;
             const uint32_t key = keys[i];
             if ((key & hi) != (prefix & hi)) continue;
-            // no-return LDS add on the thread's own column: no round trip, and the adds to one
-            // word land in program order (one writer), so the sums repeat bit for bit
-            __hip_atomic_fetch_add(&hist[((key >> shift) & 15u) * kNT + t], w_of(i), __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_WORKGROUP);
+            radix_add(hist, key, shift, w_of(i));
         }
-        __syncthreads();
-#pragma unroll
-        for (int h = 0; h < kBins / kWaves; ++h) {
-            const int bin = wave + h * kWaves;
-            double sum = 0.0;
-#pragma unroll
-            for (int j = 0; j < kNT / 64; ++j) sum += hist[bin * kNT + j * 64 + lane];
-#pragma unroll
-            for (int o = 32; o > 0; o >>= 1) sum += dshfl_xor(sum, o);
-            if (lane == 0) s_tot[bin] = sum;
-        }
-        __syncthreads();
-        // every wave walks the 16 digit totals from the top (lane v holds digit v's) and takes the
-        // same decision
-        const double mine = s_tot[lane & (kBins - 1)];
-        double acc = above, before = above;
-        int best = 0;
-        for (int v = kBins - 1; v >= 0; --v) {
-            before = acc;
-            acc += readlane_d(mine, v);
-            if (acc >= goal) { best = v; break; }
-        }
-        prefix |= (uint32_t)best << shift;
-        above = before;
-        at = acc;
+        radix_pick(hist, s_tot, shift, goal, prefix, above, at);
     }
     *mass = at;
     return prefix;
@@ -460,15 +479,8 @@ __device__ __forceinline__ bool sample_small_topk(const uint32_t (&keys)[kCPT], 
     return true;
 }
 
-__device__ __forceinline__ int sample_row(const float* row, int V, double T, double p, int top_k, double u) {
-    __shared__ double s_hist[kBins * kNT];   // 128 KiB: per-thread digit columns
-    __shared__ double s_tot[kBins];          // digit totals (read by every thread after the last pass)
-    __shared__ double s_d[kWaves];
-    __shared__ int s_i[kWaves];
-    __shared__ float s_f[kWaves];
-    const int id0 = threadIdx.x * kCPT;
-    // ids id0 .. id0+31 as order-preserving keys (the float is recovered from the key where needed)
-    uint32_t keys[kCPT];
+// ids id0 .. id0+31 of a row as order-preserving keys (ids past V: -inf)
+__device__ __forceinline__ void load_keys(const float* row, int V, int id0, uint32_t (&keys)[kCPT]) {
 #pragma unroll
     for (int i = 0; i < kCPT; i += 4) {
         if (id0 + i + 3 < V && (V & 3) == 0) {
@@ -480,6 +492,18 @@ __device__ __forceinline__ int sample_row(const float* row, int V, double T, dou
             for (int j = 0; j < 4; ++j) keys[i + j] = order_key(id0 + i + j < V ? row[id0 + i + j] : -INFINITY);
         }
     }
+}
+
+__device__ __forceinline__ int sample_row(const float* row, int V, double T, double p, int top_k, double u) {
+    __shared__ double s_hist[kBins * kNT];   // 128 KiB: per-thread digit columns
+    __shared__ double s_tot[kBins];          // digit totals (read by every thread after the last pass)
+    __shared__ double s_d[kWaves];
+    __shared__ int s_i[kWaves];
+    __shared__ float s_f[kWaves];
+    const int id0 = threadIdx.x * kCPT;
+    // ids id0 .. id0+31 as order-preserving keys (the float is recovered from the key where needed)
+    uint32_t keys[kCPT];
+    load_keys(row, V, id0, keys);
     Bits kept = 0;   // bit i: id0+i is kept by top-k
 #pragma unroll
     for (int i = 0; i < kCPT; ++i) if (id0 + i < V) kept |= 1u << i;
@@ -554,6 +578,152 @@ __device__ __forceinline__ int sample_row(const float* row, int V, double T, dou
     return cand;
 }
 
+// ---- vocabularies past one chunk of kNT * kCPT ids
+// Chunk c covers ids [c * kChunk, (c + 1) * kChunk); thread t holds ids
+// c * kChunk + 32 t + i of each.  Only the kept bits stay resident (in LDS);
+// every pass reloads a chunk's keys from the row (from L2 after the first) and
+// recomputes their float64 weights, so registers do not grow with V.  The
+// chunks are visited in order, so each lower-ids-first rule (top-k ties, the
+// inverse CDF) keeps ascending id order.  Same decisions as sample_row: top-k
+// by a count threshold, top-p by a weight threshold, inverse CDF.
+static constexpr int kChunk = kNT * kCPT;
+static constexpr int kMaxChunks = 4;   // V <= 131072
+
+__device__ __forceinline__ int sample_row_chunked(const float* row, int V, double T, double p, int top_k, double u) {
+    __shared__ double s_hist[kBins * kNT];     // 128 KiB: per-thread digit columns
+    __shared__ Bits s_kept[kMaxChunks * kNT];  // thread t's kept bits of chunk c at [c * kNT + t]
+    __shared__ double s_tot[kBins];
+    __shared__ double s_d[kWaves];
+    __shared__ int s_i[kWaves];
+    __shared__ float s_f[kWaves];
+    const int t = threadIdx.x, tb = t * kCPT;
+    const int nch = (V + kChunk - 1) / kChunk;
+    uint32_t keys[kCPT];
+    for (int c = 0; c < nch; ++c) {   // each thread reads back only its own words
+        Bits kb = 0;
+#pragma unroll
+        for (int i = 0; i < kCPT; ++i) if (c * kChunk + tb + i < V) kb |= 1u << i;
+        s_kept[c * kNT + t] = kb;
+    }
+    if (top_k > 0 && top_k < V) {
+        // largest key Kk with count(key >= Kk) >= top_k (counts are exact in double)
+        uint32_t Kk = 0;
+        double above = 0.0, at = 0.0;
+#pragma unroll 1
+        for (int shift = 28; shift >= 0; shift -= 4) {
+            const uint32_t hi = shift == 28 ? 0u : 0xFFFFFFFFu << (shift + 4);
+            radix_clear(s_hist);
+            for (int c = 0; c < nch; ++c) {
+                load_keys(row, V, c * kChunk + tb, keys);
+                const Bits kb = s_kept[c * kNT + t];
+#pragma unroll
+                for (int i = 0; i < kCPT; ++i)
+                    if (((kb >> i) & 1u) && (keys[i] & hi) == (Kk & hi)) radix_add(s_hist, keys[i], shift, 1.0);
+            }
+            radix_pick(s_hist, s_tot, shift, (double)top_k, Kk, above, at);
+        }
+        int gt = 0;
+        for (int c = 0; c < nch; ++c) {
+            load_keys(row, V, c * kChunk + tb, keys);
+            const Bits kb = s_kept[c * kNT + t];
+#pragma unroll
+            for (int i = 0; i < kCPT; ++i) gt += ((kb >> i) & 1u) && keys[i] > Kk;
+        }
+        const int need = top_k - block_sum_i(gt, s_i);
+        int base = 0;   // ids at Kk in earlier chunks
+        for (int c = 0; c < nch; ++c) {
+            load_keys(row, V, c * kChunk + tb, keys);
+            const Bits kb = s_kept[c * kNT + t];
+            int eq = 0;
+#pragma unroll
+            for (int i = 0; i < kCPT; ++i) eq += ((kb >> i) & 1u) && keys[i] == Kk;
+            int rank = base + block_exscan_i(eq, s_i);
+            base += block_sum_i(eq, s_i);
+            Bits nk = 0;
+#pragma unroll
+            for (int i = 0; i < kCPT; ++i) {
+                if (!((kb >> i) & 1u)) continue;
+                if (keys[i] > Kk) nk |= 1u << i;
+                else if (keys[i] == Kk) { if (rank < need) nk |= 1u << i; ++rank; }
+            }
+            s_kept[c * kNT + t] = nk;
+        }
+    }
+    uint32_t kmax = 0;
+    for (int c = 0; c < nch; ++c) {
+        load_keys(row, V, c * kChunk + tb, keys);
+        const Bits kb = s_kept[c * kNT + t];
+#pragma unroll
+        for (int i = 0; i < kCPT; ++i) if ((kb >> i) & 1u) kmax = max(kmax, keys[i]);
+    }
+    const float lmax = block_max_f(key_value(kmax), s_f);
+    const double zmax = (double)lmax / T;
+    double tot[1] = {0.0};
+    for (int c = 0; c < nch; ++c) {
+        load_keys(row, V, c * kChunk + tb, keys);
+        const Bits kb = s_kept[c * kNT + t];
+#pragma unroll
+        for (int i = 0; i < kCPT; ++i)
+            if ((kb >> i) & 1u) tot[0] += exp((double)key_value(keys[i]) / T - zmax);
+    }
+    block_sum_d<1>(tot, s_d);
+    const double pE = (p < 1.0 ? p : 1.0) * tot[0];
+
+    // top-p threshold key and the mass of the nucleus
+    uint32_t Ks = 0;
+    double above = 0.0, mass = 0.0;
+#pragma unroll 1
+    for (int shift = 28; shift >= 0; shift -= 4) {
+        const uint32_t hi = shift == 28 ? 0u : 0xFFFFFFFFu << (shift + 4);
+        radix_clear(s_hist);
+        for (int c = 0; c < nch; ++c) {
+            load_keys(row, V, c * kChunk + tb, keys);
+            const Bits kb = s_kept[c * kNT + t];
+#pragma unroll
+            for (int i = 0; i < kCPT; ++i)
+                if (((kb >> i) & 1u) && (keys[i] & hi) == (Ks & hi))
+                    radix_add(s_hist, keys[i], shift, exp((double)key_value(keys[i]) / T - zmax));
+        }
+        radix_pick(s_hist, s_tot, shift, pE, Ks, above, mass);
+    }
+
+    // inverse CDF over the nucleus in ascending id order, chunk by chunk
+    const double target = u * mass;
+    double run = 0.0;   // nucleus mass of the earlier chunks
+    int last = -1;
+    for (int c = 0; c < nch; ++c) {
+        load_keys(row, V, c * kChunk + tb, keys);
+        const Bits kb = s_kept[c * kNT + t];
+        double e[kCPT];
+        double loc[1] = {0.0};
+        Bits inN = 0;
+#pragma unroll
+        for (int i = 0; i < kCPT; ++i) {
+            e[i] = 0.0;
+            if (((kb >> i) & 1u) && keys[i] >= Ks) {
+                e[i] = exp((double)key_value(keys[i]) / T - zmax);
+                loc[0] += e[i];
+                inN |= 1u << i;
+            }
+        }
+        double cum = run + block_exscan_d(loc[0], s_d);
+        int cand = 0x7fffffff;
+#pragma unroll
+        for (int i = 0; i < kCPT; ++i) {
+            if (!((inN >> i) & 1u)) continue;
+            cum += e[i];
+            last = c * kChunk + tb + i;
+            if (cand == 0x7fffffff && cum > target) cand = c * kChunk + tb + i;
+        }
+        cand = block_min_i(cand, s_i);
+        if (cand != 0x7fffffff) return cand;
+        block_sum_d<1>(loc, s_d);
+        run += loc[0];
+    }
+    return block_max_i(last, s_i);
+}
+
+template <bool CHUNKED>
 __global__ void __launch_bounds__(kNT) verify_nucleus_kernel(const float* logits, int q, int V, const int* drafts,
                                                              int drafts_ld, float temperature, float top_p,
                                                              int top_k, uint64_t seed, const int* pos0,
@@ -568,7 +738,8 @@ __global__ void __launch_bounds__(kNT) verify_nucleus_kernel(const float* logits
     int t;
     if (sample) {
         const double u = keyed_uniform(seed, b, pos0[b] + (row_depth ? row_depth[row] : j));
-        t = sample_row(lg, V, (double)temperature, (double)top_p, top_k, u);
+        if constexpr (CHUNKED) t = sample_row_chunked(lg, V, (double)temperature, (double)top_p, top_k, u);
+        else t = sample_row(lg, V, (double)temperature, (double)top_p, top_k, u);
     } else {
         t = block_argmax<kNT>(lg, V, s_val, s_idx);
     }
@@ -579,9 +750,10 @@ __global__ void __launch_bounds__(kNT) verify_nucleus_kernel(const float* logits
 hipError_t launch_verify_nucleus(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,
                                  float temperature, float top_p, int top_k, uint64_t seed, const int* pos0,
                                  int* tokens_out, int* n_accept, int* counter, hipStream_t s, const int* row_depth) {
-    if (V > kNT * kCPT || (row_depth && drafts)) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(verify_nucleus_kernel, dim3(B * q), dim3(kNT), 0, s, logits, q, V, drafts, drafts_ld,
-                       temperature, top_p, top_k, seed, pos0, row_depth, tokens_out, n_accept, counter);
+    if (V > kChunk * kMaxChunks || (row_depth && drafts)) return hipErrorInvalidValue;
+    auto kern = V > kChunk ? verify_nucleus_kernel<true> : verify_nucleus_kernel<false>;
+    hipLaunchKernelGGL(kern, dim3(B * q), dim3(kNT), 0, s, logits, q, V, drafts, drafts_ld, temperature, top_p, top_k,
+                       seed, pos0, row_depth, tokens_out, n_accept, counter);
     return hipGetLastError();
 }
 

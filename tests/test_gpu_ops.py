@@ -266,6 +266,62 @@ def test_verify_nucleus_top_k_ties_keep_lower_ids(top_k):
     ctx.close()
 
 
+@pytest.mark.parametrize("V,T,p,top_k", [(50000, 0.8, 0.95, 0), (50000, 1.0, 0.9, 100), (131072, 0.8, 0.95, 0),
+                                         (131072, 1.0, 0.95, 10), (128256, 1.5, 0.98, 0)])
+def test_verify_nucleus_long_vocab_bit_exact(V, T, p, top_k):
+    """Vocabularies past 32768 ids (sampled chunk by chunk): samples, accepted lengths and the
+    draft-step-1 form equal the oracle's, as for the 32016-id rows.  Ties at a top-k cut and the
+    ascending-id inverse CDF cross chunk boundaries here: a tie group spans ids in several chunks."""
+    print(f"nucleus V={V} T={T} p={p} top_k={top_k}", flush=True)
+    Bn, q = 3, 4
+    lg = _logits(Bn, q, V, 2.0, 6)
+    lg[1, 1, [5, 40000, V - 1]] = lg[1, 1].max() + 0.5   # a three-way tie for the top across chunks
+    seed = 2024
+    pos0 = (17 + 5 * np.arange(Bn)).astype(np.int32)
+    ref = [D.verify_nucleus(lg[b], np.zeros(q - 1), T, p, top_k, seed, b, int(pos0[b])) for b in range(Bn)]
+    drafts = np.zeros((Bn, q - 1), np.int32)
+    for b in range(Bn):
+        s_ = ref[b][0]
+        mb = b % q
+        drafts[b] = (s_[: q - 1] + 1) % V
+        drafts[b, :mb] = s_[:mb]
+    ctx = _tiny_ctx(Bn, q, V)
+    tok = torch.empty(Bn * q, dtype=torch.int32, device="cuda")
+    m = torch.empty(Bn, dtype=torch.int32, device="cuda")
+    B.sdsat_verify_nucleus(ctx.handle, Bn, q, torch.from_numpy(lg).cuda(), torch.from_numpy(drafts).cuda(), T, p,
+                           top_k, seed, torch.from_numpy(pos0).cuda(), tok, m)
+    torch.cuda.synchronize()
+    tok, m = tok.cpu().numpy().reshape(Bn, q), m.cpu().numpy()
+    for b in range(Bn):
+        s_, rm, margin = D.verify_nucleus(lg[b], drafts[b], T, p, top_k, seed, b, int(pos0[b]))
+        assert margin > 1e-9
+        assert list(tok[b]) == list(s_) and m[b] == rm == b % q, b
+    tok1 = torch.empty(Bn * q, dtype=torch.int32, device="cuda")
+    B.sdsat_verify_nucleus(ctx.handle, Bn, q, torch.from_numpy(lg).cuda(), None, T, p, top_k, seed,
+                           torch.from_numpy(pos0).cuda(), tok1, None)
+    torch.cuda.synchronize()
+    tok1 = tok1.cpu().numpy().reshape(Bn, q)
+    for b in range(Bn):
+        assert list(tok1[b]) == list(D.verify_nucleus(lg[b], None, T, p, top_k, seed, b, int(pos0[b]))[0])
+    assert tok1[1, 1] == 5   # row 1 of draft step 1 is the arg-max: the lowest of the tied ids
+    ctx.close()
+
+
+def test_verify_nucleus_vocab_limit():
+    """Past 131072 ids nucleus verification reports SDSAT_EUNSUPPORTED; greedy has no limit."""
+    Bn, q, V = 1, 2, 131073
+    ctx = _tiny_ctx(Bn, q, V)
+    lg = torch.zeros((Bn * q, V), dtype=torch.float32, device="cuda")
+    tok = torch.empty(Bn * q, dtype=torch.int32, device="cuda")
+    pos0 = torch.zeros(Bn, dtype=torch.int32, device="cuda")
+    with pytest.raises(B.SdsatError, match="131072"):
+        B.sdsat_verify_nucleus(ctx.handle, Bn, q, lg, None, 1.0, 0.9, 0, 1, pos0, tok, None)
+    B.sdsat_verify_greedy(ctx.handle, Bn, q, lg, None, tok, None)
+    torch.cuda.synchronize()
+    assert tok.cpu().numpy().tolist() == [0, 0]
+    ctx.close()
+
+
 # ---------------------------------------------------------------- commit
 def test_commit_chain_and_tree_gather():
     wl = helpers.small_bf16()
