@@ -128,7 +128,7 @@ struct sdsat_ctx {
     uint64_t* tree_mask = nullptr;
     float* logits = nullptr;
     // large blocks (more than kSkinnyRows rows): normalised rows (element type) and float GEMM outputs
-    void* hbuf = nullptr; float* c_qkv = nullptr; float* c_gu = nullptr; float* c_y = nullptr;
+    void* hbuf = nullptr; float* c_y = nullptr;
     int* h_pin = nullptr;   // pinned host staging
     size_t h_pin_ints = 0;
     int* h_rec = nullptr;      // pinned host copy of the loop records
@@ -219,11 +219,7 @@ void carve(sdsat_ctx* c, Carver& cv) {
     c->tree_mask = (uint64_t*)cv.take(bq * 8);
     c->logits = (float*)cv.take(bq * D.V * 4);
     c->hbuf = cv.take((size_t)D.maxM * D.d_pad * e);
-    if (D.maxM > kSkinnyRows) {
-        c->c_qkv = (float*)cv.take((size_t)D.maxM * 3 * D.d * 4);
-        c->c_gu = (float*)cv.take((size_t)D.maxM * 2 * D.F * 4);
-        c->c_y = (float*)cv.take((size_t)D.maxM * D.d * 4 * 2);   // two split-K halves
-    }
+    if (D.maxM > kSkinnyRows) c->c_y = (float*)cv.take((size_t)D.maxM * D.d * 4 * 2);   // two split-K halves
 }
 
 void* layer_k(sdsat_ctx* c, int l) { return (char*)c->kc + (size_t)l * c->layer_elems * c->D.esz; }
@@ -345,8 +341,32 @@ int big_gemm(sdsat_ctx* c, int M, int N, int K, const void* A, int lda, const vo
     return SDSAT_OK;
 }
 
+// The QKV GEMM of a large block with RoPE, the Q output and the K / V cache writes in its epilogue.
+int big_gemm_qkv(sdsat_ctx* c, int B, int q, const void* A, const void* const* w, int l) {
+    const Dims& D = c->D;
+    PrefillGemmArgs p{};
+    p.M = B * q; p.N = 3 * D.d; p.K = D.d; p.A = A; p.lda = D.d_pad;
+    p.W0 = w[1]; p.W1 = w[2]; p.W2 = w[3]; p.n_per = D.d; p.ksplit = 1;
+    p.ep = PG_QKV; p.q = q; p.H = D.H; p.Dh = D.Dh; p.S_max = D.S; p.cache_len = c->cache_len; p.rope = c->rope;
+    p.qbuf = (float*)c->qbuf; p.kc = layer_k(c, l); p.vc = layer_v(c, l); p.err = c->err_flag;
+    HIPCHK(c, launch_prefill_gemm(D.dtype, p, c->stream));
+    return SDSAT_OK;
+}
+
+// The gate | up GEMM of a large block with SwiGLU in its epilogue: u = silu(gate) * up in the element type.
+int big_gemm_swiglu(sdsat_ctx* c, int M, const void* A, const void* w_gate, const void* w_up) {
+    const Dims& D = c->D;
+    PrefillGemmArgs p{};
+    p.M = M; p.N = 2 * D.F; p.K = D.d; p.A = A; p.lda = D.d_pad;
+    p.W0 = w_gate; p.W1 = w_up; p.n_per = D.F; p.ksplit = 1;
+    p.ep = PG_SWIGLU; p.u = c->ubuf; p.ldu = D.F_pad;
+    HIPCHK(c, launch_prefill_gemm(D.dtype, p, c->stream));
+    return SDSAT_OK;
+}
+
 // Block forward of a large block (B*q > kSkinnyRows rows, chain mask): linear layers as matrix-core GEMMs
-// on the caller's weights, the rest in row-wise kernels that round where the skinny path rounds.
+// on the caller's weights (QKV and gate | up with their RoPE / cache and SwiGLU epilogues), the rest in
+// row-wise kernels that round where the skinny path rounds.
 int large_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, float* logits) {
     const Dims& D = c->D;
     const int M = B * q;
@@ -358,10 +378,8 @@ int large_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, float* l
     for (int l = 0; l < D.L; ++l) {
         const void* const* w = c->w_src.data() + 1 + 9 * l;   // attn_norm, wq, wk, wv, wo, ffn_norm, wg, wu, wd
         HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, eps, M, c->hbuf, D.d_pad, c->stream));
-        int rc = big_gemm(c, M, 3 * D.d, D.d, c->hbuf, D.d_pad, w[1], w[2], w[3], D.d, c->c_qkv, 3 * D.d);
+        int rc = big_gemm_qkv(c, B, q, c->hbuf, w, l);
         if (rc) return rc;
-        HIPCHK(c, launch_qkv_rope(D.dtype, c->c_qkv, 3 * D.d, M, q, D.H, D.Dh, c->cache_len, D.S, c->rope,
-                                  (float*)c->qbuf, layer_k(c, l), layer_v(c, l), c->err_flag, c->stream));
         rc = attention_layer(c, l, B, q, nullptr, (const float*)c->qbuf, c->obuf, 0, D.d_pad);
         if (rc) return rc;
         const size_t y_part = (size_t)D.maxM * D.d;   // offset of the second split-K half in c_y
@@ -371,9 +389,8 @@ int large_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, float* l
         HIPCHK(c, launch_resid_rows(c->c_y, split ? c->c_y + y_part : nullptr, D.d, M, D.d, c->x, D.d, c->xg, D.d_pad,
                                     c->ffn_norm[l], c->ssq, D.n_ssq, c->stream));
         HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, eps, M, c->hbuf, D.d_pad, c->stream));
-        rc = big_gemm(c, M, 2 * D.F, D.d, c->hbuf, D.d_pad, w[6], w[7], nullptr, D.F, c->c_gu, 2 * D.F);
+        rc = big_gemm_swiglu(c, M, c->hbuf, w[6], w[7]);
         if (rc) return rc;
-        HIPCHK(c, launch_swiglu_rows(D.dtype, c->c_gu, c->c_gu + D.F, 2 * D.F, M, D.F, c->ubuf, D.F_pad, c->stream));
         rc = big_gemm(c, M, D.d, D.F, c->ubuf, D.F_pad, w[8], nullptr, nullptr, D.d, c->c_y, D.d, y_part, &split);
         if (rc) return rc;
         HIPCHK(c, launch_resid_rows(c->c_y, split ? c->c_y + y_part : nullptr, D.d, M, D.d, c->x, D.d, c->xg, D.d_pad,

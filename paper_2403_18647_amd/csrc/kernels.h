@@ -146,12 +146,23 @@ hipError_t launch_rope_table(const double* inv_freq, int S, int half, float* rop
 // K must be a multiple of 8 (16-byte loads); rows of A past K read as zero only up to K.
 // With ksplit 2 (prefill_gemm_ksplit) the contraction is split in two halves whose partial products go
 // to C and C + c_part; the consumer adds them (partial 0 + partial 1).
+// Epilogues of the prefill GEMM: PG_STORE writes C (float); PG_QKV takes N = 3 n_per columns Q | K | V
+// (heads of Dh columns), applies RoPE at cache_len[b] + row and writes Q (float) to qbuf [M][H][Dh],
+// K and V in the element type into the cache (K [B][H][S_max][Dh], V key-permuted [B][H][S_max/32][Dh][32]);
+// PG_SWIGLU takes N = 2 n_per columns gate | up and writes u = silu(gate) * up in the element type to
+// u [M][ldu].  The fused epilogues need ksplit 1.
+enum { PG_STORE = 0, PG_QKV = 1, PG_SWIGLU = 2 };
 struct PrefillGemmArgs {
     int M, N, K;
     const void* A; int lda;
     const void* W0; const void* W1; const void* W2; int n_per;
     float* C; int ldc;
     int ksplit; size_t c_part;
+    int ep;
+    // PG_QKV
+    int q, H, Dh, S_max; const int* cache_len; const float* rope; float* qbuf; void* kc; void* vc; int* err;
+    // PG_SWIGLU
+    void* u; int ldu;
 };
 int prefill_gemm_ksplit(int M, int N, int K);
 hipError_t launch_prefill_gemm(int dtype, const PrefillGemmArgs& p, hipStream_t s);
@@ -159,16 +170,10 @@ hipError_t launch_prefill_gemm(int dtype, const PrefillGemmArgs& p, hipStream_t 
 // h = elem(xg / rms) with rms from the row's per-16-column sums of squares
 hipError_t launch_rms_rows(int dtype, const float* xg, int ldxg, const float* ssq, int n_ssq, int K, float eps, int M,
                            void* h, int ldh, hipStream_t s);
-// c[m] = Q | K | V (float, row stride ldc): RoPE, Q to qbuf [M][H][Dh], K / V into the cache at cache_len[b] + row
-hipError_t launch_qkv_rope(int dtype, const float* c, int ldc, int M, int q, int H, int Dh, const int* cache_len,
-                           int S_max, const float* rope, float* qbuf, void* kc, void* vc, int* err, hipStream_t s);
 // x += y (y = y0 + y1 when y1 is given: two split-K partials); xg = x o gnext; ssq = per-16-column sums
 // of squares of x
 hipError_t launch_resid_rows(const float* y, const float* y1, int ldy, int M, int N, float* x, int ldx, float* xg,
                              int ldxg, const float* gnext, float* ssq, int n_tiles, hipStream_t s);
-// u = elem(silu(g) * up)
-hipError_t launch_swiglu_rows(int dtype, const float* g, const float* up, int ldg, int M, int F, void* u, int ldu,
-                              hipStream_t s);
 
 // ---------------------------------------------------------------- verify
 hipError_t launch_verify_greedy(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,
