@@ -375,9 +375,10 @@ int large_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, float* l
     prof_begin(c, logits ? PK_BLOCK : PK_PREFILL, &evb);
     HIPCHK(c, launch_embed(D.dtype, c->embed, D.V + D.A, D.d, tokens, M, c->x, c->xg, c->attn_norm[0], D.d_pad,
                            c->ssq, D.n_ssq, c->err_flag, c->stream));
+    // layer 0's normalised input; later layers get theirs from the residual kernel before them
+    HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, eps, M, c->hbuf, D.d_pad, c->stream));
     for (int l = 0; l < D.L; ++l) {
         const void* const* w = c->w_src.data() + 1 + 9 * l;   // attn_norm, wq, wk, wv, wo, ffn_norm, wg, wu, wd
-        HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, eps, M, c->hbuf, D.d_pad, c->stream));
         int rc = big_gemm_qkv(c, B, q, c->hbuf, w, l);
         if (rc) return rc;
         rc = attention_layer(c, l, B, q, nullptr, (const float*)c->qbuf, c->obuf, 0, D.d_pad);
@@ -386,18 +387,17 @@ int large_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, float* l
         bool split = false;
         rc = big_gemm(c, M, D.d, D.d, c->obuf, D.d_pad, w[4], nullptr, nullptr, D.d, c->c_y, D.d, y_part, &split);
         if (rc) return rc;
-        HIPCHK(c, launch_resid_rows(c->c_y, split ? c->c_y + y_part : nullptr, D.d, M, D.d, c->x, D.d, c->xg, D.d_pad,
-                                    c->ffn_norm[l], c->ssq, D.n_ssq, c->stream));
-        HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, eps, M, c->hbuf, D.d_pad, c->stream));
+        HIPCHK(c, launch_resid_norm_rows(D.dtype, c->c_y, split ? c->c_y + y_part : nullptr, D.d, M, D.d, c->x, D.d,
+                                         c->ffn_norm[l], eps, c->hbuf, D.d_pad, c->stream));
         rc = big_gemm_swiglu(c, M, c->hbuf, w[6], w[7]);
         if (rc) return rc;
         rc = big_gemm(c, M, D.d, D.F, c->ubuf, D.F_pad, w[8], nullptr, nullptr, D.d, c->c_y, D.d, y_part, &split);
         if (rc) return rc;
-        HIPCHK(c, launch_resid_rows(c->c_y, split ? c->c_y + y_part : nullptr, D.d, M, D.d, c->x, D.d, c->xg, D.d_pad,
-                                    l + 1 < D.L ? c->attn_norm[l + 1] : c->final_norm, c->ssq, D.n_ssq, c->stream));
+        HIPCHK(c, launch_resid_norm_rows(D.dtype, c->c_y, split ? c->c_y + y_part : nullptr, D.d, M, D.d, c->x, D.d,
+                                         l + 1 < D.L ? c->attn_norm[l + 1] : c->final_norm, eps, c->hbuf, D.d_pad,
+                                         c->stream));
     }
     if (logits) {
-        HIPCHK(c, launch_rms_rows(D.dtype, c->xg, D.d_pad, c->ssq, D.n_ssq, D.d, eps, M, c->hbuf, D.d_pad, c->stream));
         int rc = big_gemm(c, M, D.V, D.d, c->hbuf, D.d_pad, c->w_src[2 + 9 * D.L], nullptr, nullptr, D.V, logits, D.V);
         if (rc) return rc;
     }

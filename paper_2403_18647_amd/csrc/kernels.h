@@ -170,10 +170,10 @@ hipError_t launch_prefill_gemm(int dtype, const PrefillGemmArgs& p, hipStream_t 
 // h = elem(xg / rms) with rms from the row's per-16-column sums of squares
 hipError_t launch_rms_rows(int dtype, const float* xg, int ldxg, const float* ssq, int n_ssq, int K, float eps, int M,
                            void* h, int ldh, hipStream_t s);
-// x += y (y = y0 + y1 when y1 is given: two split-K partials); xg = x o gnext; ssq = per-16-column sums
-// of squares of x
-hipError_t launch_resid_rows(const float* y, const float* y1, int ldy, int M, int N, float* x, int ldx, float* xg,
-                             int ldxg, const float* gnext, float* ssq, int n_tiles, hipStream_t s);
+// x += y (y = y0 + y1 when y1 is given: two split-K partials); h = elem((x o g) / rms(x)), bitwise what
+// the residual epilogue's per-16-column sums of squares and rms_rows give (rows of up to 8192 columns)
+hipError_t launch_resid_norm_rows(int dtype, const float* y, const float* y1, int ldy, int M, int N, float* x,
+                                  int ldx, const float* g, float eps, void* h, int ldh, hipStream_t s);
 
 // ---------------------------------------------------------------- verify
 hipError_t launch_verify_greedy(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,

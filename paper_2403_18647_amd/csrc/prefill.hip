@@ -48,25 +48,69 @@ __global__ void __launch_bounds__(256) rms_rows_kernel(const float* xg, int ldxg
         if (k0 + i < K) hr[k0 + i] = to_elem<T>(v[i] * inv);
 }
 
-// x[m][n] += y[m][n]; xg[m][n] = x[m][n] * gnext[n]; ssq[m][n/16] = the sum of
-// squares over each 16-column group (butterfly in the decode epilogue's order).
-__global__ void __launch_bounds__(256) resid_rows_kernel(const float* y, const float* y1, int ldy, int N, float* x,
-                                                         int ldx, float* xg, int ldxg, const float* gnext, float* ssq,
-                                                         int n_tiles) {
-    const int m = blockIdx.y, n = blockIdx.x * blockDim.x + threadIdx.x;
-    float ss = 0.f;
-    if (n < N) {
-        const float yv = y1 ? y[(size_t)m * ldy + n] + y1[(size_t)m * ldy + n] : y[(size_t)m * ldy + n];
-        const float v = x[(size_t)m * ldx + n] + yv;
-        x[(size_t)m * ldx + n] = v;
-        xg[(size_t)m * ldxg + n] = v * gnext[n];
-        ss = v * v;
+// The residual add and the next RMSNorm of a large block in one pass over each
+// row: x[m] += y[m] (+ y1[m], the second half of a split contraction), then
+// h[m] = elem((x[m] o g) / rms_m).  One workgroup per row; each thread keeps
+// its columns' x o g in registers.  The sums of squares are formed per 16-column
+// group in the decode residual epilogue's butterfly and reduced in rms_rows'
+// order (lane-strided, then a wave butterfly), so h is bitwise what a separate
+// residual pass and rms_rows give.
+static constexpr int kNormRowThreads = 1024;
+static constexpr int kNormRowMaxPer = 8;   // columns per thread: rows of up to 8192
+template <typename T>
+__global__ void __launch_bounds__(kNormRowThreads) resid_norm_rows_kernel(const float* y, const float* y1, int ldy,
+                                                                          int N, float* x, int ldx, const float* g,
+                                                                          float eps, T* h, int ldh) {
+    constexpr int NT = kNormRowThreads, P = kNormRowMaxPer;
+    __shared__ float s_ssq[P * NT / 16];
+    __shared__ float s_inv;
+    const int m = blockIdx.x, t = threadIdx.x;
+    const int nch = (N + NT - 1) / NT;
+    // every load first (indices clamped into the row), then the arithmetic
+    float yv[P], xv[P], gv[P];
+#pragma unroll
+    for (int c = 0; c < P; ++c) {
+        const int n = min(c * NT + t, N - 1);
+        yv[c] = xv[c] = gv[c] = 0.f;
+        if (c < nch) {
+            yv[c] = y1 ? y[(size_t)m * ldy + n] + y1[(size_t)m * ldy + n] : y[(size_t)m * ldy + n];
+            xv[c] = x[(size_t)m * ldx + n];
+            gv[c] = g[n];
+        }
     }
-    ss += __shfl_xor(ss, 8, 64);
-    ss += __shfl_xor(ss, 4, 64);
-    ss += __shfl_xor(ss, 2, 64);
-    ss += __shfl_xor(ss, 1, 64);
-    if ((n & 15) == 0 && n < N) ssq[(size_t)m * n_tiles + n / 16] = ss;
+#pragma unroll
+    for (int c = 0; c < P; ++c) {
+        if (c >= nch) continue;
+        const int n = c * NT + t;
+        float ss = 0.f;
+        if (n < N) {
+            const float v = xv[c] + yv[c];
+            x[(size_t)m * ldx + n] = v;
+            xv[c] = v * gv[c];   // x o g from here on
+            ss = v * v;
+        }
+        ss += __shfl_xor(ss, 8, 64);
+        ss += __shfl_xor(ss, 4, 64);
+        ss += __shfl_xor(ss, 2, 64);
+        ss += __shfl_xor(ss, 1, 64);
+        if ((n & 15) == 0 && n < N) s_ssq[n / 16] = ss;
+    }
+    __syncthreads();
+    if (t < 64) {
+        const int n_ssq = (N + 15) / 16;
+        float sum = 0.f;
+        for (int col = t; col < n_ssq; col += 64) sum += s_ssq[col];
+        sum = wave_sum(sum);
+        if (t == 0) s_inv = 1.0f / sqrtf(sum / (float)N + eps);
+    }
+    __syncthreads();
+    const float inv = s_inv;
+    T* hr = h + (size_t)m * ldh;
+#pragma unroll
+    for (int c = 0; c < P; ++c) {
+        const int n = c * NT + t;
+        if (c < nch && n < N) hr[n] = to_elem<T>(xv[c] * inv);
+    }
 }
 
 hipError_t launch_rms_rows(int dtype, const float* xg, int ldxg, const float* ssq, int n_ssq, int K, float eps, int M,
@@ -83,11 +127,16 @@ hipError_t launch_rms_rows(int dtype, const float* xg, int ldxg, const float* ss
     return hipGetLastError();
 }
 
-hipError_t launch_resid_rows(const float* y, const float* y1, int ldy, int M, int N, float* x, int ldx, float* xg,
-                             int ldxg, const float* gnext, float* ssq, int n_tiles, hipStream_t s) {
+hipError_t launch_resid_norm_rows(int dtype, const float* y, const float* y1, int ldy, int M, int N, float* x,
+                                  int ldx, const float* g, float eps, void* h, int ldh, hipStream_t s) {
     if (M < 1) return hipSuccess;
-    hipLaunchKernelGGL(resid_rows_kernel, dim3((N + 255) / 256, M), dim3(256), 0, s, y, y1, ldy, N, x, ldx, xg, ldxg,
-                       gnext, ssq, n_tiles);
+    if (N < 1 || N > kNormRowMaxPer * kNormRowThreads) return hipErrorInvalidValue;
+    if (dtype == 1)
+        hipLaunchKernelGGL(resid_norm_rows_kernel<uint16_t>, dim3(M), dim3(kNormRowThreads), 0, s, y, y1, ldy, N, x,
+                           ldx, g, eps, static_cast<uint16_t*>(h), ldh);
+    else
+        hipLaunchKernelGGL(resid_norm_rows_kernel<float>, dim3(M), dim3(kNormRowThreads), 0, s, y, y1, ldy, N, x, ldx,
+                           g, eps, static_cast<float*>(h), ldh);
     return hipGetLastError();
 }
 
