@@ -308,6 +308,16 @@ int fits(sdsat_ctx* c, int B, int q, bool* ok) {
 int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask, const float* qbuf, void* out,
                     int out_f32, int ldo) {
     const Dims& D = c->D;
+    if (!mask && q > 16) {   // many rows (prefill chunks): 64-row tiles, no key splits
+        AttnArgs a{};
+        a.qbuf = qbuf; a.kc = layer_k(c, layer); a.vc = layer_v(c, layer); a.cache_len = c->cache_len;
+        a.B = B; a.q = q; a.H = D.H; a.S_max = D.S; a.scale = (float)(1.0 / std::sqrt((double)D.Dh));
+        a.out = out; a.out_f32 = out_f32; a.ldo = ldo; a.err = c->err_flag;
+        hipEvent_t e0, e1;
+        prof_pair(c, PK_ATTN, &e0, &e1);
+        HIPCHK(c, launch_attention_rows(D.dtype, D.Dh, a, c->stream, e0, e1));
+        return SDSAT_OK;
+    }
     const AttnPlan p = plan_attention(B, D.H, q, D.Dh, max_hint(c, B), D.S);
     if (attention_plan_partial_floats(p, B, D.H, D.Dh) > c->attn_part_floats)   // sized at init for every plan
         return fail(c, SDSAT_EDEVICE, "attention plan needs more split partials than the workspace holds");

@@ -481,6 +481,157 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
     }
 }
 
+// Blocks of many rows with the chain mask (prefill chunks): one workgroup of
+// kRowWaves waves per (sequence, head, 64-row tile).  Wave w owns rows
+// 16w .. 16w + 15 of the tile and runs the per-block step above over every key
+// block its rows can see, so the waves need no merge.  A 32-key block's K rows
+// and V's key-permuted columns are contiguous runs of the cache; the workgroup
+// stages them in LDS (rows padded by 32 bytes, two buffers, the next block's
+// loads in flight in registers while the current one is used), so the tile
+// reads each block once instead of once per wave.
+static constexpr int kRowWaves = 4;
+template <typename T, int DH>
+__global__ void __launch_bounds__(64 * kRowWaves) attn_rows_kernel(AttnArgs a) {
+    constexpr int NDS = DH / 32, NDT = DH / 16, E = (int)sizeof(T);
+    constexpr int KLD = DH + 32 / E, VLD = 32 + 32 / E;   // staged row strides (elements)
+    constexpr int CH = 16 / E;                              // elements per 16-byte chunk
+    constexpr int NCH = 32 * DH / CH;                       // chunks per staged operand
+    constexpr int NT = 64 * kRowWaves, PER = NCH / NT;
+    static_assert(PER * NT == NCH, "whole chunks per thread");
+    constexpr int NQF = (E == 2 ? 2 : 1) * NDS;              // Q fragments per lane (hi, and lo for bf16)
+    __shared__ __align__(16) T s_k[2][32 * KLD];
+    __shared__ __align__(16) T s_v[2][DH * VLD];
+    __shared__ Frag<T> s_qf[kRowWaves][NQF * 64];
+
+    const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int c = lane & 15, g = lane >> 4;
+    const int q = a.q, n_rt = (q + 63) / 64;
+    const int rt = (int)blockIdx.x % n_rt, bh = (int)blockIdx.x / n_rt;
+    const int b = bh / a.H, h = bh % a.H;
+    const int L = a.cache_len[b];
+    if (L + q > a.S_max) {   // the host checks capacity; never read past this sequence's cache
+        if (tid == 0) atomicOr(a.err, 4);
+        return;
+    }
+    const T* kbase = reinterpret_cast<const T*>(a.kc) + ((size_t)b * a.H + h) * a.S_max * DH;
+    const T* vbase = reinterpret_cast<const T*>(a.vc) + ((size_t)b * a.H + h) * a.S_max * DH;
+    const int r0 = 64 * rt, w0 = r0 + 16 * wave, m = w0 + c;
+    const int nblk = (L + min(r0 + 63, q - 1) + 32) / 32;                 // the tile's last row
+    const int wblk = w0 < q ? (L + min(w0 + 15, q - 1) + 32) / 32 : 0;     // this wave's last row
+
+    // the wave's Q rows as matrix-core fragments (hi / lo) in its LDS region; rows past q read row q - 1
+    {
+        const f32x4_t* qsrc =
+            reinterpret_cast<const f32x4_t*>(a.qbuf + (((size_t)b * q + min(m, q - 1)) * a.H + h) * DH + 8 * g);
+#pragma unroll
+        for (int ds = 0; ds < NDS; ++ds) {
+            const f32x4_t q0 = qsrc[ds * 8], q1 = qsrc[ds * 8 + 1];
+            const float x8[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
+            Frag<T> fh, fl;
+            split_frag<T>(x8, fh, fl);
+            s_qf[wave][ds * 64 + lane] = fh;
+            if constexpr (E == 2) s_qf[wave][(NDS + ds) * 64 + lane] = fl;
+        }
+    }
+    // Two register sets of staged loads: while block i is used from LDS, block i + 1 (requested one
+    // step earlier) is on its way to the other LDS buffer and block i + 2 is requested.  Block indices
+    // are clamped (a repeated last block is staged, never used), and the steps run in unconditional
+    // pairs, so the wait before each LDS write counts only the older set's loads.
+    struct Stage { u32x4_t k[PER], v[PER]; };
+    Stage st0, st1;
+    auto gload = [&](Stage& r, int blk) {
+        const u32x4_t* ks = reinterpret_cast<const u32x4_t*>(kbase + (size_t)min(blk, nblk - 1) * 32 * DH);
+        const u32x4_t* vs = reinterpret_cast<const u32x4_t*>(vbase + (size_t)min(blk, nblk - 1) * 32 * DH);
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            r.k[i] = ks[tid + NT * i];
+            r.v[i] = vs[tid + NT * i];
+        }
+    };
+    auto lstore = [&](const Stage& r, int buf) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int ch = tid + NT * i;
+            *reinterpret_cast<u32x4_t*>(&s_k[buf][(ch / (DH / CH)) * KLD + (ch % (DH / CH)) * CH]) = r.k[i];
+            *reinterpret_cast<u32x4_t*>(&s_v[buf][(ch / (32 / CH)) * VLD + (ch % (32 / CH)) * CH]) = r.v[i];
+        }
+    };
+    gload(st0, 0);
+    gload(st1, 1);
+    lstore(st0, 0);
+    __syncthreads();
+
+    float rmax = -INFINITY, rsum = 0.f;
+    f32x4_t o[NDT];
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const int Tb = L + q;
+    // block i from LDS buffer i & 1; `next` holds block i + 1, `free` takes block i + 2
+    auto step = [&](int i, const Stage& next, Stage& free) {
+        const int buf = i & 1;
+        gload(free, i + 2);
+        if (i < wblk) {
+            Frag<T> kf[2][NDS], vf[NDT];
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                for (int ds = 0; ds < NDS; ++ds) kf[kt][ds] = Frag<T>::load(&s_k[buf][(16 * kt + c) * KLD + ds * 32 + 8 * g]);
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) vf[dt] = Frag<T>::load(&s_v[buf][(16 * dt + c) * VLD + 8 * g]);
+            attend_block<T, NDS, NDT>(kf, vf, s_qf[wave], lane, 0ull, i, m, L, Tb, q, false, a.scale, g, rmax, rsum, o);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // the other buffer was last read in step i - 1, before the barrier that ended it
+        lstore(next, buf ^ 1);
+        __syncthreads();
+    };
+    int i = 0;
+    for (; i + 1 < nblk; i += 2) {
+        step(i, st1, st0);
+        step(i + 1, st0, st1);
+    }
+    if (i < nblk) step(i, st1, st0);
+    if (m >= q || wblk == 0) return;
+    rsum += __shfl_xor(rsum, 16, 64);
+    rsum += __shfl_xor(rsum, 32, 64);
+    const float inv = 1.0f / rsum;
+    const size_t row = ((size_t)b * q + m) * a.ldo + (size_t)h * DH;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+        const int d = 16 * dt + 4 * g;
+        const f32x4_t acc = o[dt];
+        if (a.out_f32) {
+            float* po = reinterpret_cast<float*>(a.out) + row + d;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) po[r] = acc[r] * inv;
+        } else if constexpr (E == 2) {   // 4 bf16 in one 8-byte store
+            const uint2 pk = {f32x2_to_bf16x2(acc[0] * inv, acc[1] * inv), f32x2_to_bf16x2(acc[2] * inv, acc[3] * inv)};
+            *reinterpret_cast<uint2*>(reinterpret_cast<T*>(a.out) + row + d) = pk;
+        } else {
+            T* po = reinterpret_cast<T*>(a.out) + row + d;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) po[r] = to_elem<T>(acc[r] * inv);
+        }
+    }
+}
+
+hipError_t launch_attention_rows(int dtype, int head_dim, const AttnArgs& a, hipStream_t s, hipEvent_t ev0,
+                                 hipEvent_t ev1) {
+    if (a.q < 1 || a.q > 4096 || a.mask || a.B < 1 || a.H < 1 || a.S_max < 32 || a.S_max % 32 || a.ldo % 4 ||
+        !a.qbuf || !a.kc || !a.vc || !a.cache_len || !a.out || !a.err)
+        return hipErrorInvalidValue;
+    void (*kern)(AttnArgs) = nullptr;
+    if (dtype == 1) kern = head_dim == 128 ? attn_rows_kernel<uint16_t, 128> : head_dim == 64 ? attn_rows_kernel<uint16_t, 64> : nullptr;
+    else kern = head_dim == 128 ? attn_rows_kernel<float, 128> : head_dim == 64 ? attn_rows_kernel<float, 64> : nullptr;
+    if (!kern) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)(a.B * a.H * ((a.q + 63) / 64)));
+    if (ev0)
+        hipExtLaunchKernelGGL(kern, grid, dim3(64 * kRowWaves), 0, s, ev0, ev1, 0, a);
+    else
+        hipLaunchKernelGGL(kern, grid, dim3(64 * kRowWaves), 0, s, a);
+    return hipGetLastError();
+}
+
 template <typename T, int DH>
 static hipError_t launch_dh(const AttnPlan& p, const AttnArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     void (*kern)(AttnArgs) = attn_kernel<T, DH, 1>;

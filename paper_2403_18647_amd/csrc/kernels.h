@@ -120,6 +120,10 @@ size_t attention_counter_ints(int B_max, int H, int q_max);
 // ev0 / ev1 (optional): start and end of the attention kernel
 hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s,
                             hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+// Blocks of more than 16 rows with the chain mask (mask NULL): 64-row tiles, the key blocks staged in LDS;
+// plan, splits, per_split, cols, part and counter are not used
+hipError_t launch_attention_rows(int dtype, int head_dim, const AttnArgs& a, hipStream_t s,
+                                 hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 // ---------------------------------------------------------------- misc kernels
 hipError_t launch_embed(int dtype, const void* embed, int n_rows_emb, int d, const int* tokens, int M,
