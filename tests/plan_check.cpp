@@ -12,8 +12,14 @@
 //     up to 64 rows.
 //  4. Skinny GEMMs: the contraction slices (waves x workgroups per tile) do not depend on the rows
 //     M, for M = 1..64, so a row's value is the same in any block.
+//  5. The prefill launches refuse, before any device call, arguments their kernels do not handle:
+//     fused epilogues with a split contraction, heads other than 64 / 128 columns, segments that are
+//     not whole heads, rows not whole sequences, caches not in 32-key blocks, missing buffers; the
+//     prefill attention with a tree mask or a head width it has no instance for.  Only invalid
+//     argument sets are passed (a valid one would launch).
 #include <algorithm>
 #include <cstdio>
+#include <vector>
 
 #include "kernels.h"
 
@@ -86,6 +92,66 @@ int main() {
                           (size_t)g.n_tiles * p.waves * p.ksplit * p.mt * 64 * 16, part);
             }
         }
+    }
+    // 5. launch-argument checks (each set below is invalid in exactly the way its label says)
+    {
+        int dummy[64];
+        void* ptr = dummy;
+        auto qkv = [&]() {
+            PrefillGemmArgs p{};
+            p.M = 140; p.N = 3 * 256; p.K = 256; p.A = ptr; p.lda = 256; p.W0 = p.W1 = p.W2 = ptr; p.n_per = 256;
+            p.ksplit = 1; p.ep = PG_QKV; p.q = 70; p.H = 2; p.Dh = 128; p.S_max = 512;
+            p.cache_len = dummy; p.rope = reinterpret_cast<const float*>(ptr); p.qbuf = reinterpret_cast<float*>(ptr);
+            p.kc = p.vc = ptr; p.err = dummy;
+            return p;
+        };
+        auto swiglu = [&]() {
+            PrefillGemmArgs p{};
+            p.M = 140; p.N = 2 * 688; p.K = 256; p.A = ptr; p.lda = 256; p.W0 = p.W1 = ptr; p.n_per = 688;
+            p.ksplit = 1; p.ep = PG_SWIGLU; p.u = ptr; p.ldu = 688;
+            return p;
+        };
+        struct Bad { const char* what; PrefillGemmArgs p; };
+        std::vector<Bad> bad;
+        { auto p = qkv(); p.ksplit = 2; bad.push_back({"QKV epilogue with a split contraction", p}); }
+        { auto p = qkv(); p.Dh = 96; p.n_per = 192; p.N = 576; bad.push_back({"QKV heads of 96 columns", p}); }
+        { auto p = qkv(); p.H = 3; bad.push_back({"QKV segment not whole heads", p}); }
+        { auto p = qkv(); p.q = 69; bad.push_back({"QKV rows not whole sequences", p}); }
+        { auto p = qkv(); p.S_max = 500; bad.push_back({"QKV cache not in 32-key blocks", p}); }
+        { auto p = qkv(); p.qbuf = nullptr; bad.push_back({"QKV without a Q buffer", p}); }
+        { auto p = qkv(); p.vc = nullptr; bad.push_back({"QKV without a V cache", p}); }
+        { auto p = qkv(); p.N = 2 * 256; bad.push_back({"QKV with two segments", p}); }
+        { auto p = qkv(); p.K = 252; bad.push_back({"contraction not in 8-element chunks", p}); }
+        { auto p = qkv(); p.ep = 7; bad.push_back({"unknown epilogue", p}); }
+        { auto p = swiglu(); p.u = nullptr; bad.push_back({"SwiGLU without an output", p}); }
+        { auto p = swiglu(); p.ldu = 600; bad.push_back({"SwiGLU output rows too short", p}); }
+        { auto p = swiglu(); p.ksplit = 2; bad.push_back({"SwiGLU epilogue with a split contraction", p}); }
+        { auto p = swiglu(); p.N = 3 * 688; p.W2 = ptr; bad.push_back({"SwiGLU with three segments", p}); }
+        { auto p = swiglu(); p.ep = PG_STORE; bad.push_back({"plain store without C", p}); }
+        { auto p = swiglu(); p.ep = PG_STORE; p.C = reinterpret_cast<float*>(ptr); p.ldc = 100;
+          bad.push_back({"plain store with C rows too short", p}); }
+        for (const Bad& b : bad)
+            for (int dtype : {0, 1})
+                CHECK(launch_prefill_gemm(dtype, b.p, nullptr) == hipErrorInvalidValue, "prefill GEMM accepted: %s",
+                      b.what);
+        auto rows = [&]() {
+            AttnArgs a{};
+            a.qbuf = reinterpret_cast<const float*>(ptr); a.kc = a.vc = ptr; a.cache_len = dummy;
+            a.B = 2; a.q = 70; a.H = 2; a.S_max = 512; a.scale = 0.1f; a.out = ptr; a.ldo = 256; a.err = dummy;
+            return a;
+        };
+        struct BadA { const char* what; AttnArgs a; int head_dim; };
+        std::vector<BadA> bada;
+        { auto a = rows(); a.mask = reinterpret_cast<const uint64_t*>(ptr); bada.push_back({"prefill attention with a tree mask", a, 128}); }
+        { auto a = rows(); bada.push_back({"prefill attention, heads of 96 columns", a, 96}); }
+        { auto a = rows(); a.S_max = 500; bada.push_back({"prefill attention, cache not in 32-key blocks", a, 128}); }
+        { auto a = rows(); a.q = 0; bada.push_back({"prefill attention without rows", a, 128}); }
+        { auto a = rows(); a.ldo = 258; bada.push_back({"prefill attention, output stride not in 4s", a, 128}); }
+        { auto a = rows(); a.out = nullptr; bada.push_back({"prefill attention without an output", a, 128}); }
+        for (const BadA& b : bada)
+            for (int dtype : {0, 1})
+                CHECK(launch_attention_rows(dtype, b.head_dim, b.a, nullptr) == hipErrorInvalidValue,
+                      "prefill attention accepted: %s", b.what);
     }
     std::printf("%s (%d failed)\n", failures ? "FAILED" : "ok", failures);
     return failures ? 1 : 0;

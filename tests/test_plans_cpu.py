@@ -1,7 +1,8 @@
 """Host-side checks of the library's launch plans (tests/plan_check.cpp): workspace sizing of the
 attention split partials and residual-GEMM partial tiles for every plan a call can make, and the
 plan properties block-size invariance rests on (a fixed key partition and fixed contraction slices
-whatever the block rows).  Compiled with the host compiler against the built library; no device."""
+whatever the block rows), and the prefill launches' refusal of arguments their kernels do not
+handle.  Compiled with the host compiler against the built library; no device."""
 import os
 import shutil
 import subprocess
