@@ -482,28 +482,39 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnArgs a) {
 }
 
 // Blocks of many rows with the chain mask (prefill chunks): one workgroup of
-// kRowWaves waves per (sequence, head, 64-row tile).  Wave w owns rows
-// 16w .. 16w + 15 of the tile and runs the per-block step above over every key
-// block its rows can see, so the waves need no merge.  A 32-key block's K rows
-// and V's key-permuted columns are contiguous runs of the cache; the workgroup
-// stages them in LDS (rows padded by 32 bytes, two buffers, the next block's
-// loads in flight in registers while the current one is used), so the tile
-// reads each block once instead of once per wave.
-static constexpr int kRowWaves = 4;
+// 8 waves per (sequence, head, 64-row tile).  The waves come in pairs per 16
+// rows: wave (r, kp) owns rows 16r .. 16r + 15 of the tile and the key blocks
+// of parity kp, and runs the per-block step above over those its rows can see;
+// at the end each pair merges its two partial results by log-sum-exp through
+// LDS (parity 0 first).  A 32-key block's K rows and V's key-permuted columns
+// are contiguous runs of the cache; the workgroup stages two blocks per step in
+// LDS (rows padded by 32 bytes, two buffers, two register sets of loads so the
+// blocks of step i + 2 are requested while step i's are used), so a block is
+// read from L2 once per tile rather than once per wave.
+static constexpr int kRowSub = 4;                 // 16-row subtiles per workgroup
+static constexpr int kRowWaves = 2 * kRowSub;     // two key parities per subtile
 template <typename T, int DH>
 __global__ void __launch_bounds__(64 * kRowWaves) attn_rows_kernel(AttnArgs a) {
     constexpr int NDS = DH / 32, NDT = DH / 16, E = (int)sizeof(T);
     constexpr int KLD = DH + 32 / E, VLD = 32 + 32 / E;   // staged row strides (elements)
     constexpr int CH = 16 / E;                              // elements per 16-byte chunk
-    constexpr int NCH = 32 * DH / CH;                       // chunks per staged operand
-    constexpr int NT = 64 * kRowWaves, PER = NCH / NT;
-    static_assert(PER * NT == NCH, "whole chunks per thread");
+    constexpr int NCH = 32 * DH / CH;                       // chunks per staged operand of one block
+    constexpr int NT = 64 * kRowWaves, PER = 2 * NCH / NT;  // two blocks per step
+    static_assert(PER * NT == 2 * NCH, "whole chunks per thread");
     constexpr int NQF = (E == 2 ? 2 : 1) * NDS;              // Q fragments per lane (hi, and lo for bf16)
-    __shared__ __align__(16) T s_k[2][32 * KLD];
-    __shared__ __align__(16) T s_v[2][DH * VLD];
-    __shared__ Frag<T> s_qf[kRowWaves][NQF * 64];
+    constexpr int KBLK = 32 * KLD, VBLK = DH * VLD;
+    // [buffer][block of the step] K and V tiles; after the last step, the parity-1 partials for the merge
+    constexpr int STAGE_BYTES = 2 * 2 * (KBLK + VBLK) * E;
+    constexpr int MERGE_BYTES = kRowSub * (NDT * 64 * 16 + 2 * 64 * 4);
+    static_assert(MERGE_BYTES <= STAGE_BYTES, "merge buffer fits the stage buffers");
+    __shared__ __align__(16) unsigned char smem[STAGE_BYTES];
+    __shared__ Frag<T> s_qf[kRowSub][NQF * 64];
+    T* s_stage = reinterpret_cast<T*>(smem);
+    auto s_k = [&](int buf, int j) { return s_stage + (buf * 2 + j) * (KBLK + VBLK); };
+    auto s_v = [&](int buf, int j) { return s_stage + (buf * 2 + j) * (KBLK + VBLK) + KBLK; };
 
     const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int rs = wave % kRowSub, kp = wave / kRowSub;
     const int c = lane & 15, g = lane >> 4;
     const int q = a.q, n_rt = (q + 63) / 64;
     const int rt = (int)blockIdx.x % n_rt, bh = (int)blockIdx.x / n_rt;
@@ -515,12 +526,14 @@ __global__ void __launch_bounds__(64 * kRowWaves) attn_rows_kernel(AttnArgs a) {
     }
     const T* kbase = reinterpret_cast<const T*>(a.kc) + ((size_t)b * a.H + h) * a.S_max * DH;
     const T* vbase = reinterpret_cast<const T*>(a.vc) + ((size_t)b * a.H + h) * a.S_max * DH;
-    const int r0 = 64 * rt, w0 = r0 + 16 * wave, m = w0 + c;
+    const int r0 = 64 * rt, w0 = r0 + 16 * rs, m = w0 + c;
     const int nblk = (L + min(r0 + 63, q - 1) + 32) / 32;                 // the tile's last row
-    const int wblk = w0 < q ? (L + min(w0 + 15, q - 1) + 32) / 32 : 0;     // this wave's last row
+    const int wblk = w0 < q ? (L + min(w0 + 15, q - 1) + 32) / 32 : 0;     // this subtile's last row
+    const int nstep = (nblk + 1) / 2;
 
-    // the wave's Q rows as matrix-core fragments (hi / lo) in its LDS region; rows past q read row q - 1
-    {
+    // the subtile's Q rows as matrix-core fragments (hi / lo) in LDS, written by its parity-0 wave;
+    // rows past q read row q - 1
+    if (kp == 0) {
         const f32x4_t* qsrc =
             reinterpret_cast<const f32x4_t*>(a.qbuf + (((size_t)b * q + min(m, q - 1)) * a.H + h) * DH + 8 * g);
 #pragma unroll
@@ -529,31 +542,31 @@ __global__ void __launch_bounds__(64 * kRowWaves) attn_rows_kernel(AttnArgs a) {
             const float x8[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
             Frag<T> fh, fl;
             split_frag<T>(x8, fh, fl);
-            s_qf[wave][ds * 64 + lane] = fh;
-            if constexpr (E == 2) s_qf[wave][(NDS + ds) * 64 + lane] = fl;
+            s_qf[rs][ds * 64 + lane] = fh;
+            if constexpr (E == 2) s_qf[rs][(NDS + ds) * 64 + lane] = fl;
         }
     }
-    // Two register sets of staged loads: while block i is used from LDS, block i + 1 (requested one
-    // step earlier) is on its way to the other LDS buffer and block i + 2 is requested.  Block indices
-    // are clamped (a repeated last block is staged, never used), and the steps run in unconditional
-    // pairs, so the wait before each LDS write counts only the older set's loads.
+    // Two register sets: while step i's blocks are used from LDS, step i + 1's (requested one step
+    // earlier) go to the other buffer and step i + 2's are requested.  Block indices are clamped (a
+    // repeated last block is staged, never used), and the steps run in unconditional pairs, so the
+    // wait before each LDS write counts only the older set's loads.
     struct Stage { u32x4_t k[PER], v[PER]; };
     Stage st0, st1;
-    auto gload = [&](Stage& r, int blk) {
-        const u32x4_t* ks = reinterpret_cast<const u32x4_t*>(kbase + (size_t)min(blk, nblk - 1) * 32 * DH);
-        const u32x4_t* vs = reinterpret_cast<const u32x4_t*>(vbase + (size_t)min(blk, nblk - 1) * 32 * DH);
+    auto gload = [&](Stage& r, int step) {
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
-            r.k[i] = ks[tid + NT * i];
-            r.v[i] = vs[tid + NT * i];
+            const int ch = tid + NT * i, j = ch / NCH, cc = ch % NCH;
+            const size_t off = (size_t)min(2 * step + j, nblk - 1) * 32 * DH;
+            r.k[i] = reinterpret_cast<const u32x4_t*>(kbase + off)[cc];
+            r.v[i] = reinterpret_cast<const u32x4_t*>(vbase + off)[cc];
         }
     };
     auto lstore = [&](const Stage& r, int buf) {
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
-            const int ch = tid + NT * i;
-            *reinterpret_cast<u32x4_t*>(&s_k[buf][(ch / (DH / CH)) * KLD + (ch % (DH / CH)) * CH]) = r.k[i];
-            *reinterpret_cast<u32x4_t*>(&s_v[buf][(ch / (32 / CH)) * VLD + (ch % (32 / CH)) * CH]) = r.v[i];
+            const int ch = tid + NT * i, j = ch / NCH, cc = ch % NCH;
+            *reinterpret_cast<u32x4_t*>(s_k(buf, j) + (cc / (DH / CH)) * KLD + (cc % (DH / CH)) * CH) = r.k[i];
+            *reinterpret_cast<u32x4_t*>(s_v(buf, j) + (cc / (32 / CH)) * VLD + (cc % (32 / CH)) * CH) = r.v[i];
         }
     };
     gload(st0, 0);
@@ -566,19 +579,21 @@ __global__ void __launch_bounds__(64 * kRowWaves) attn_rows_kernel(AttnArgs a) {
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     const int Tb = L + q;
-    // block i from LDS buffer i & 1; `next` holds block i + 1, `free` takes block i + 2
+    // step i from LDS buffer i & 1 (this wave: block 2i + kp); `next` holds step i + 1, `free` takes i + 2
     auto step = [&](int i, const Stage& next, Stage& free) {
-        const int buf = i & 1;
+        const int buf = i & 1, blk = 2 * i + kp;
         gload(free, i + 2);
-        if (i < wblk) {
+        if (blk < wblk) {
+            const T* sk = s_k(buf, kp);
+            const T* sv = s_v(buf, kp);
             Frag<T> kf[2][NDS], vf[NDT];
 #pragma unroll
             for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-                for (int ds = 0; ds < NDS; ++ds) kf[kt][ds] = Frag<T>::load(&s_k[buf][(16 * kt + c) * KLD + ds * 32 + 8 * g]);
+                for (int ds = 0; ds < NDS; ++ds) kf[kt][ds] = Frag<T>::load(sk + (16 * kt + c) * KLD + ds * 32 + 8 * g);
 #pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) vf[dt] = Frag<T>::load(&s_v[buf][(16 * dt + c) * VLD + 8 * g]);
-            attend_block<T, NDS, NDT>(kf, vf, s_qf[wave], lane, 0ull, i, m, L, Tb, q, false, a.scale, g, rmax, rsum, o);
+            for (int dt = 0; dt < NDT; ++dt) vf[dt] = Frag<T>::load(sv + (16 * dt + c) * VLD + 8 * g);
+            attend_block<T, NDS, NDT>(kf, vf, s_qf[rs], lane, 0ull, blk, m, L, Tb, q, false, a.scale, g, rmax, rsum, o);
         }
         __builtin_amdgcn_sched_barrier(0);
         // the other buffer was last read in step i - 1, before the barrier that ended it
@@ -586,20 +601,35 @@ __global__ void __launch_bounds__(64 * kRowWaves) attn_rows_kernel(AttnArgs a) {
         __syncthreads();
     };
     int i = 0;
-    for (; i + 1 < nblk; i += 2) {
+    for (; i + 1 < nstep; i += 2) {
         step(i, st1, st0);
         step(i + 1, st0, st1);
     }
-    if (i < nblk) step(i, st1, st0);
-    if (m >= q || wblk == 0) return;
+    if (i < nstep) step(i, st1, st0);
+
+    // merge the two key parities of each subtile: parity 1 leaves its partial in LDS (the stage
+    // buffers are free after the last step's barrier), parity 0 combines and writes
     rsum += __shfl_xor(rsum, 16, 64);
     rsum += __shfl_xor(rsum, 32, 64);
-    const float inv = 1.0f / rsum;
+    f32x4_t* m_o = reinterpret_cast<f32x4_t*>(smem) + rs * NDT * 64;
+    float* m_s = reinterpret_cast<float*>(smem + kRowSub * NDT * 64 * 16) + rs * 128;
+    if (kp == 1) {
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) m_o[dt * 64 + lane] = o[dt];
+        m_s[lane] = rmax;
+        m_s[64 + lane] = rsum;
+    }
+    __syncthreads();
+    if (kp == 1 || m >= q || wblk == 0) return;
+    const float m1 = m_s[lane], s1 = m_s[64 + lane];
+    const float gmax = fmaxf(rmax, m1);
+    const float a0 = rmax == -INFINITY ? 0.f : expf(rmax - gmax), a1 = m1 == -INFINITY ? 0.f : expf(m1 - gmax);
+    const float inv = 1.0f / (a0 * rsum + a1 * s1);
     const size_t row = ((size_t)b * q + m) * a.ldo + (size_t)h * DH;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) {
         const int d = 16 * dt + 4 * g;
-        const f32x4_t acc = o[dt];
+        const f32x4_t acc = o[dt] * a0 + m_o[dt * 64 + lane] * a1;
         if (a.out_f32) {
             float* po = reinterpret_cast<float*>(a.out) + row + d;
 #pragma unroll
@@ -621,8 +651,9 @@ hipError_t launch_attention_rows(int dtype, int head_dim, const AttnArgs& a, hip
         !a.qbuf || !a.kc || !a.vc || !a.cache_len || !a.out || !a.err)
         return hipErrorInvalidValue;
     void (*kern)(AttnArgs) = nullptr;
+    // float models with 128-wide heads would need more LDS than a workgroup has: attn_kernel serves them
     if (dtype == 1) kern = head_dim == 128 ? attn_rows_kernel<uint16_t, 128> : head_dim == 64 ? attn_rows_kernel<uint16_t, 64> : nullptr;
-    else kern = head_dim == 128 ? attn_rows_kernel<float, 128> : head_dim == 64 ? attn_rows_kernel<float, 64> : nullptr;
+    else kern = head_dim == 64 ? attn_rows_kernel<float, 64> : nullptr;
     if (!kern) return hipErrorInvalidValue;
     const dim3 grid((unsigned)(a.B * a.H * ((a.q + 63) / 64)));
     if (ev0)

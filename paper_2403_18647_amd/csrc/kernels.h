@@ -121,7 +121,9 @@ size_t attention_counter_ints(int B_max, int H, int q_max);
 hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s,
                             hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // Blocks of more than 16 rows with the chain mask (mask NULL): 64-row tiles, the key blocks staged in LDS;
-// plan, splits, per_split, cols, part and counter are not used
+// plan, splits, per_split, cols, part and counter are not used.  bf16 with heads of 64 or 128 columns,
+// float with 64 (attention_rows_supported)
+inline bool attention_rows_supported(int dtype, int head_dim) { return head_dim == 64 || (dtype == 1 && head_dim == 128); }
 hipError_t launch_attention_rows(int dtype, int head_dim, const AttnArgs& a, hipStream_t s,
                                  hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 

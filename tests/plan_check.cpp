@@ -144,6 +144,11 @@ int main() {
         std::vector<BadA> bada;
         { auto a = rows(); a.mask = reinterpret_cast<const uint64_t*>(ptr); bada.push_back({"prefill attention with a tree mask", a, 128}); }
         { auto a = rows(); bada.push_back({"prefill attention, heads of 96 columns", a, 96}); }
+        {
+            auto a = rows();
+            CHECK(launch_attention_rows(0, 128, a, nullptr) == hipErrorInvalidValue && !attention_rows_supported(0, 128),
+                  "prefill attention accepted float heads of 128 columns");
+        }
         { auto a = rows(); a.S_max = 500; bada.push_back({"prefill attention, cache not in 32-key blocks", a, 128}); }
         { auto a = rows(); a.q = 0; bada.push_back({"prefill attention without rows", a, 128}); }
         { auto a = rows(); a.ldo = 258; bada.push_back({"prefill attention, output stride not in 4s", a, 128}); }
