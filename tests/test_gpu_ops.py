@@ -109,6 +109,16 @@ def test_attention_bf16_head128(lens, q):
     _attn_case(helpers.small_bf16(), lens, q)
 
 
+@pytest.mark.parametrize("dtype,lens,q", [("bf16", [0, 37], 200), ("bf16", [129], 511), ("bf16", [1000, 0, 64], 70),
+                                          ("fp32", [0], 130), ("fp32", [70, 3], 97)])
+def test_attention_prefill_rows(dtype, lens, q):
+    """Blocks of more than 16 rows (the prefill attention: 64-row tiles, two waves per 16 rows on
+    alternate key blocks, merged at the end): several tiles, a ragged last tile, cache prefixes of
+    0 to 1000 keys, a batch with different lengths; every element against the oracle's attention."""
+    print(f"attention prefill rows {dtype} lens={lens} q={q}", flush=True)
+    _attn_case(helpers.small_bf16() if dtype == "bf16" else synth.workload("tiny"), lens, q)
+
+
 def test_attention_tree_mask():
     # row 0 root, rows 1,2 children of 0, row 3 child of 2, row 4 child of 1
     par = [-1, 0, 0, 2, 1]
