@@ -219,7 +219,7 @@ void carve(sdsat_ctx* c, Carver& cv) {
     c->tree_mask = (uint64_t*)cv.take(bq * 8);
     c->logits = (float*)cv.take(bq * D.V * 4);
     c->hbuf = cv.take((size_t)D.maxM * D.d_pad * e);
-    if (D.maxM > kSkinnyRows) c->c_y = (float*)cv.take((size_t)D.maxM * D.d * 4 * 2);   // two split-K halves
+    if (D.maxM > kSkinnyRows) c->c_y = (float*)cv.take((size_t)D.maxM * D.d * 4 * kPrefillMaxSplit);   // split-K parts
 }
 
 void* layer_k(sdsat_ctx* c, int l) { return (char*)c->kc + (size_t)l * c->layer_elems * c->D.esz; }
@@ -337,16 +337,17 @@ int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask,
 // C[M][N] (row stride ldc, float) = A[M][K] (row stride lda) . W[N][K]^T, A and W in the model's element
 // type, W the caller's row-major [out, in] weights (up to three of n_per rows each, stacked along N): the
 // matrix-core GEMM of large blocks.
-// With c_part > 0 (the offset of a second output) a GEMM with fewer than 256 tiles and a long contraction
-// is split in two halves; *split tells the caller to add them.
+// With c_part > 0 (the offset between partial outputs, room for kPrefillMaxSplit of them) a GEMM with
+// fewer than 256 tiles and a long contraction is split (prefill_gemm_ksplit); *parts tells the caller how
+// many partials to add.
 int big_gemm(sdsat_ctx* c, int M, int N, int K, const void* A, int lda, const void* W0, const void* W1,
-             const void* W2, int n_per, float* C, int ldc, size_t c_part = 0, bool* split = nullptr) {
+             const void* W2, int n_per, float* C, int ldc, size_t c_part = 0, int* parts = nullptr) {
     PrefillGemmArgs p{};
     p.M = M; p.N = N; p.K = K; p.A = A; p.lda = lda; p.W0 = W0; p.W1 = W1; p.W2 = W2; p.n_per = n_per;
     p.C = C; p.ldc = ldc;
     p.ksplit = c_part ? prefill_gemm_ksplit(M, N, K) : 1;
     p.c_part = c_part;
-    if (split) *split = p.ksplit > 1;
+    if (parts) *parts = p.ksplit;
     HIPCHK(c, launch_prefill_gemm(c->D.dtype, p, c->stream));
     return SDSAT_OK;
 }
@@ -393,17 +394,17 @@ int large_block_impl(sdsat_ctx* c, int B, int q, const int32_t* tokens, float* l
         if (rc) return rc;
         rc = attention_layer(c, l, B, q, nullptr, (const float*)c->qbuf, c->obuf, 0, D.d_pad);
         if (rc) return rc;
-        const size_t y_part = (size_t)D.maxM * D.d;   // offset of the second split-K half in c_y
-        bool split = false;
-        rc = big_gemm(c, M, D.d, D.d, c->obuf, D.d_pad, w[4], nullptr, nullptr, D.d, c->c_y, D.d, y_part, &split);
+        const size_t y_part = (size_t)D.maxM * D.d;   // offset between split-K partials in c_y
+        int parts = 1;
+        rc = big_gemm(c, M, D.d, D.d, c->obuf, D.d_pad, w[4], nullptr, nullptr, D.d, c->c_y, D.d, y_part, &parts);
         if (rc) return rc;
-        HIPCHK(c, launch_resid_norm_rows(D.dtype, c->c_y, split ? c->c_y + y_part : nullptr, D.d, M, D.d, c->x, D.d,
-                                         c->ffn_norm[l], eps, c->hbuf, D.d_pad, c->stream));
+        HIPCHK(c, launch_resid_norm_rows(D.dtype, c->c_y, parts, y_part, D.d, M, D.d, c->x, D.d, c->ffn_norm[l], eps,
+                                         c->hbuf, D.d_pad, c->stream));
         rc = big_gemm_swiglu(c, M, c->hbuf, w[6], w[7]);
         if (rc) return rc;
-        rc = big_gemm(c, M, D.d, D.F, c->ubuf, D.F_pad, w[8], nullptr, nullptr, D.d, c->c_y, D.d, y_part, &split);
+        rc = big_gemm(c, M, D.d, D.F, c->ubuf, D.F_pad, w[8], nullptr, nullptr, D.d, c->c_y, D.d, y_part, &parts);
         if (rc) return rc;
-        HIPCHK(c, launch_resid_norm_rows(D.dtype, c->c_y, split ? c->c_y + y_part : nullptr, D.d, M, D.d, c->x, D.d,
+        HIPCHK(c, launch_resid_norm_rows(D.dtype, c->c_y, parts, y_part, D.d, M, D.d, c->x, D.d,
                                          l + 1 < D.L ? c->attn_norm[l + 1] : c->final_norm, eps, c->hbuf, D.d_pad,
                                          c->stream));
     }

@@ -150,8 +150,8 @@ hipError_t launch_rope_table(const double* inv_freq, int S, int half, float* rop
 // C[M][ldc] (float) = A[M][lda] (element type) . W[N][K]^T on the matrix cores, W = up to three
 // row-major [n_per, K] matrices stacked along N (W0 rows 0..n_per-1, W1 the next n_per, ...).
 // K must be a multiple of 8 (16-byte loads); rows of A past K read as zero only up to K.
-// With ksplit 2 (prefill_gemm_ksplit) the contraction is split in two halves whose partial products go
-// to C and C + c_part; the consumer adds them (partial 0 + partial 1).
+// With ksplit > 1 (prefill_gemm_ksplit, at most kPrefillMaxSplit) the contraction is split into parts of
+// whole stages whose partial products go to C + part * c_part; the consumer adds them in part order.
 // Epilogues of the prefill GEMM: PG_STORE writes C (float); PG_QKV takes N = 3 n_per columns Q | K | V
 // (heads of Dh columns), applies RoPE at cache_len[b] + row and writes Q (float) to qbuf [M][H][Dh],
 // K and V in the element type into the cache (K [B][H][S_max][Dh], V key-permuted [B][H][S_max/32][Dh][32]);
@@ -170,16 +170,18 @@ struct PrefillGemmArgs {
     // PG_SWIGLU
     void* u; int ldu;
 };
+constexpr int kPrefillMaxSplit = 4;
 int prefill_gemm_ksplit(int M, int N, int K);
 hipError_t launch_prefill_gemm(int dtype, const PrefillGemmArgs& p, hipStream_t s);
 // Row-wise steps around the prefill GEMMs of blocks of more than 64 rows.
 // h = elem(xg / rms) with rms from the row's per-16-column sums of squares
 hipError_t launch_rms_rows(int dtype, const float* xg, int ldxg, const float* ssq, int n_ssq, int K, float eps, int M,
                            void* h, int ldh, hipStream_t s);
-// x += y (y = y0 + y1 when y1 is given: two split-K partials); h = elem((x o g) / rms(x)), bitwise what
-// the residual epilogue's per-16-column sums of squares and rms_rows give (rows of up to 8192 columns)
-hipError_t launch_resid_norm_rows(int dtype, const float* y, const float* y1, int ldy, int M, int N, float* x,
-                                  int ldx, const float* g, float eps, void* h, int ldh, hipStream_t s);
+// x += y with y = ((y_0 + y_1) + y_2) + ..., the parts of a split contraction (parts >= 1, part p at
+// y + p * part_stride); h = elem((x o g) / rms(x)), bitwise what the residual epilogue's per-16-column
+// sums of squares and rms_rows give (rows of up to 8192 columns)
+hipError_t launch_resid_norm_rows(int dtype, const float* y, int parts, size_t part_stride, int ldy, int M, int N,
+                                  float* x, int ldx, const float* g, float eps, void* h, int ldh, hipStream_t s);
 
 // ---------------------------------------------------------------- verify
 hipError_t launch_verify_greedy(const float* logits, int B, int q, int V, const int* drafts, int drafts_ld,

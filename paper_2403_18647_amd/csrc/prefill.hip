@@ -49,7 +49,7 @@ __global__ void __launch_bounds__(256) rms_rows_kernel(const float* xg, int ldxg
 }
 
 // The residual add and the next RMSNorm of a large block in one pass over each
-// row: x[m] += y[m] (+ y1[m], the second half of a split contraction), then
+// row: x[m] += y[m] (the sum of a split contraction's parts, in part order), then
 // h[m] = elem((x[m] o g) / rms_m).  One workgroup per row; each thread keeps
 // its columns' x o g in registers.  The sums of squares are formed per 16-column
 // group in the decode residual epilogue's butterfly and reduced in rms_rows'
@@ -58,9 +58,9 @@ __global__ void __launch_bounds__(256) rms_rows_kernel(const float* xg, int ldxg
 static constexpr int kNormRowThreads = 1024;
 static constexpr int kNormRowMaxPer = 8;   // columns per thread: rows of up to 8192
 template <typename T>
-__global__ void __launch_bounds__(kNormRowThreads) resid_norm_rows_kernel(const float* y, const float* y1, int ldy,
-                                                                          int N, float* x, int ldx, const float* g,
-                                                                          float eps, T* h, int ldh) {
+__global__ void __launch_bounds__(kNormRowThreads) resid_norm_rows_kernel(const float* y, int parts, size_t part_stride,
+                                                                          int ldy, int N, float* x, int ldx,
+                                                                          const float* g, float eps, T* h, int ldh) {
     constexpr int NT = kNormRowThreads, P = kNormRowMaxPer;
     __shared__ float s_ssq[P * NT / 16];
     __shared__ float s_inv;
@@ -73,7 +73,14 @@ __global__ void __launch_bounds__(kNormRowThreads) resid_norm_rows_kernel(const 
         const int n = min(c * NT + t, N - 1);
         yv[c] = xv[c] = gv[c] = 0.f;
         if (c < nch) {
-            yv[c] = y1 ? y[(size_t)m * ldy + n] + y1[(size_t)m * ldy + n] : y[(size_t)m * ldy + n];
+            float pv[kPrefillMaxSplit];
+#pragma unroll
+            for (int q = 0; q < kPrefillMaxSplit; ++q)
+                pv[q] = q < parts ? y[q * part_stride + (size_t)m * ldy + n] : 0.f;
+            yv[c] = pv[0];
+#pragma unroll
+            for (int q = 1; q < kPrefillMaxSplit; ++q)
+                if (q < parts) yv[c] += pv[q];
             xv[c] = x[(size_t)m * ldx + n];
             gv[c] = g[n];
         }
@@ -127,16 +134,16 @@ hipError_t launch_rms_rows(int dtype, const float* xg, int ldxg, const float* ss
     return hipGetLastError();
 }
 
-hipError_t launch_resid_norm_rows(int dtype, const float* y, const float* y1, int ldy, int M, int N, float* x,
-                                  int ldx, const float* g, float eps, void* h, int ldh, hipStream_t s) {
+hipError_t launch_resid_norm_rows(int dtype, const float* y, int parts, size_t part_stride, int ldy, int M, int N,
+                                  float* x, int ldx, const float* g, float eps, void* h, int ldh, hipStream_t s) {
     if (M < 1) return hipSuccess;
-    if (N < 1 || N > kNormRowMaxPer * kNormRowThreads) return hipErrorInvalidValue;
+    if (N < 1 || N > kNormRowMaxPer * kNormRowThreads || parts < 1 || parts > kPrefillMaxSplit) return hipErrorInvalidValue;
     if (dtype == 1)
-        hipLaunchKernelGGL(resid_norm_rows_kernel<uint16_t>, dim3(M), dim3(kNormRowThreads), 0, s, y, y1, ldy, N, x,
-                           ldx, g, eps, static_cast<uint16_t*>(h), ldh);
+        hipLaunchKernelGGL(resid_norm_rows_kernel<uint16_t>, dim3(M), dim3(kNormRowThreads), 0, s, y, parts,
+                           part_stride, ldy, N, x, ldx, g, eps, static_cast<uint16_t*>(h), ldh);
     else
-        hipLaunchKernelGGL(resid_norm_rows_kernel<float>, dim3(M), dim3(kNormRowThreads), 0, s, y, y1, ldy, N, x, ldx,
-                           g, eps, static_cast<float*>(h), ldh);
+        hipLaunchKernelGGL(resid_norm_rows_kernel<float>, dim3(M), dim3(kNormRowThreads), 0, s, y, parts, part_stride,
+                           ldy, N, x, ldx, g, eps, static_cast<float*>(h), ldh);
     return hipGetLastError();
 }
 

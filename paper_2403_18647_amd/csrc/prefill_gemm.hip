@@ -316,17 +316,19 @@ hipError_t go(const PrefillGemmArgs& p, hipStream_t s) {
 
 int prefill_gemm_ksplit(int M, int N, int K) {
     const long tiles = (long)((M + 127) / 128) * ((N + 127) / 128);
-    return tiles < 256 && K >= 1024 ? 2 : 1;
+    if (K < 1024 || tiles >= 256) return 1;
+    return tiles <= 128 && K >= 2048 ? 4 : 2;
 }
 
 // 128 x 128 tiles (bf16: 8 waves of 32 x 64, float: 4 waves of 64 x 64, 32-wide
-// stages).  prefill_gemm_ksplit: a GEMM whose tiles make less than
-// one round of workgroups over the 256 compute units and whose contraction is
-// long is better split in two (O and down at 7B: 128 -> 256 workgroups), where
-// the caller can add the partials.
+// stages).  prefill_gemm_ksplit: a GEMM whose tiles make less than one round of
+// workgroups over the 256 compute units and whose contraction is long is split
+// into parts whose partials the caller adds; up to two workgroups of 80 KB of LDS
+// fit a compute unit, so a split fills both (O and down at 7B, 511 rows: 128
+// tiles, 4 parts, 512 workgroups).
 hipError_t launch_prefill_gemm(int dtype, const PrefillGemmArgs& p, hipStream_t s) {
     if (p.M < 1 || p.N < 1 || p.K < 1 || p.K % 8 || p.n_per < 1 || p.N > 3 * p.n_per || !p.A || !p.W0 ||
-        (p.N > p.n_per && !p.W1) || (p.N > 2 * p.n_per && !p.W2) || p.lda < p.K || p.ksplit < 1 || p.ksplit > 2)
+        (p.N > p.n_per && !p.W1) || (p.N > 2 * p.n_per && !p.W2) || p.lda < p.K || p.ksplit < 1 || p.ksplit > kPrefillMaxSplit)
         return hipErrorInvalidValue;
     if (p.ep == PG_STORE) {
         if (!p.C || p.ldc < p.N || (p.ksplit > 1 && p.c_part < (size_t)p.M * p.ldc)) return hipErrorInvalidValue;

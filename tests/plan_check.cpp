@@ -130,10 +130,29 @@ int main() {
         { auto p = swiglu(); p.ep = PG_STORE; bad.push_back({"plain store without C", p}); }
         { auto p = swiglu(); p.ep = PG_STORE; p.C = reinterpret_cast<float*>(ptr); p.ldc = 100;
           bad.push_back({"plain store with C rows too short", p}); }
+        { auto p = swiglu(); p.ep = PG_STORE; p.C = reinterpret_cast<float*>(ptr); p.ldc = p.N; p.ksplit = 5;
+          p.c_part = (size_t)p.M * p.ldc; bad.push_back({"split into more parts than the partial buffers hold", p}); }
+        { auto p = swiglu(); p.ep = PG_STORE; p.C = reinterpret_cast<float*>(ptr); p.ldc = p.N; p.ksplit = 4;
+          p.c_part = (size_t)p.M * p.ldc - 1; bad.push_back({"split partials that overlap", p}); }
         for (const Bad& b : bad)
             for (int dtype : {0, 1})
                 CHECK(launch_prefill_gemm(dtype, b.p, nullptr) == hipErrorInvalidValue, "prefill GEMM accepted: %s",
                       b.what);
+        // split plans: O and down of a 511-row 7B block fill two workgroups per compute unit; a block of
+        // 256 tiles or a short contraction stays whole; the partial buffers hold every plan
+        struct Split { int M, N, K, parts; };
+        for (const Split& t : {Split{511, 4096, 4096, 4}, Split{511, 4096, 11008, 4}, Split{140, 1024, 2752, 4},
+                               Split{140, 1024, 1024, 2}, Split{200, 4096, 1024, 2}, Split{1024, 4096, 11008, 1},
+                               Split{511, 4096, 1000, 1}, Split{2047, 5120, 13824, 1}, Split{140, 256, 688, 1}}) {
+            const int k = prefill_gemm_ksplit(t.M, t.N, t.K);
+            CHECK(k == t.parts && k >= 1 && k <= kPrefillMaxSplit, "prefill split of %d x %d x %d: %d parts, expected %d",
+                  t.M, t.N, t.K, k, t.parts);
+        }
+        for (int parts : {0, kPrefillMaxSplit + 1})
+            CHECK(launch_resid_norm_rows(1, reinterpret_cast<const float*>(ptr), parts, 0, 256, 4, 256,
+                                         reinterpret_cast<float*>(ptr), 256, reinterpret_cast<const float*>(ptr), 1e-5f,
+                                         ptr, 256, nullptr) == hipErrorInvalidValue,
+                  "residual row kernel accepted %d parts", parts);
         auto rows = [&]() {
             AttnArgs a{};
             a.qbuf = reinterpret_cast<const float*>(ptr); a.kc = a.vc = ptr; a.cache_len = dummy;

@@ -79,7 +79,7 @@ def test_block_rows_bitwise_equal_single_token_steps(dtype, k, prompt_len):
     ctx.close()
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("dtype", ["bf16", "fp32", "bf16_split"])
 def test_large_block_matches_oracle(dtype):
     """A block of more than 64 rows (the prompt-prefill path: matrix-core GEMMs on the caller's weights
     around row-wise kernels that round where the decode kernels round) matches the oracle's block
@@ -87,8 +87,14 @@ def test_large_block_matches_oracle(dtype):
     Batch 2 x 70 rows after a 40-token prefix prefilled in 16-row blocks: 140 GEMM rows (a partial
     128-row tile), a 688-wide FFN (a down contraction that ends inside a 64-wide stage, and a gate|up
     column tile that straddles the two stacked matrices) and a 1000-entry vocabulary (a partial
-    column tile)."""
-    if dtype == "bf16":
+    column tile).  bf16_split: one layer of width 1024 and FFN 2752, long enough contractions for the
+    residual GEMMs to be split over workgroups (O in 2 parts of 8 stages, down in 4 parts of 11, 11, 11
+    and 10 stages) and the parts added by the residual / RMSNorm row kernel."""
+    if dtype == "bf16_split":
+        shape = synth.small_shape(n_layers=1, d_model=1024, n_heads=8, head_dim=128, d_ffn=2752, vocab=1000,
+                                  n_adaptive=5, rope_base=1e6, dtype="bf16")
+        tol = 3e-2
+    elif dtype == "bf16":
         shape = synth.small_shape(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=688, vocab=1000,
                                   n_adaptive=5, rope_base=1e6, dtype="bf16")
         tol = 3e-2
@@ -98,7 +104,7 @@ def test_large_block_matches_oracle(dtype):
     Bn, P, q, q2 = 2, 40, 70, 6
     wl = synth.Workload("large", shape, seed=13, batch=Bn, k=q2 - 1, prompt_len=P, max_new=1, gain_std=0.1)
     W = helpers.oracle_weights(wl)
-    bf16 = dtype == "bf16"
+    bf16 = dtype != "fp32"
     prompts = synth.prompts(wl)
     rng = np.random.default_rng(5)
     toks = rng.integers(0, shape.vocab, (Bn, q)).astype(np.int32)
