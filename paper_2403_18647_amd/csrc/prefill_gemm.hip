@@ -40,7 +40,9 @@ namespace {
 // BK 128 (one workgroup per compute unit): 15.6 ms; 8 waves of 64 x 32: 14.1 ms; 4 waves of 64 x 64,
 // BK 32: 17.3 ms, BK 64: 18.8 ms; 16 waves of 32 x 32, BK 64: 14.7 ms; one register stage instead of
 // two: 14.9 ms.  Three register stages (at the register budget of two workgroups per compute unit,
-// with a small spill) measured slower than two: 13.6 against 12.8 ms in one run.
+// with a small spill) measured slower than two: 13.6 against 12.8 ms in one run.  With the fused
+// epilogues and the four-part O / down split: 8 waves of 32 x 64 11.2-11.6 ms; 8 waves of 64 x 64 in
+// 256 x 128 tiles 12.4-12.5 ms; 4 waves of 64 x 64 12.4 ms.
 template <typename T, int BK_> struct PTile {
     static constexpr int BK = BK_;
     static constexpr int EPC = 16 / sizeof(T);          // elements per 16-byte chunk
