@@ -52,11 +52,14 @@ static constexpr int kAttnWorkgroups = 256;
 // capacity, as many splits as fit one round of 256 workgroups per row tile),
 // and within a split block i goes to wave i mod waves.  Each 16-row tile of
 // the block has its own workgroups and reads only the key blocks its last row
-// can see.  A query row therefore sees the same keys in the same order of
+// can see.  A query row of a block of up to 16 rows (one row tile: every
+// decode block with k <= 15) therefore sees the same keys in the same order of
 // accumulation whatever the block size q and the cache length: blocks it
 // cannot see (later rows of its own block) add exact zeros.  So a token's
 // logits do not depend on how many draft rows share its block, and greedy
-// SDSAT reproduces autoregressive decoding bit for bit.  Waves per workgroup:
+// SDSAT reproduces autoregressive decoding bit for bit.  Blocks of several row
+// tiles take one split (and chain blocks of more than 16 rows the row kernel
+// below), whose order of accumulation differs.  Waves per workgroup:
 // one per block of the split, at most 8.  Column slices change which
 // workgroup writes a column of O, not how it is computed: each slice's values
 // are those of the single workgroup, bit for bit, so the slice count may
