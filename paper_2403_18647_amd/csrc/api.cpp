@@ -308,7 +308,7 @@ int fits(sdsat_ctx* c, int B, int q, bool* ok) {
 int attention_layer(sdsat_ctx* c, int layer, int B, int q, const uint64_t* mask, const float* qbuf, void* out,
                     int out_f32, int ldo) {
     const Dims& D = c->D;
-    if (!mask && q > 16 && attention_rows_supported(D.dtype, D.Dh)) {   // many rows: 64-row tiles, no key splits
+    if (!mask && q > kAttnSplitRows && attention_rows_supported(D.dtype, D.Dh)) {   // prefill: 64-row tiles
         AttnArgs a{};
         a.qbuf = qbuf; a.kc = layer_k(c, layer); a.vc = layer_v(c, layer); a.cache_len = c->cache_len;
         a.B = B; a.q = q; a.H = D.H; a.S_max = D.S; a.scale = (float)(1.0 / std::sqrt((double)D.Dh));

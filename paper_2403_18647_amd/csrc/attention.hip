@@ -52,14 +52,15 @@ static constexpr int kAttnWorkgroups = 256;
 // capacity, as many splits as fit one round of 256 workgroups per row tile),
 // and within a split block i goes to wave i mod waves.  Each 16-row tile of
 // the block has its own workgroups and reads only the key blocks its last row
-// can see.  A query row of a block of up to 16 rows (one row tile: every
-// decode block with k <= 15) therefore sees the same keys in the same order of
-// accumulation whatever the block size q and the cache length: blocks it
-// cannot see (later rows of its own block) add exact zeros.  So a token's
-// logits do not depend on how many draft rows share its block, and greedy
-// SDSAT reproduces autoregressive decoding bit for bit.  Blocks of several row
-// tiles take one split (and chain blocks of more than 16 rows the row kernel
-// below), whose order of accumulation differs.  Waves per workgroup:
+// can see.  A query row of a block of up to kAttnSplitRows rows (every decode
+// block) therefore sees the same keys in the same order of accumulation
+// whatever the block size q and the cache length: blocks it cannot see (later
+// rows of its own block) add exact zeros, and so do the partials of splits
+// that hold none of its keys.  So a token's logits do not depend on how many
+// draft rows share its block, and greedy SDSAT reproduces autoregressive
+// decoding bit for bit.  Longer blocks (prefill chunks) take one split (with
+// the chain mask, the row kernel below), whose order of accumulation differs.
+// Waves per workgroup:
 // one per block of the split, at most 8.  Column slices change which
 // workgroup writes a column of O, not how it is computed: each slice's values
 // are those of the single workgroup, bit for bit, so the slice count may
@@ -72,12 +73,11 @@ AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_ma
     // a full cache gives about kAttnWorkgroups workgroups per row tile; where that allows only two
     // splits, one split is planned (measured at batch 4 x 32 heads with a combine kernel: 26.4 ->
     // 23.6 us per layer)
-    // A block of several 16-row tiles (a prefill chunk) has workgroups enough across its row tiles and
-    // takes one split (the key partition only has to be the same for every decode block size, and a
-    // decode block is one row tile).
+    // A prefill chunk (more than kAttnSplitRows rows) has workgroups enough across its row tiles and
+    // takes one split: the key partition only has to be the same for every decode block size.
     p.row_tiles = (q + 15) / 16;
     int target = std::max(1, std::min(kMaxSplits, kAttnWorkgroups / pairs));
-    if (target <= 2 || p.row_tiles > 1) target = 1;
+    if (target <= 2 || q > kAttnSplitRows) target = 1;
     p.per_split = (cap + target - 1) / target;
     p.splits = (nblk + p.per_split - 1) / p.per_split;
     p.waves = std::max(1, std::min(p.per_split, kMaxWaves));
@@ -99,7 +99,7 @@ size_t attention_plan_partial_floats(const AttnPlan& p, int B, int H, int head_d
 size_t attention_partial_floats(int B_max, int H, int q_max, int head_dim, int S_max) {
     size_t most = 0;
     for (int b = 1; b <= B_max; ++b)
-        for (int q : {std::min(q_max, 16), q_max})
+        for (int q : {std::min(q_max, 16), std::min(q_max, kAttnSplitRows), q_max})
             most = std::max(most, attention_plan_partial_floats(plan_attention(b, H, q, head_dim, S_max, S_max), b, H,
                                                                 head_dim));
     return most;

@@ -112,6 +112,10 @@ struct AttnArgs {
 // `splits` x `cols` workgroups of `waves` waves per (sequence, head, 16-row tile); max_len: the
 // host's upper bound of the cache lengths; S_max: key slots per sequence
 struct AttnPlan { int waves, splits, per_split, row_tiles, grid, lds_bytes, cols; };
+// Blocks of up to this many rows per sequence (every decode block: M <= 64) keep the decode key
+// partition, so a row's logits do not depend on the block size; longer blocks (prefill chunks) take
+// one split, and with the chain mask the row kernel below.
+constexpr int kAttnSplitRows = 64;
 AttnPlan plan_attention(int B, int H, int q, int head_dim, int max_len, int S_max);
 // partial buffer and arrival counters a context needs for its largest blocks; what one plan needs
 size_t attention_partial_floats(int B_max, int H, int q_max, int head_dim, int S_max);
@@ -120,7 +124,7 @@ size_t attention_counter_ints(int B_max, int H, int q_max);
 // ev0 / ev1 (optional): start and end of the attention kernel
 hipError_t launch_attention(int dtype, int head_dim, const AttnPlan& p, const AttnArgs& a, hipStream_t s,
                             hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
-// Blocks of more than 16 rows with the chain mask (mask NULL): 64-row tiles, the key blocks staged in LDS;
+// Blocks of more than kAttnSplitRows rows with the chain mask (mask NULL): 64-row tiles, the key blocks staged in LDS;
 // plan, splits, per_split, cols, part and counter are not used.  bf16 with heads of 64 or 128 columns,
 // float with 64 (attention_rows_supported)
 inline bool attention_rows_supported(int dtype, int head_dim) { return head_dim == 64 || (dtype == 1 && head_dim == 128); }

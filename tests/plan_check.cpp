@@ -59,7 +59,7 @@ int main() {
                     CHECK(p.grid == B * c.H * p.row_tiles * p.splits * p.cols && p.splits >= 1 && p.waves >= 1 &&
                               p.per_split >= 1 && (long)p.splits * p.per_split * 32 >= std::min(S, len + q),
                           "attention plan shape: B %d q %d len %d", B, q, len);
-                    if (q <= 16) {
+                    if (q <= kAttnSplitRows) {
                         CHECK(p.per_split == ref.per_split && p.waves == ref.waves,
                               "key partition varies with the block: B %d q %d len %d (%d/%d waves %d/%d)", B, q, len,
                               p.per_split, ref.per_split, p.waves, ref.waves);

@@ -43,7 +43,8 @@ def test_teacher_forced_k0_and_k10():
 
 
 @pytest.mark.parametrize("dtype,k,prompt_len", [("bf16", 5, 318), ("bf16", 10, 254), ("fp32", 5, 189),
-                                                 ("bf16", 5, 40), ("bf16", 10, 1625)])
+                                                 ("bf16", 5, 40), ("bf16", 10, 1625), ("bf16", 20, 318),
+                                                 ("fp32", 40, 189), ("bf16", 63, 700)])
 def test_block_rows_bitwise_equal_single_token_steps(dtype, k, prompt_len):
     """A token's logits do not depend on how many draft rows share its block (Section 2.1,
     Eq. 1-3 compare a block's predictions with autoregressive ones): row r of a (k+1)-row
@@ -51,7 +52,8 @@ def test_block_rows_bitwise_equal_single_token_steps(dtype, k, prompt_len):
     after rows 0..r-1 were committed one at a time.  The block spans a 32-key block and a
     key-split boundary, with several key splits per head.  At the 1625-token prompt a key
     partition sized from the current length plus the block size (51 vs 52 key blocks in 3
-    splits) would give the block and the single-token steps different split boundaries."""
+    splits) would give the block and the single-token steps different split boundaries.  Blocks
+    of 21, 41 and 64 rows span two to four 16-row tiles, each with the same key splits."""
     if dtype == "bf16":
         shape = synth.small_shape(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=688, vocab=1000,
                                   n_adaptive=10, rope_base=1e6, dtype="bf16")
