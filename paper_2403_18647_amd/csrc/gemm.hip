@@ -21,9 +21,11 @@
 //    type at the matrix-core input.  Both give the normalised activation a bf16
 //    model stores, rounded once, bit for bit the same.
 //  * Residual GEMMs whose tile count would leave some compute units a second
-//    workgroup (13B: 320 tiles on 256 units) spread each tile's waves over
-//    several workgroups and fold the waves' partial tiles in a second kernel,
-//    in the same wave order (plan_gemm_resid).
+//    workgroup (13B: 320 tiles on 256 units), and long narrow ones of blocks of
+//    several row tiles (four tiles per workgroup, so each row byte read feeds
+//    four), spread each tile's waves over several workgroups and fold the
+//    waves' partial tiles in a second kernel, in the same wave order
+//    (plan_gemm_resid).
 //  * Fused epilogues, run by wave 0 on the reduced tile:
 //      EP_STORE   float output (LM-head logits)
 //      EP_QKV     RoPE on Q and K columns, Q (float) to its buffer, K and V into
@@ -127,8 +129,21 @@ GemmPlan plan_gemm(int M, int n_tiles, int k_steps) {
 // so the results are the same bit for bit.  Measured at 13B, 11 rows: down
 // (432 contraction steps) 39.4 -> 32.6 us; O (160 steps) 16.6 -> 17.1 us, its
 // waves' work too short to cover the fold kernel's launch, so it stays whole.
+// Blocks of several row tiles re-read all of their rows in every workgroup (L2 hits, but at batch
+// 4 x 6 rows the down GEMM's 528 KB of rows per workgroup outweigh its 352 KB of weights).  A narrow
+// residual GEMM with a long contraction then takes four column tiles per workgroup, so each row byte
+// feeds four tiles, and spreads each tile's wave slices over one-wave workgroups (same slices, same
+// fold order: the same values).
 GemmPlan plan_gemm_resid(int M, int n_tiles, int k_steps) {
     GemmPlan p = plan_gemm(M, n_tiles, k_steps);
+    if (p.mt > 1 && p.ntw == 1 && n_tiles <= 512 && k_steps >= 256) {
+        p.ntw = 4;
+        p.ksplit = p.waves;
+        p.waves = 1;
+        p.grid = (n_tiles + p.ntw - 1) / p.ntw * p.ksplit;
+        p.lds_bytes = p.waves * p.mt * 64 * 16;
+        return p;
+    }
     if (p.ntw != 1 || n_tiles <= 256 || k_steps < 256) return p;
     auto spread = [&](int k) {   // workgroup rounds over the average, per compute unit
         const long n = (long)n_tiles * k;
@@ -326,10 +341,12 @@ __global__ void __launch_bounds__(NTW > 1 ? 256 : 512) gemm_kernel(GemmArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int c = lane & 15, g = lane >> 4;
     const int M = a.M;
-    // a split residual GEMM: workgroup (kpart, tile) holds waves kpart * nw .. of the tile's nwt
-    const bool split = EP == EP_RESID && NTW == 1 && a.ksplit > 1;
-    const int kpart = split ? (int)blockIdx.x / a.n_tiles : 0;
-    const int tile0 = split ? (int)blockIdx.x - kpart * a.n_tiles : (int)blockIdx.x * NTW;
+    // a split residual GEMM: workgroup (kpart, group of NTW tiles) holds waves kpart * nw .. of each
+    // of its tiles' nwt
+    const bool split = EP == EP_RESID && a.ksplit > 1;
+    const int n_groups = (a.n_tiles + NTW - 1) / NTW;
+    const int kpart = split ? (int)blockIdx.x / n_groups : 0;
+    const int tile0 = ((int)blockIdx.x - kpart * n_groups) * NTW;
     const int nwt = split ? nw * a.ksplit : nw;
     const int gw = kpart * nw + wave;
 
@@ -461,10 +478,14 @@ __global__ void __launch_bounds__(NTW > 1 ? 256 : 512) gemm_kernel(GemmArgs a) {
         if (s + 3 * U < nks) mma_batch<T, XF, XT, MT, NTW, U>(acc, w1, x1, inv);
     }
 
-    if (split) {   // raw partial tile of this wave, folded by gemm_fold_kernel
-        f32x4_t* pp = reinterpret_cast<f32x4_t*>(a.part) + ((size_t)tile0 * nwt + gw) * MT * 64 + lane;
+    if (split) {   // raw partial tiles of this wave, folded by gemm_fold_kernel
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) pp[mt * 64] = acc[0][mt];
+        for (int j = 0; j < NTW; ++j) {
+            if (tile0 + j >= a.n_tiles) break;
+            f32x4_t* pp = reinterpret_cast<f32x4_t*>(a.part) + ((size_t)(tile0 + j) * nwt + gw) * MT * 64 + lane;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) pp[mt * 64] = acc[j][mt];
+        }
         return;
     }
 
@@ -519,7 +540,8 @@ static hipError_t launch_mt(const GemmPlan& p, const GemmArgs& a, hipStream_t s,
     const dim3 grid(p.grid), block(64 * p.waves);
     if (p.waves > (p.ntw > 1 ? 4 : 8)) return hipErrorInvalidValue;
     const bool split = p.ksplit > 1;
-    if (split && (EP != EP_RESID || p.ntw != 1 || !a.part || a.ksplit != p.ksplit || p.grid != a.n_tiles * p.ksplit))
+    if (split && (EP != EP_RESID || !a.part || a.ksplit != p.ksplit ||
+                  p.grid != (a.n_tiles + p.ntw - 1) / p.ntw * p.ksplit))
         return hipErrorInvalidValue;
     if (!split && a.ksplit > 1) return hipErrorInvalidValue;
     auto go = [&](auto kernel) {
