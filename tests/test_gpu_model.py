@@ -44,7 +44,8 @@ def test_teacher_forced_k0_and_k10():
 
 @pytest.mark.parametrize("dtype,k,prompt_len", [("bf16", 5, 318), ("bf16", 10, 254), ("fp32", 5, 189),
                                                  ("bf16", 5, 40), ("bf16", 10, 1625), ("bf16", 20, 318),
-                                                 ("fp32", 40, 189), ("bf16", 63, 700)])
+                                                 ("fp32", 40, 189), ("bf16", 63, 700), ("bf16_ffn8192", 20, 300),
+                                                 ("bf16_ffn8192", 40, 300)])
 def test_block_rows_bitwise_equal_single_token_steps(dtype, k, prompt_len):
     """A token's logits do not depend on how many draft rows share its block (Section 2.1,
     Eq. 1-3 compare a block's predictions with autoregressive ones): row r of a (k+1)-row
@@ -53,8 +54,14 @@ def test_block_rows_bitwise_equal_single_token_steps(dtype, k, prompt_len):
     key-split boundary, with several key splits per head.  At the 1625-token prompt a key
     partition sized from the current length plus the block size (51 vs 52 key blocks in 3
     splits) would give the block and the single-token steps different split boundaries.  Blocks
-    of 21, 41 and 64 rows span two to four 16-row tiles, each with the same key splits."""
-    if dtype == "bf16":
+    of 21, 41 and 64 rows span two to four 16-row tiles, each with the same key splits.  With an
+    FFN of 8192 (256 contraction steps) the down GEMM of a block of several row tiles takes four
+    column tiles per one-wave workgroup and folds its 8 wave slices in a second kernel, while a
+    single token's takes one 8-wave workgroup: the same slices summed in the same order."""
+    if dtype == "bf16_ffn8192":
+        shape = synth.small_shape(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=8192, vocab=1000,
+                                  n_adaptive=10, rope_base=1e6, dtype="bf16")
+    elif dtype == "bf16":
         shape = synth.small_shape(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=688, vocab=1000,
                                   n_adaptive=10, rope_base=1e6, dtype="bf16")
     else:
